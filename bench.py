@@ -1,0 +1,179 @@
+"""Benchmark: effective TFLOP/s (nonzero blocks) of factorized sparse attention,
+forward + backward with recomputation, on one MI355X.
+
+One step = forward and backward over each of the two measured workloads:
+  strided, n = 12,288, l = 128, B = 64, batch 2, 8 merged heads of 64
+  fixed,   n = 65,536, l = 256, c = 32, B = 64, batch 1, 8 merged heads of 64
+Inputs are seeded N(0, 1) bf16 tensors already resident in device memory; the
+block layouts are built once before timing.  Every present B x B block is
+credited 14 B^2 d FLOPs per (batch, head): 4 B^2 d forward (QK^T, PV) and
+10 B^2 d backward (QK^T recomputed, dO V^T, P^T dO, dS^T Q, dS K).
+
+Prints one JSON line.  The fp64 oracle is timed on the host cores on one
+(batch, head) slice of each workload and scaled to the whole step.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective TFLOP/s (nonzero blocks) fwd+bwd and % bf16 MFMA peak at n=12288/65536"
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+HBM_PEAK_GBS = 8000.0
+BENCH_WORKLOADS = ("strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged")
+
+
+def credited_flops(w, nnz):
+    """14 B^2 d per present block per (batch, head); interleaved heads split the layouts."""
+    heads_per_layout = [w.heads] if len(nnz) == 1 else [(w.heads + 1) // 2, w.heads // 2]
+    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout))
+    return 14.0 * w.block * w.block * w.d_head * blocks, 4.0 * w.block * w.block * w.d_head * blocks
+
+
+def algorithmic_bwd_bytes(w):
+    """Backward call: read Q, K, V, O, dO, LSE; write dQ, dK, dV; D written and read."""
+    e = w.batch * w.heads * w.n
+    return 8 * e * w.d_head * 2 + 3 * e * 4
+
+
+def cpu_baseline(workloads, inputs):
+    """Time the fp64 oracle on one (batch, head) slice of each workload, full
+    sequence, and scale by batch * heads to the whole step."""
+    from oracle import oracle
+    from paper_1904_10509_amd.inputs import as_oracle_array
+
+    est_s, credited, parts = 0.0, 0.0, []
+    for w, nnz, x in workloads:
+        sl = [as_oracle_array(x[name][:1, :1]) for name in ("q", "k", "v", "dout")]
+        t0 = time.perf_counter()
+        oracle.backward(*sl, pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
+        dt = time.perf_counter() - t0
+        est_s += dt * w.batch * w.heads
+        credited += credited_flops(w, nnz)[0]
+        parts.append(f"{w.name}: 1 of {w.batch * w.heads} (batch, head) slices in {dt:.2f} s")
+    return {
+        "value": credited / est_s / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": "; ".join(parts) + "; full fwd+bwd (the oracle's backward recomputes its forward),"
+                  " time scaled by batch*heads",
+        "est_step_s": est_s,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the sharding design note); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_1904_10509_amd import sparse_attn as sa
+    from paper_1904_10509_amd.inputs import WORKLOADS, workload_inputs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    runs = []
+    for name in BENCH_WORKLOADS:
+        w = WORKLOADS[name]
+        x = workload_inputs(w)
+        lay = sa.build_layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode, device=dev)
+        q, k, v, dout = (x[n_].to(dev) for n_ in ("q", "k", "v", "dout"))
+        o = torch.empty_like(q)
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=dev)
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+        need = sa.sparse_attn_bwd_workspace_size(*lay.pattern_args, w.batch, w.heads, w.d_head, sa.SA_BF16)
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        runs.append(dict(w=w, x=x, lay=lay, q=q, k=k, v=v, dout=dout, o=o, lse=lse, grads=grads, ws=ws))
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        for idx, r in enumerate(runs):
+            if events is not None:
+                events[idx][0].record(stream)
+            sa.forward(r["q"], r["k"], r["v"], r["lay"], r["w"].scale, out=r["o"], lse=r["lse"])
+            if events is not None:
+                events[idx][1].record(stream)
+            sa.backward(r["q"], r["k"], r["v"], r["o"], r["dout"], r["lse"], r["lay"], r["w"].scale,
+                        grads=r["grads"], workspace=r["ws"])
+            if events is not None:
+                events[idx][2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in runs] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    per = {}
+    total_credited = 0.0
+    fwd_ms_all, bwd_ms_all = [], []
+    for idx, r in enumerate(runs):
+        w = r["w"]
+        fwd_ms = sum(ev[s][idx][0].elapsed_time(ev[s][idx][1]) for s in range(args.steps)) / args.steps
+        bwd_ms = sum(ev[s][idx][1].elapsed_time(ev[s][idx][2]) for s in range(args.steps)) / args.steps
+        cred, cred_fwd = credited_flops(w, r["lay"].nnz)
+        total_credited += cred
+        fwd_ms_all.append(fwd_ms)
+        bwd_ms_all.append(bwd_ms)
+        per[w.name] = {
+            "n": w.n, "nnz_blocks": r["lay"].nnz, "credited_flop": cred,
+            "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+            "fwd_tflops": cred_fwd / (fwd_ms * 1e-3) / 1e12,
+            "bwd_tflops": (cred - cred_fwd) / (bwd_ms * 1e-3) / 1e12,
+            "fwd_bwd_tflops": cred / ((fwd_ms + bwd_ms) * 1e-3) / 1e12,
+            "pct_bf16_peak": 100 * cred / ((fwd_ms + bwd_ms) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        }
+    ms_per_step = wall * 1e3 / args.steps
+    value = total_credited / (ms_per_step * 1e-3) / 1e12
+
+    # roofline of the dominant call: the backward of the largest workload
+    dom = max(range(len(runs)), key=lambda i: bwd_ms_all[i])
+    dw = runs[dom]["w"]
+    cred, cred_fwd = credited_flops(dw, runs[dom]["lay"].nnz)
+    achieved = (cred - cred_fwd) / (bwd_ms_all[dom] * 1e-3) / 1e12
+    roofline = {
+        "kernel": f"sparse_attn_bwd on {dw.name} (bwd_pre + bwd_dkdv_bf16 + bwd_dq_convert launches)",
+        "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+        "avg_ms": bwd_ms_all[dom], "algorithmic_bytes": algorithmic_bwd_bytes(dw),
+    }
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": " + ".join(BENCH_WORKLOADS),
+                   "workloads": {r["w"].name: r["w"].describe() for r in runs}},
+        "pct_bf16_peak": 100 * value / PEAK_BF16_TFLOPS,
+        "per_workload": per,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline([(r["w"], r["lay"].nnz, r["x"]) for r in runs], None)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,176 @@
+/*
+ * sparse_attn.h -- C ABI of the MI355X (gfx950) factorized sparse attention
+ * library.
+ *
+ * The operation is the attend function of Child et al. (2019), Sec. 4.2
+ * (eq. attend_fn): for every position i,
+ *     O_i = softmax_j( scale * q_i . k_j )  V_j     over j in S_i,
+ * with S_i one of the factorized connectivity patterns of Sec. 4.3, combined
+ * over heads as in Sec. 5.1, plus its gradient for training.  The forward
+ * saves one log-sum-exp per row so that the backward recomputes the attention
+ * weights instead of storing them (Sec. 5.4).  Work is done in B x B blocks of
+ * the attention matrix, and blocks above the diagonal are never visited
+ * (Sec. 5.5).
+ *
+ * Positions are 0-based.  With stride l and summary width c:
+ *   strided A1 = { max(0, i-l), ..., i }                  (l + 1 positions)
+ *   strided A2 = { j <= i : (i - j) mod l == 0 }
+ *   fixed   A1 = { j <= i : floor(j / l) == floor(i / l) }
+ *   fixed   A2 = { j <= i : j mod l >= l - c }             (1 <= c <= l)
+ * A row whose set is empty (fixed A2 alone, first block) yields O_i = 0,
+ * LSE_i = -inf and no gradient.
+ *
+ * Conventions for every entry point:
+ *   - All functions are extern "C"; no C++ or PyTorch type crosses the ABI.
+ *   - Device pointers point to memory allocated by the caller; the library
+ *     allocates no device memory and keeps no mutable global state.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device work is enqueued asynchronously; nothing synchronizes.
+ *   - Every argument is validated before anything is enqueued.  On error a
+ *     negative sa_status is returned and no work is enqueued.  After the
+ *     launches, a HIP launch error is reported as SA_ERR_HIP.  The library
+ *     never prints and never aborts.
+ *   - Tensors Q, K, V, O, dO, dQ, dK, dV are [batch, heads, n, d_head] with d
+ *     contiguous and the same element strides (batch, head, sequence) for all;
+ *     the sequence stride must be >= d_head and every base address 16-byte
+ *     aligned, every stride a multiple of 8 elements.  LSE is [batch, heads, n]
+ *     contiguous fp32 (natural logarithm).
+ */
+#ifndef SPARSE_ATTN_H
+#define SPARSE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SA_OK = 0,
+    SA_ERR_INVALID = -1,          /* an argument is out of range or NULL */
+    SA_ERR_UNSUPPORTED = -2,      /* valid request this build does not implement */
+    SA_ERR_BUFFER_TOO_SMALL = -3, /* a caller buffer is smaller than required */
+    SA_ERR_HIP = -4               /* the HIP runtime reported an error */
+} sa_status;
+
+/* Connectivity pattern, Sec. 4.3. */
+typedef enum { SA_STRIDED = 0, SA_FIXED = 1 } sa_pattern;
+
+/* Head combination, Sec. 5.1:
+ *   SA_MODE_A1 / SA_MODE_A2: one factor for the whole call (eq. sepwpmat: a
+ *       residual block r uses factor r mod 2, so a call picks one of them);
+ *   SA_MODE_MERGED: every head attends to A1 u A2 (eq. mergedmat);
+ *   SA_MODE_INTERLEAVED: multi-head attention whose heads alternate the
+ *       factors, head h using A1 when h is even and A2 when h is odd. */
+typedef enum {
+    SA_MODE_A1 = 0,
+    SA_MODE_A2 = 1,
+    SA_MODE_MERGED = 2,
+    SA_MODE_INTERLEAVED = 3
+} sa_head_mode;
+
+/* Element type of Q, K, V, O, dO, dQ, dK, dV.  Products accumulate in fp32. */
+typedef enum { SA_F32 = 0, SA_BF16 = 1 } sa_dtype;
+
+/* Tile kinds stored in the layout. */
+enum { SA_TILE_FULL = 0, SA_TILE_MASKED = 1 };
+
+/*
+ * Pattern arguments shared by all entry points:
+ *   n          sequence length, 1 <= n < 2^31, a multiple of `block`
+ *   block      tile edge B in {16, 32, 64}
+ *   stride_l   l >= 1 (Sec. 4.3); any l >= n makes A1 dense causal
+ *   summary_c  c: 1 <= c <= l for SA_FIXED, must be 0 for SA_STRIDED
+ *   pattern    sa_pattern
+ *   head_mode  sa_head_mode
+ */
+
+/*
+ * Size query for the block layout (host only, synchronous, no device work).
+ * Sec. 5.5: the product is computed over B x B blocks; a block (qb, kb) with
+ * kb <= qb is present when any pair (i, j) in it is attended.
+ * Outputs: *n_layouts = 2 for SA_MODE_INTERLEAVED (layout 0 holds A1, layout
+ * 1 holds A2), else 1; nnz[0..1] = present blocks per layout (nnz[1] = 0 when
+ * there is one layout).  Each layout needs nq + 1 row and column pointers,
+ * nq = n / block.
+ */
+int sparse_attn_layout_size(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                            int32_t pattern, int32_t head_mode, int32_t* n_layouts,
+                            int64_t* nnz);
+
+/*
+ * Build the block layout on the device (asynchronous on `stream`).
+ * All output arrays are device memory owned by the caller:
+ *   row_ptr [n_layouts * (nq + 1)]  int32, absolute offsets: layout g's rows are
+ *                                   row_ptr[g*(nq+1) + qb] .. row_ptr[g*(nq+1)+qb+1]
+ *   col_idx [nnz_total]             int32 key block of each present block,
+ *                                   strictly ascending within a row
+ *   kind    [nnz_total]             uint8 SA_TILE_FULL when all B*B pairs are
+ *                                   attended, else SA_TILE_MASKED
+ *   col_ptr [n_layouts * (nq + 1)]  int32, the same blocks grouped by key block
+ *   row_idx [nnz_total]             int32 query block, strictly ascending
+ *   kind_t  [nnz_total]             uint8 kind of each entry in column order
+ * `capacity` is the caller's element count of col_idx / kind / row_idx /
+ * kind_t; SA_ERR_BUFFER_TOO_SMALL when below the total from the size query.
+ */
+int sparse_attn_layout(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                       int32_t pattern, int32_t head_mode, int32_t* row_ptr, int32_t* col_idx,
+                       uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
+                       int64_t capacity, void* stream);
+
+/*
+ * Forward (Sec. 4.2 eq. attend_fn over the sets of Sec. 4.3 / 5.1).
+ *   row_ptr, col_idx, kind   the layout built for the same pattern arguments
+ *   batch, heads             >= 1
+ *   d_head                   in {32, 64, 128}
+ *   dtype                    sa_dtype of q, k, v and o
+ *   q, k, v                  device inputs, [batch, heads, n, d_head]
+ *   strides                  host array {batch, head, sequence} in elements
+ *   softmax_scale            multiplies q . k (the paper uses 1/sqrt(d_head))
+ *   o                        device output, same shape and strides as q
+ *   lse                      device output [batch, heads, n] fp32:
+ *                            log sum_j exp(scale q_i . k_j), -inf for empty rows
+ */
+int sparse_attn_fwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                    int32_t pattern, int32_t head_mode, const int32_t* row_ptr,
+                    const int32_t* col_idx, const uint8_t* kind, int32_t batch, int32_t heads,
+                    int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                    const int64_t* strides, float softmax_scale, void* o, float* lse,
+                    void* stream);
+
+/*
+ * Bytes of device workspace that sparse_attn_bwd needs (host only).
+ */
+int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
+                                   int32_t summary_c, int32_t pattern, int32_t head_mode,
+                                   int32_t batch, int32_t heads, int32_t d_head, int32_t dtype,
+                                   size_t* bytes);
+
+/*
+ * Backward with recomputation (Sec. 5.4): gradients of a loss L with
+ * dL/dO = dout, given the forward's o and lse.  The attention weights are
+ * recomputed blockwise as exp(scale q_i . k_j - LSE_i); nothing of size
+ * n x n is stored.  Layout arguments as in the forward plus the column view
+ * (col_ptr, row_idx, kind_t).  dq, dk, dv are device outputs with the
+ * strides of q.  workspace is caller-owned device memory of at least
+ * sparse_attn_bwd_workspace_size bytes (SA_ERR_BUFFER_TOO_SMALL otherwise);
+ * its contents on entry are ignored.
+ */
+int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                    int32_t pattern, int32_t head_mode, const int32_t* row_ptr,
+                    const int32_t* col_idx, const uint8_t* kind, const int32_t* col_ptr,
+                    const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                    int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                    const void* v, const void* o, const void* dout, const float* lse,
+                    const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static English description of a status code. */
+const char* sparse_attn_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSE_ATTN_H */

@@ -1,0 +1,204 @@
+// C ABI (include/sparse_attn.h): argument validation, launch configuration and
+// status codes.  Nothing is enqueued unless every argument is valid.
+#include <math.h>
+
+#include "../../include/sparse_attn.h"
+#include "sa_internal.h"
+
+namespace {
+
+using sa::Pattern;
+
+struct PatternArgs {
+    int64_t n;
+    int32_t block, l, c, pattern, mode;
+    int64_t nq;
+    int n_layouts;
+};
+
+int check_pattern(int64_t n, int32_t block, int32_t l, int32_t c, int32_t pattern, int32_t mode,
+                  PatternArgs* out) {
+    if (block != 16 && block != 32 && block != 64) return SA_ERR_INVALID;
+    if (n < 1 || n > INT32_MAX || n % block != 0) return SA_ERR_INVALID;
+    if (l < 1) return SA_ERR_INVALID;
+    if (pattern != SA_STRIDED && pattern != SA_FIXED) return SA_ERR_INVALID;
+    if (mode < SA_MODE_A1 || mode > SA_MODE_INTERLEAVED) return SA_ERR_INVALID;
+    if (pattern == SA_FIXED && (c < 1 || c > l)) return SA_ERR_INVALID;
+    if (pattern == SA_STRIDED && c != 0) return SA_ERR_INVALID;
+    out->n = n;
+    out->block = block;
+    out->l = l;
+    out->c = c;
+    out->pattern = pattern;
+    out->mode = mode;
+    out->nq = n / block;
+    out->n_layouts = mode == SA_MODE_INTERLEAVED ? 2 : 1;
+    return SA_OK;
+}
+
+Pattern pattern_of_layout(const PatternArgs& p, int g) {
+    Pattern s;
+    s.pattern = p.pattern;
+    s.part = sa::part_of_layout(p.mode, g);
+    s.l = p.l;
+    s.c = p.c;
+    return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_tensor_args(const PatternArgs& p, int32_t batch, int32_t heads, int32_t d, int32_t dtype,
+                      const int64_t* strides) {
+    if (batch < 1 || heads < 1) return SA_ERR_INVALID;
+    if (dtype != SA_F32 && dtype != SA_BF16) return SA_ERR_INVALID;
+    if (d != 32 && d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
+    if (!strides) return SA_ERR_INVALID;
+    const int64_t unit = dtype == SA_BF16 ? 8 : 4;  // elements per 16 bytes
+    for (int t = 0; t < 3; ++t)
+        if (strides[t] < 0 || strides[t] % unit != 0) return SA_ERR_INVALID;
+    if (strides[2] < d) return SA_ERR_INVALID;
+    if ((int64_t)batch * heads > INT32_MAX / 2) return SA_ERR_INVALID;
+    return SA_OK;
+}
+
+sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32_t d,
+                       const int64_t* strides, float scale, const int32_t* row_ptr,
+                       const int32_t* col_idx, const uint8_t* kind, const int32_t* col_ptr,
+                       const int32_t* row_idx, const uint8_t* kind_t) {
+    sa::AttnArgs a;
+    a.pattern = p.pattern;
+    a.mode = p.mode;
+    a.l = p.l;
+    a.c = p.c;
+    a.n = (int32_t)p.n;
+    a.nq = (int32_t)p.nq;
+    a.block = p.block;
+    a.batch = batch;
+    a.heads = heads;
+    a.d = d;
+    a.sb = strides[0];
+    a.sh = strides[1];
+    a.ss = strides[2];
+    a.scale = scale;
+    a.scale_log2 = scale * sa::kLog2eHost;
+    a.row_ptr = row_ptr;
+    a.col_idx = col_idx;
+    a.kind = kind;
+    a.col_ptr = col_ptr;
+    a.row_idx = row_idx;
+    a.kind_t = kind_t;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sparse_attn_layout_size(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                            int32_t pattern, int32_t head_mode, int32_t* n_layouts,
+                            int64_t* nnz) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    if (!n_layouts || !nnz) return SA_ERR_INVALID;
+    int64_t counts[2] = {0, 0};
+    for (int g = 0; g < p.n_layouts; ++g) counts[g] = sa::layout_count_host(pattern_of_layout(p, g), n, block);
+    if (counts[0] + counts[1] > INT32_MAX) return SA_ERR_UNSUPPORTED;  // int32 layout indices
+    *n_layouts = p.n_layouts;
+    nnz[0] = counts[0];
+    nnz[1] = counts[1];
+    return SA_OK;
+}
+
+int sparse_attn_layout(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                       int32_t pattern, int32_t head_mode, int32_t* row_ptr, int32_t* col_idx,
+                       uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
+                       int64_t capacity, void* stream) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
+    int64_t total = 0;
+    for (int g = 0; g < p.n_layouts; ++g) total += sa::layout_count_host(pattern_of_layout(p, g), n, block);
+    if (total > INT32_MAX) return SA_ERR_UNSUPPORTED;
+    if (capacity < total) return SA_ERR_BUFFER_TOO_SMALL;
+    hipError_t e = sa::layout_launch(n, block, pattern, head_mode, stride_l, summary_c, p.n_layouts,
+                                     row_ptr, col_idx, kind, col_ptr, row_idx, kind_t,
+                                     static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+int sparse_attn_fwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                    int32_t pattern, int32_t head_mode, const int32_t* row_ptr,
+                    const int32_t* col_idx, const uint8_t* kind, int32_t batch, int32_t heads,
+                    int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                    const int64_t* strides, float softmax_scale, void* o, float* lse,
+                    void* stream) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    st = check_tensor_args(p, batch, heads, d_head, dtype, strides);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !q || !k || !v || !o || !lse) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale)) return SA_ERR_INVALID;
+    sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,
+                               kind, nullptr, nullptr, nullptr);
+    hipError_t e = sa::fwd_launch(a, dtype, q, k, v, o, lse, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
+                                   int32_t summary_c, int32_t pattern, int32_t head_mode,
+                                   int32_t batch, int32_t heads, int32_t d_head, int32_t dtype,
+                                   size_t* bytes) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    if (batch < 1 || heads < 1 || (dtype != SA_F32 && dtype != SA_BF16) || !bytes) return SA_ERR_INVALID;
+    if (d_head != 32 && d_head != 64 && d_head != 128) return SA_ERR_UNSUPPORTED;
+    *bytes = sa::bwd_workspace_bytes(batch, heads, n, d_head, dtype);
+    return SA_OK;
+}
+
+int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
+                    int32_t pattern, int32_t head_mode, const int32_t* row_ptr,
+                    const int32_t* col_idx, const uint8_t* kind, const int32_t* col_ptr,
+                    const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                    int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                    const void* v, const void* o, const void* dout, const float* lse,
+                    const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    st = check_tensor_args(p, batch, heads, d_head, dtype, strides);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
+    if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale)) return SA_ERR_INVALID;
+    const size_t need = sa::bwd_workspace_bytes(batch, heads, n, d_head, dtype);
+    if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
+    if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;
+    sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,
+                               kind, col_ptr, row_idx, kind_t);
+    hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
+                                  static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+const char* sparse_attn_status_string(int status) {
+    switch (status) {
+    case SA_OK: return "success";
+    case SA_ERR_INVALID: return "invalid argument";
+    case SA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SA_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case SA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

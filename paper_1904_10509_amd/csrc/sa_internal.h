@@ -1,0 +1,50 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "sa_pattern.h"
+
+namespace sa {
+
+constexpr float kLog2eHost = 1.4426950408889634f;
+
+// Present blocks of one layout, counted on the host with the O(1) test.
+int64_t layout_count_host(const Pattern& p, int64_t n, int64_t B);
+
+hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode, int64_t l,
+                         int64_t c, int n_layouts, int32_t* row_ptr, int32_t* col_idx,
+                         uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
+                         hipStream_t stream);
+
+// Everything a kernel needs to know about one call.
+struct AttnArgs {
+    int32_t pattern, mode;
+    int32_t l, c;          // validated to fit in 32 bits
+    int32_t n, nq, block;  // n < 2^31
+    int32_t batch, heads, d;
+    int64_t sb, sh, ss;    // element strides: batch, head, sequence
+    float scale;           // softmax scale
+    float scale_log2;      // scale * log2(e)
+    const int32_t* row_ptr;
+    const int32_t* col_idx;
+    const uint8_t* kind;
+    const int32_t* col_ptr;
+    const int32_t* row_idx;
+    const uint8_t* kind_t;
+};
+
+// Forward.  q, k, v, o use the strides in `a`; lse is [batch, heads, n].
+hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
+                      void* o, float* lse, hipStream_t stream);
+
+// Backward workspace: fp32 dq accumulator [b, h, n, d] and D [b, h, n].
+size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype);
+
+hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
+                      const void* o, const void* dout, const float* lse, void* dq, void* dk,
+                      void* dv, void* workspace, hipStream_t stream);
+
+}  // namespace sa

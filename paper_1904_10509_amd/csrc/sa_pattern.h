@@ -1,0 +1,122 @@
+// Pattern math of the library (host and device): block presence in O(1),
+// attended-pair counts over a column range in O(1), and the element predicate
+// used to mask partial blocks.  Sets are those of Sec. 4.3 (0-based, causal);
+// the closed forms below are derived from them.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sa {
+
+enum { STRIDED = 0, FIXED = 1 };
+enum { MODE_A1 = 0, MODE_A2 = 1, MODE_MERGED = 2, MODE_INTERLEAVED = 3 };
+enum { PART_A1 = 0, PART_A2 = 1, PART_MERGED = 2 };
+enum { TILE_FULL = 0, TILE_MASKED = 1 };
+
+struct Pattern {
+    int32_t pattern;  // STRIDED or FIXED
+    int32_t part;     // PART_A1, PART_A2 or PART_MERGED
+    int64_t l;        // stride
+    int64_t c;        // summary width (fixed pattern)
+};
+
+// Factor a head uses (Sec. 5.1).
+__host__ __device__ inline int part_of_head(int mode, int h) {
+    if (mode == MODE_INTERLEAVED) return (h & 1) ? PART_A2 : PART_A1;
+    return mode == MODE_A1 ? PART_A1 : (mode == MODE_A2 ? PART_A2 : PART_MERGED);
+}
+
+// Part held by layout g.
+__host__ __device__ inline int part_of_layout(int mode, int g) {
+    if (mode == MODE_INTERLEAVED) return g == 0 ? PART_A1 : PART_A2;
+    return part_of_head(mode, 0);
+}
+
+__host__ __device__ inline int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+__host__ __device__ inline int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+
+// First fixed-pattern summary column >= x (x >= 0).
+__host__ __device__ inline int64_t first_summary_at_or_after(int64_t x, int64_t l, int64_t c) {
+    int64_t r = x % l;
+    return r >= l - c ? x : x - r + (l - c);
+}
+
+// Is any pair of the block rows [r0, r1] x columns [c0, c1] attended?  The
+// caller guarantees c0 <= r1 (blocks on or below the diagonal).
+__host__ __device__ inline bool block_present_part(int pattern, int part, int64_t l, int64_t c,
+                                                   int64_t r0, int64_t r1, int64_t c0, int64_t c1) {
+    if (pattern == STRIDED) {
+        int64_t dmin = r0 - c1, dmax = r1 - c0;  // every difference i - j in between occurs
+        if (part == PART_A1) return dmin <= l;
+        // a multiple of l in [max(0, dmin), dmax]
+        return (dmax / l) * l >= max64(0, dmin);
+    }
+    if (part == PART_A1) {
+        // some l-block meets both the rows and the columns
+        return max64(r0 / l, c0 / l) <= min64(r1 / l, c1 / l);
+    }
+    return first_summary_at_or_after(c0, l, c) <= min64(c1, r1);
+}
+
+__host__ __device__ inline bool block_present(const Pattern& p, int64_t r0, int64_t r1, int64_t c0,
+                                              int64_t c1) {
+    if (p.part == PART_MERGED)
+        return block_present_part(p.pattern, PART_A1, p.l, p.c, r0, r1, c0, c1) ||
+               block_present_part(p.pattern, PART_A2, p.l, p.c, r0, r1, c0, c1);
+    return block_present_part(p.pattern, p.part, p.l, p.c, r0, r1, c0, c1);
+}
+
+// Number of integers in [lo, hi].
+__host__ __device__ inline int64_t span(int64_t lo, int64_t hi) { return hi >= lo ? hi - lo + 1 : 0; }
+
+// Number of j in [lo, hi] with j = i - k*l, k >= 0 (0 <= lo, hi <= i).
+__host__ __device__ inline int64_t strided_hits(int64_t i, int64_t l, int64_t lo, int64_t hi) {
+    if (hi < lo) return 0;
+    int64_t kmax = (i - lo) / l;
+    int64_t kmin = (i - hi + l - 1) / l;
+    return kmax >= kmin ? kmax - kmin + 1 : 0;
+}
+
+// Number of summary columns in [0, x] (x >= -1).
+__host__ __device__ inline int64_t summary_upto(int64_t x, int64_t l, int64_t c) {
+    int64_t m = x + 1;
+    return (m / l) * c + max64(0, m % l - (l - c));
+}
+
+// |S_i intersected with [lo, hi]| for one part (lo >= 0).
+__host__ __device__ inline int64_t attended_in_range(const Pattern& p, int64_t i, int64_t lo,
+                                                     int64_t hi) {
+    hi = min64(hi, i);
+    if (hi < lo) return 0;
+    if (p.pattern == STRIDED) {
+        int64_t band = span(max64(lo, i - p.l), hi);
+        if (p.part == PART_A1) return band;
+        if (p.part == PART_A2) return strided_hits(i, p.l, lo, hi);
+        return band + strided_hits(i, p.l, lo, min64(hi, i - p.l - 1));
+    }
+    int64_t blk0 = (i / p.l) * p.l;
+    int64_t own = span(max64(lo, blk0), hi);
+    if (p.part == PART_A1) return own;
+    if (p.part == PART_A2) return summary_upto(hi, p.l, p.c) - summary_upto(lo - 1, p.l, p.c);
+    int64_t hi2 = min64(hi, blk0 - 1);
+    int64_t earlier = hi2 >= lo ? summary_upto(hi2, p.l, p.c) - summary_upto(lo - 1, p.l, p.c) : 0;
+    return own + earlier;
+}
+
+// Element predicate in 32-bit arithmetic (0 <= i, j < 2^31).
+__host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32_t c, int32_t i,
+                                         int32_t j) {
+    if (j > i) return false;
+    if (pattern == STRIDED) {
+        int32_t d = i - j;
+        bool a1 = d <= l;
+        bool a2 = (d % l) == 0;
+        return part == PART_A1 ? a1 : (part == PART_A2 ? a2 : (a1 || a2));
+    }
+    bool a1 = (i / l) == (j / l);
+    bool a2 = (j % l) >= l - c;
+    return part == PART_A1 ? a1 : (part == PART_A2 ? a2 : (a1 || a2));
+}
+
+}  // namespace sa

@@ -1,0 +1,256 @@
+"""ctypes binding of libsparse_attn.so (include/sparse_attn.h).
+
+The functions named like the C entry points only marshal arguments: every
+step of the computation runs in the library's HIP kernels.  PyTorch supplies
+device memory and the current stream.  The convenience layer below them
+(``build_layout``, ``forward``, ``backward``, ``SparseAttention``) allocates
+outputs with torch and calls those same entry points.
+
+Loading fails loudly when the library has not been built; there is no
+fallback implementation.
+"""
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_attn.so")
+
+SA_OK, SA_ERR_INVALID, SA_ERR_UNSUPPORTED, SA_ERR_BUFFER_TOO_SMALL, SA_ERR_HIP = 0, -1, -2, -3, -4
+SA_STRIDED, SA_FIXED = 0, 1
+SA_MODE_A1, SA_MODE_A2, SA_MODE_MERGED, SA_MODE_INTERLEAVED = 0, 1, 2, 3
+SA_F32, SA_BF16 = 0, 1
+SA_TILE_FULL, SA_TILE_MASKED = 0, 1
+
+EXPORTED = (
+    "sparse_attn_layout_size",
+    "sparse_attn_layout",
+    "sparse_attn_fwd",
+    "sparse_attn_bwd_workspace_size",
+    "sparse_attn_bwd",
+    "sparse_attn_status_string",
+)
+
+_lib = None
+_i32, _i64, _f32, _vp, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+_PAT = [_i64, _i32, _i32, _i32, _i32, _i32]  # n, block, stride_l, summary_c, pattern, head_mode
+
+
+class SparseAttnError(RuntimeError):
+    def __init__(self, func, status):
+        self.status = status
+        super().__init__(f"{func} failed: {status_string(status)} ({status})")
+
+
+def lib():
+    """Load the built library (raises if it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        L.sparse_attn_layout_size.argtypes = _PAT + [_vp, _vp]
+        L.sparse_attn_layout.argtypes = _PAT + [_vp] * 6 + [_i64, _vp]
+        L.sparse_attn_fwd.argtypes = _PAT + [_vp] * 3 + [_i32] * 4 + [_vp] * 4 + [_f32, _vp, _vp, _vp]
+        L.sparse_attn_bwd_workspace_size.argtypes = _PAT + [_i32] * 4 + [_vp]
+        L.sparse_attn_bwd.argtypes = (_PAT + [_vp] * 6 + [_i32] * 4 + [_vp] * 7 + [_f32]
+                                      + [_vp] * 4 + [_sz, _vp])
+        L.sparse_attn_status_string.argtypes = [ctypes.c_int]
+        L.sparse_attn_status_string.restype = ctypes.c_char_p
+        for name in EXPORTED[:-1]:
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().sparse_attn_status_string(int(status)).decode()
+
+
+def _check(func, status):
+    if status != SA_OK:
+        raise SparseAttnError(func, status)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _strides(*tensors):
+    st = tensors[0].stride()
+    for t in tensors:
+        if t.dim() != 4 or t.stride() != st or t.stride(3) != 1:
+            raise ValueError("tensors must be [batch, heads, n, d] with d contiguous and identical strides")
+    return (ctypes.c_int64 * 3)(st[0], st[1], st[2])
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return SA_BF16
+    if t.dtype == torch.float32:
+        return SA_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+# ---------------------------------------------------------------------------
+# Entry points, same names and argument order as the C ABI
+# ---------------------------------------------------------------------------
+def sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode):
+    ng = ctypes.c_int32(0)
+    nnz = (ctypes.c_int64 * 2)(0, 0)
+    st = lib().sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode,
+                                       ctypes.byref(ng), nnz)
+    _check("sparse_attn_layout_size", st)
+    return ng.value, [nnz[0], nnz[1]][: ng.value]
+
+
+def sparse_attn_layout(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,
+                       col_ptr, row_idx, kind_t, capacity, stream=None):
+    st = lib().sparse_attn_layout(n, block, stride_l, summary_c, pattern, head_mode, _ptr(row_ptr),
+                                  _ptr(col_idx), _ptr(kind), _ptr(col_ptr), _ptr(row_idx), _ptr(kind_t),
+                                  capacity, _stream(stream, row_ptr.device))
+    _check("sparse_attn_layout", st)
+
+
+def sparse_attn_fwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,
+                    batch, heads, d_head, dtype, q, k, v, strides, softmax_scale, o, lse, stream=None):
+    st = lib().sparse_attn_fwd(n, block, stride_l, summary_c, pattern, head_mode, _ptr(row_ptr),
+                               _ptr(col_idx), _ptr(kind), batch, heads, d_head, dtype, _ptr(q), _ptr(k),
+                               _ptr(v), strides, softmax_scale, _ptr(o), _ptr(lse),
+                               _stream(stream, q.device))
+    _check("sparse_attn_fwd", st)
+
+
+def sparse_attn_bwd_workspace_size(n, block, stride_l, summary_c, pattern, head_mode, batch, heads,
+                                   d_head, dtype):
+    out = ctypes.c_size_t(0)
+    st = lib().sparse_attn_bwd_workspace_size(n, block, stride_l, summary_c, pattern, head_mode, batch,
+                                              heads, d_head, dtype, ctypes.byref(out))
+    _check("sparse_attn_bwd_workspace_size", st)
+    return out.value
+
+
+def sparse_attn_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,
+                    col_ptr, row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse,
+                    strides, softmax_scale, dq, dk, dv, workspace, workspace_bytes, stream=None):
+    st = lib().sparse_attn_bwd(n, block, stride_l, summary_c, pattern, head_mode, _ptr(row_ptr),
+                               _ptr(col_idx), _ptr(kind), _ptr(col_ptr), _ptr(row_idx), _ptr(kind_t),
+                               batch, heads, d_head, dtype, _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                               _ptr(dout), _ptr(lse), strides, softmax_scale, _ptr(dq), _ptr(dk),
+                               _ptr(dv), _ptr(workspace), workspace_bytes, _stream(stream, q.device))
+    _check("sparse_attn_bwd", st)
+
+
+# ---------------------------------------------------------------------------
+# Convenience layer: torch allocates, the entry points above compute
+# ---------------------------------------------------------------------------
+@dataclass
+class Layout:
+    n: int
+    block: int
+    stride_l: int
+    summary_c: int
+    pattern: int
+    head_mode: int
+    n_layouts: int
+    nnz: list
+    row_ptr: torch.Tensor
+    col_idx: torch.Tensor
+    kind: torch.Tensor
+    col_ptr: torch.Tensor
+    row_idx: torch.Tensor
+    kind_t: torch.Tensor
+
+    @property
+    def pattern_args(self):
+        return (self.n, self.block, self.stride_l, self.summary_c, self.pattern, self.head_mode)
+
+    @property
+    def row_args(self):
+        return (self.row_ptr, self.col_idx, self.kind)
+
+    @property
+    def col_args(self):
+        return (self.col_ptr, self.row_idx, self.kind_t)
+
+
+def build_layout(n, block, stride_l, summary_c, pattern, head_mode, device="cuda", stream=None):
+    ng, nnz = sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode)
+    nq = n // block
+    total = max(1, sum(nnz))
+    dev = torch.device(device)
+    lay = Layout(n, block, stride_l, summary_c, pattern, head_mode, ng, nnz,
+                 row_ptr=torch.empty(ng * (nq + 1), dtype=torch.int32, device=dev),
+                 col_idx=torch.empty(total, dtype=torch.int32, device=dev),
+                 kind=torch.empty(total, dtype=torch.uint8, device=dev),
+                 col_ptr=torch.empty(ng * (nq + 1), dtype=torch.int32, device=dev),
+                 row_idx=torch.empty(total, dtype=torch.int32, device=dev),
+                 kind_t=torch.empty(total, dtype=torch.uint8, device=dev))
+    sparse_attn_layout(*lay.pattern_args, lay.row_ptr, lay.col_idx, lay.kind, lay.col_ptr, lay.row_idx,
+                       lay.kind_t, total, stream)
+    return lay
+
+
+def _scale(softmax_scale, d):
+    return float(1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale)
+
+
+def forward(q, k, v, layout: Layout, softmax_scale=None, out=None, lse=None, stream=None):
+    """O and LSE of sparse attention over ``layout``; q, k, v are [b, h, n, d] on the GPU."""
+    b, h, n, d = q.shape
+    if n != layout.n:
+        raise ValueError("sequence length differs from the layout's")
+    strides = _strides(q, k, v)
+    o = torch.empty_like(q) if out is None else out
+    _strides(q, o)
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if lse is None else lse
+    sparse_attn_fwd(*layout.pattern_args, *layout.row_args, b, h, d, _dtype_code(q), q, k, v, strides,
+                    _scale(softmax_scale, d), o, lse, stream)
+    return o, lse
+
+
+def backward(q, k, v, o, dout, lse, layout: Layout, softmax_scale=None, grads=None, workspace=None,
+             stream=None):
+    """dq, dk, dv of sparse attention given the forward's o and lse."""
+    b, h, n, d = q.shape
+    strides = _strides(q, k, v, o, dout)
+    dq, dk, dv = grads if grads is not None else (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    _strides(q, dq, dk, dv)
+    dtype = _dtype_code(q)
+    need = sparse_attn_bwd_workspace_size(*layout.pattern_args, b, h, d, dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    sparse_attn_bwd(*layout.pattern_args, *layout.row_args, *layout.col_args, b, h, d, dtype, q, k, v, o,
+                    dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
+                    workspace.numel() * workspace.element_size(), stream)
+    return dq, dk, dv
+
+
+class SparseAttention(torch.autograd.Function):
+    """Autograd wrapper: saves O and LSE, recomputes attention weights in backward."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, layout, softmax_scale=None):
+        o, lse = forward(q, k, v, layout, softmax_scale)
+        ctx.save_for_backward(q, k, v, o, lse)
+        ctx.layout = layout
+        ctx.softmax_scale = softmax_scale
+        return o
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, o, lse = ctx.saved_tensors
+        dq, dk, dv = backward(q, k, v, o, dout.contiguous(), lse, ctx.layout, ctx.softmax_scale)
+        return dq, dk, dv, None, None

@@ -1,0 +1,136 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+the header declares, validates arguments before touching device memory, and
+its host-side layout size query agrees with the oracle's brute force."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1904_10509_amd import sparse_attn as sa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparse_attn.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(sa.LIB_PATH):
+        from paper_1904_10509_amd import build
+        build.build()
+    return sa.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(sparse_attn_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(sa.EXPORTED), names
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    assert sa.status_string(0) == "success"
+    for code in (-1, -2, -3, -4):
+        assert sa.status_string(code) not in ("success", "unknown status")
+    assert sa.status_string(7) == "unknown status"
+
+
+SIZE_CASES = [
+    (256, 16, 16, 0, 0, 2), (256, 16, 16, 0, 0, 0), (256, 16, 16, 0, 0, 1), (256, 16, 16, 0, 0, 3),
+    (384, 32, 7, 0, 0, 2), (128, 16, 1, 0, 0, 2), (128, 32, 500, 0, 0, 0), (64, 64, 9, 0, 0, 1),
+    (3072, 32, 128, 32, 1, 3), (240, 16, 20, 1, 1, 2), (192, 64, 24, 10, 1, 1), (128, 16, 500, 3, 1, 2),
+    (512, 64, 256, 32, 1, 2), (512, 16, 48, 48, 1, 3), (12288, 64, 128, 0, 0, 2),
+    (65536, 64, 256, 32, 1, 2),
+]
+
+
+@pytest.mark.parametrize("n,B,l,c,pattern,mode", SIZE_CASES)
+def test_layout_size_matches_oracle(L, orc, n, B, l, c, pattern, mode):
+    ng, nnz = sa.sparse_attn_layout_size(n, B, l, c, pattern, mode)
+    lay = orc.layout(n, B, l, c, pattern, mode)
+    assert ng == lay["n_layouts"]
+    assert list(nnz) == list(lay["nnz"])
+
+
+@pytest.mark.parametrize("args", [
+    (100, 16, 8, 0, 0, 2),    # n not a multiple of block
+    (256, 24, 8, 0, 0, 2),    # block not supported
+    (256, 16, 0, 0, 0, 2),    # l < 1
+    (256, 16, 8, 3, 0, 2),    # c given for strided
+    (256, 16, 8, 0, 1, 2),    # c = 0 for fixed
+    (256, 16, 8, 9, 1, 2),    # c > l
+    (256, 16, 8, 0, 2, 2),    # unknown pattern
+    (256, 16, 8, 0, 0, 4),    # unknown mode
+    (0, 16, 8, 0, 0, 2),      # n < 1
+])
+def test_layout_size_rejects_invalid(L, args):
+    ng = ctypes.c_int32(0)
+    nnz = (ctypes.c_int64 * 2)()
+    assert L.sparse_attn_layout_size(*args, ctypes.byref(ng), nnz) == sa.SA_ERR_INVALID
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def _fwd(L, **over):
+    args = dict(n=256, block=16, l=16, c=0, pattern=0, mode=2, row_ptr=FAKE, col_idx=FAKE, kind=FAKE,
+                batch=1, heads=1, d=32, dtype=sa.SA_BF16, q=FAKE, k=FAKE, v=FAKE,
+                strides=(ctypes.c_int64 * 3)(8192, 8192, 32), scale=0.25, o=FAKE, lse=FAKE, stream=None)
+    args.update(over)
+    return L.sparse_attn_fwd(*args.values())
+
+
+@pytest.mark.parametrize("over,expect", [
+    (dict(n=250), sa.SA_ERR_INVALID),
+    (dict(c=4), sa.SA_ERR_INVALID),
+    (dict(d=48), sa.SA_ERR_UNSUPPORTED),
+    (dict(dtype=5), sa.SA_ERR_INVALID),
+    (dict(batch=0), sa.SA_ERR_INVALID),
+    (dict(q=None), sa.SA_ERR_INVALID),
+    (dict(lse=None), sa.SA_ERR_INVALID),
+    (dict(row_ptr=None), sa.SA_ERR_INVALID),
+    (dict(o=FAKE + 8), sa.SA_ERR_INVALID),                                  # misaligned
+    (dict(strides=(ctypes.c_int64 * 3)(8192, 8192, 36)), sa.SA_ERR_INVALID),  # stride not 16-byte
+    (dict(strides=(ctypes.c_int64 * 3)(8192, 8192, 16)), sa.SA_ERR_INVALID),  # rows overlap
+    (dict(strides=None), sa.SA_ERR_INVALID),
+    (dict(scale=float("nan")), sa.SA_ERR_INVALID),
+])
+def test_fwd_rejects_invalid(L, over, expect):
+    assert _fwd(L, **over) == expect
+
+
+def test_bwd_workspace_and_errors(L):
+    out = ctypes.c_size_t(0)
+    assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
+    assert out.value == 2 * 3 * 256 * (64 + 1) * 4
+    assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_F32, ctypes.byref(out)) == 0
+    assert out.value == 2 * 3 * 256 * 4
+    assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 40, sa.SA_F32, ctypes.byref(out)) == \
+        sa.SA_ERR_UNSUPPORTED
+    strides = (ctypes.c_int64 * 3)(256 * 64, 256 * 64, 64)
+    common = [256, 16, 16, 0, 0, 2] + [FAKE] * 6 + [1, 1, 64, sa.SA_BF16] + [FAKE] * 6 + [strides, 0.125] + [FAKE] * 3
+    need = 256 * 65 * 4
+    assert L.sparse_attn_bwd(*common, FAKE, need - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
+    assert L.sparse_attn_bwd(*common, None, need, None) == sa.SA_ERR_INVALID
+    bad = list(common)
+    bad[6 + 3] = None  # col_ptr
+    assert L.sparse_attn_bwd(*bad, FAKE, need, None) == sa.SA_ERR_INVALID
+
+
+def test_layout_rejects_small_capacity(L):
+    _, nnz = sa.sparse_attn_layout_size(256, 16, 16, 0, 0, 2)
+    assert L.sparse_attn_layout(256, 16, 16, 0, 0, 2, *([FAKE] * 6), nnz[0] - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
+    assert L.sparse_attn_layout(256, 16, 16, 0, 0, 2, *([FAKE] * 5), None, nnz[0], None) == sa.SA_ERR_INVALID
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(sa, "_lib", None)
+    monkeypatch.setattr(sa, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        sa.lib()

@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Layouts must match bitwise.  Outputs and gradients must match the fp64
+oracle on the same inputs within the tolerance of the element type, 1e-5 for
+fp32 and 2e-2 for bf16 (LSE: 1e-5 / 1e-3), on |gpu - oracle| / max(1, |oracle|):
+the max-abs error for values up to 1, relative above.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc_mod
+from paper_1904_10509_amd import sparse_attn as sa
+from paper_1904_10509_amd.inputs import WORKLOADS, make_inputs, workload_inputs
+
+from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+S, F = sa.SA_STRIDED, sa.SA_FIXED
+A1, A2, MG, IL = sa.SA_MODE_A1, sa.SA_MODE_A2, sa.SA_MODE_MERGED, sa.SA_MODE_INTERLEAVED
+
+
+def layout_to_cpu(lay):
+    return {k: getattr(lay, k).cpu().numpy() for k in ("row_ptr", "col_idx", "kind", "col_ptr", "row_idx", "kind_t")}
+
+
+LAYOUT_CASES = [
+    (S, 256, 16, 16, 0), (S, 256, 16, 24, 0), (S, 192, 32, 7, 0), (S, 128, 16, 1, 0), (S, 128, 32, 500, 0),
+    (S, 64, 64, 9, 0), (S, 384, 64, 128, 0), (F, 256, 16, 32, 8), (F, 256, 32, 32, 32), (F, 240, 16, 20, 1),
+    (F, 192, 64, 24, 10), (F, 128, 16, 500, 3), (F, 64, 64, 16, 4), (F, 384, 32, 128, 32),
+    (F, 512, 64, 256, 32), (S, 3072, 32, 128, 0), (F, 3072, 32, 128, 32), (S, 12288, 64, 128, 0),
+    (F, 65536, 64, 256, 32),
+]
+
+
+@pytest.mark.parametrize("pattern,n,B,l,c", LAYOUT_CASES)
+@pytest.mark.parametrize("mode", [A1, A2, MG, IL])
+def test_layout_bitwise(pattern, n, B, l, c, mode):
+    dev = device()
+    lay = sa.build_layout(n, B, l, c, pattern, mode, device=dev)
+    got = layout_to_cpu(lay)
+    ref = orc_mod.layout(n, B, l, c, pattern, mode)
+    assert lay.n_layouts == ref["n_layouts"] and list(lay.nnz) == list(ref["nnz"])
+    total = int(sum(ref["nnz"]))
+    for key in ("row_ptr", "col_ptr"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    for key in ("col_idx", "kind", "row_idx", "kind_t"):
+        np.testing.assert_array_equal(got[key][:total], ref[key], err_msg=key)
+
+
+# (pattern, mode, n, B, l, c, d, dtype, batch, heads)
+SMALL_CASES = [
+    (S, MG, 256, 16, 16, 0, 32, torch.float32, 1, 1),
+    (S, A1, 256, 16, 16, 0, 32, torch.float32, 1, 2),
+    (S, A2, 256, 16, 16, 0, 64, torch.float32, 2, 1),
+    (F, IL, 256, 32, 64, 16, 128, torch.float32, 1, 3),
+    (F, A2, 192, 16, 32, 8, 32, torch.float32, 1, 1),
+    (S, MG, 512, 64, 64, 0, 64, torch.bfloat16, 2, 2),
+    (S, MG, 512, 64, 100, 0, 64, torch.bfloat16, 1, 2),
+    (S, A1, 384, 64, 128, 0, 128, torch.bfloat16, 1, 2),
+    (S, A2, 384, 32, 48, 0, 64, torch.bfloat16, 1, 2),
+    (S, MG, 256, 16, 1, 0, 32, torch.bfloat16, 1, 1),
+    (S, MG, 320, 32, 1000, 0, 64, torch.bfloat16, 1, 1),
+    (S, MG, 64, 64, 8, 0, 64, torch.bfloat16, 1, 1),
+    (F, MG, 1024, 64, 256, 32, 64, torch.bfloat16, 1, 2),
+    (F, MG, 512, 64, 96, 40, 64, torch.bfloat16, 2, 1),
+    (F, A1, 512, 32, 128, 32, 128, torch.bfloat16, 1, 2),
+    (F, A2, 512, 32, 128, 32, 128, torch.bfloat16, 1, 2),
+    (F, IL, 768, 32, 128, 32, 128, torch.bfloat16, 2, 3),
+    (F, A2, 256, 16, 64, 1, 32, torch.bfloat16, 1, 1),
+    (F, MG, 256, 64, 64, 64, 64, torch.bfloat16, 1, 1),
+    (F, IL, 512, 16, 48, 12, 64, torch.bfloat16, 1, 2),
+]
+
+
+@pytest.mark.parametrize("pattern,mode,n,B,l,c,d,dtype,batch,heads", SMALL_CASES)
+def test_parity_small(pattern, mode, n, B, l, c, d, dtype, batch, heads):
+    x = make_inputs(batch, heads, n, d, dtype, seed=n + l + c + d)
+    scale = d ** -0.5
+    got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=mode, scale=scale)
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=pattern, mode=mode, l=l, c=c, scale=scale)
+    for name in ("o", "dq", "dk", "dv"):
+        assert max_err(got[name], ref[name]) <= TOL[dtype], (name, max_err(got[name], ref[name]))
+    assert max_err(got["lse"], ref["lse"]) <= LSE_TOL[dtype], max_err(got["lse"], ref["lse"])
+
+
+def test_workload_fp32_full():
+    w = WORKLOADS["strided_n256_l16_f32"]
+    x = workload_inputs(w)
+    for mode in (MG, A1, A2):
+        got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=mode, scale=w.scale)
+        ref = orc_mod.backward(*oracle_inputs(x), pattern=w.pattern, mode=mode, l=w.stride, c=w.summary,
+                               scale=w.scale)
+        for name in ("o", "lse", "dq", "dk", "dv"):
+            assert max_err(got[name], ref[name]) <= 1e-5, (mode, name, max_err(got[name], ref[name]))
+
+
+def test_workload_interleaved_full():
+    w = WORKLOADS["fixed_n3072_l128_c32_interleaved"]
+    x = workload_inputs(w)
+    got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=w.mode, scale=w.scale)
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary,
+                           scale=w.scale)
+    for name in ("o", "dq", "dk", "dv"):
+        assert max_err(got[name], ref[name]) <= 2e-2, (name, max_err(got[name], ref[name]))
+    assert max_err(got["lse"], ref["lse"]) <= 1e-3
+    empty = np.isneginf(ref["lse"])
+    assert empty.sum() == w.batch * (w.heads // 2) * (w.stride - w.summary)  # head 1, first block
+    assert np.all(got["o"][np.broadcast_to(empty[..., None], got["o"].shape)] == 0)
+
+
+def sample_index(w, rng, count):
+    """(b, h, i) triples: first and last rows, tile and l-block edges, random."""
+    idx = [0, 1, w.block - 1, w.block, w.stride - 1, w.stride, w.stride + 1, w.n // 2, w.n - w.block, w.n - 1]
+    idx += list(rng.integers(0, w.n, count - len(idx)))
+    b = rng.integers(0, w.batch, len(idx))
+    h = rng.integers(0, w.heads, len(idx))
+    return np.stack([b, h, np.array(idx)], axis=1)
+
+
+@pytest.mark.parametrize("name", ["strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged"])
+def test_workload_sampled(name):
+    w = WORKLOADS[name]
+    x = workload_inputs(w)
+    got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=w.mode, scale=w.scale)
+    rng = np.random.default_rng(w.seed)
+    rows = sample_index(w, rng, 48)
+    cols = sample_index(w, rng, 24)
+    xi = oracle_inputs(x)
+    kw = dict(pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
+    o, lse = orc_mod.forward_rows(*xi[:3], rows, **kw)
+    dq = orc_mod.backward_rows(*xi, rows, **kw)
+    dk, dv = orc_mod.backward_cols(*xi, cols, **kw)
+    r = (rows[:, 0], rows[:, 1], rows[:, 2])
+    cc = (cols[:, 0], cols[:, 1], cols[:, 2])
+    assert max_err(got["o"][r], o) <= 2e-2
+    assert max_err(got["lse"][r], lse) <= 1e-3
+    assert max_err(got["dq"][r], dq) <= 2e-2
+    assert max_err(got["dk"][cc], dk) <= 2e-2
+    assert max_err(got["dv"][cc], dv) <= 2e-2
+    # properties at full size: rows of P sum to one (checked through V = 1 below on a
+    # smaller case), finite outputs, gradient of a shift of all keys vanishes
+    for key in ("o", "dq", "dk", "dv", "lse"):
+        assert np.all(np.isfinite(got[key])), key
+    assert np.abs(got["dk"].sum(axis=2)).max() <= 2e-2 * np.sqrt(w.n)
+
+
+def test_ones_value_gives_ones_output():
+    dev = device()
+    for pattern, mode, l, c in ((S, MG, 64, 0), (F, MG, 64, 16), (F, A2, 64, 16)):
+        n, B, d = 512, 64, 64
+        x = make_inputs(1, 2, n, d, torch.bfloat16, seed=5)
+        x["v"] = torch.ones_like(x["v"])
+        got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=mode, scale=d ** -0.5, backward=False, dev=dev)
+        nonempty = np.isfinite(got["lse"])
+        assert np.abs(got["o"][nonempty] - 1.0).max() <= 2e-2
+        assert np.all(got["o"][~nonempty] == 0)
+
+
+def test_forward_and_layout_are_deterministic():
+    dev = device()
+    w = WORKLOADS["strided_n12288_l128_merged"]
+    x = make_inputs(1, 2, w.n, w.d_head, torch.bfloat16, seed=9)
+    q, k, v = (x[n_].to(dev) for n_ in ("q", "k", "v"))
+    lay1 = sa.build_layout(w.n, w.block, w.stride, 0, w.pattern, w.mode, device=dev)
+    lay2 = sa.build_layout(w.n, w.block, w.stride, 0, w.pattern, w.mode, device=dev)
+    for key in ("row_ptr", "col_idx", "kind", "col_ptr", "row_idx", "kind_t"):
+        assert torch.equal(getattr(lay1, key), getattr(lay2, key))
+    o1, l1 = sa.forward(q, k, v, lay1)
+    o2, l2 = sa.forward(q, k, v, lay1)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_strided_views_match_contiguous():
+    dev = device()
+    b, h, n, d, B = 2, 3, 256, 64, 32
+    base = torch.randn(b, n, h, d, generator=torch.Generator().manual_seed(3)).to(torch.bfloat16).to(dev)
+    q = base.transpose(1, 2)  # strides (n*h*d, d, h*d, 1)
+    k = (base * 0.5).transpose(1, 2)
+    v = (base - 0.25).transpose(1, 2)
+    lay = sa.build_layout(n, B, 32, 8, F, IL, device=dev)
+    o_v, lse_v = sa.forward(q, k, v, lay)
+    o_c, lse_c = sa.forward(q.contiguous(), k.contiguous(), v.contiguous(), lay)
+    assert torch.equal(o_v.contiguous(), o_c) and torch.equal(lse_v, lse_c)
+    dout = torch.randn_like(o_v)
+    g_v = sa.backward(q, k, v, o_v, dout, lse_v, lay)
+    g_c = sa.backward(q.contiguous(), k.contiguous(), v.contiguous(), o_c, dout.contiguous(), lse_c, lay)
+    for a_, b_ in zip(g_v, g_c):
+        assert (a_.contiguous().float() - b_.float()).abs().max().item() <= 1e-2
+
+
+def test_autograd_wrapper():
+    dev = device()
+    n, B, d = 256, 32, 64
+    x = make_inputs(1, 2, n, d, torch.bfloat16, seed=21)
+    lay = sa.build_layout(n, B, 32, 0, S, MG, device=dev)
+    q, k, v = (x[n_].to(dev).requires_grad_(True) for n_ in ("q", "k", "v"))
+    o = sa.SparseAttention.apply(q, k, v, lay, None)
+    (o.float() * x["dout"].to(dev).float()).sum().backward()
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=S, mode=MG, l=32, c=0, scale=d ** -0.5)
+    assert max_err(q.grad.float().cpu().numpy(), ref["dq"]) <= 2e-2
+    assert max_err(k.grad.float().cpu().numpy(), ref["dk"]) <= 2e-2
+    assert max_err(v.grad.float().cpu().numpy(), ref["dv"]) <= 2e-2
