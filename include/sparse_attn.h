@@ -127,7 +127,7 @@ int sparse_attn_layout(int64_t n, int32_t block, int32_t stride_l, int32_t summa
  *   dtype                    sa_dtype of q, k, v and o
  *   q, k, v                  device inputs, [batch, heads, n, d_head]
  *   strides                  host array {batch, head, sequence} in elements
- *   softmax_scale            multiplies q . k (the paper uses 1/sqrt(d_head))
+ *   softmax_scale            > 0, multiplies q . k (the paper uses 1/sqrt(d_head))
  *   o                        device output, same shape and strides as q
  *   lse                      device output [batch, heads, n] fp32:
  *                            log sum_j exp(scale q_i . k_j), -inf for empty rows

@@ -4,6 +4,7 @@
 
 #include "../../include/sparse_attn.h"
 #include "sa_internal.h"
+#include "sa_mask.h"
 
 namespace {
 
@@ -81,6 +82,7 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.ss = strides[2];
     a.scale = scale;
     a.scale_log2 = scale * sa::kLog2eHost;
+    a.period_bits = sa::host_period_bits(p.l);
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;
     a.kind = kind;
@@ -141,7 +143,7 @@ int sparse_attn_fwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
     if (st != SA_OK) return st;
     if (!row_ptr || !col_idx || !kind || !q || !k || !v || !o || !lse) return SA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID;
-    if (!isfinite(softmax_scale)) return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
     sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,
                                kind, nullptr, nullptr, nullptr);
     hipError_t e = sa::fwd_launch(a, dtype, q, k, v, o, lse, static_cast<hipStream_t>(stream));
@@ -179,7 +181,7 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return SA_ERR_INVALID;
-    if (!isfinite(softmax_scale)) return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
     const size_t need = sa::bwd_workspace_bytes(batch, heads, n, d_head, dtype);
     if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
     if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;

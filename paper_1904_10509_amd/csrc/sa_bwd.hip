@@ -16,6 +16,7 @@
 // fp32 path: the same quantities on the VALU, one thread per row for dq and
 // one thread per column for dk / dv, with no atomics.
 #include "sa_internal.h"
+#include "sa_mask.h"
 #include "sa_mfma.h"
 
 namespace sa {
@@ -74,210 +75,264 @@ bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout,
 // ---------------------------------------------------------------------------
 template <int D, int BLK>
 struct BwdCfg {
-    static constexpr int NW = BLK / 16;         // waves; wave w owns keys 16w .. 16w+15
+    static constexpr int KW = BLK < 32 ? BLK : 32;  // keys per wave
+    static constexpr int KBW = KW / 16;             // 16-key blocks per wave
+    static constexpr int NW = BLK / KW;             // waves
     static constexpr int NT = NW * 64;
-    static constexpr int KS = D / 32;           // 32-deep steps over d
-    static constexpr int QB = BLK / 16;         // 16-query blocks per tile
-    static constexpr int QC = (BLK + 31) / 32;  // 32-query chunks (contraction over queries)
+    static constexpr int KS = D / 32;               // 32-deep steps over d
+    static constexpr int QB = BLK / 16;             // 16-query blocks per tile
+    static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
-    static constexpr int RP = D + 8;            // pitch of row-major [BLK][D] tiles
-    static constexpr int TP = BLK + 8;          // pitch of transposed [D][BLK] tiles and sdS
+    static constexpr int P = D + 8;                 // pitch of row-major [BLK][D] tiles
+    static constexpr int SP = BLK + 8;              // pitch of dS [query][key]
+    static constexpr int CH = BLK * D / 8;          // 16-byte chunks per Q (or dO) tile
+    static constexpr int CPT = (CH + NT - 1) / NT;
+    static constexpr int QRW = BLK / NW;            // dQ rows per wave
+    static constexpr int QBQ = QRW / 16;            // their 16-row blocks
 };
 
-// Stage rows [row0, row0 + BLK) of a [.., D] bf16 tensor into LDS twice:
-// row-major (pitch RP) and transposed (pitch TP).
 template <int D, int BLK>
-__device__ inline void stage_both(const uint16_t* __restrict__ src, int64_t row0, int64_t ss,
-                                  uint16_t* dst, uint16_t* dstT, int tid) {
-    using C = BwdCfg<D, BLK>;
-    uint32_t* dstT32 = reinterpret_cast<uint32_t*>(dstT);
-    for (int u = tid; u < (BLK / 2) * (D / 8); u += C::NT) {
-        const int pr = u / (D / 8), col = (u % (D / 8)) * 8;
-        u32x4 r0 = *reinterpret_cast<const u32x4*>(src + (row0 + 2 * pr) * ss + col);
-        u32x4 r1 = *reinterpret_cast<const u32x4*>(src + (row0 + 2 * pr + 1) * ss + col);
-        *reinterpret_cast<u32x4*>(dst + (2 * pr) * C::RP + col) = r0;
-        *reinterpret_cast<u32x4*>(dst + (2 * pr + 1) * C::RP + col) = r1;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            uint32_t lo = (r0[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-            uint32_t hi = (r1[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-            dstT32[((col + e) * C::TP) / 2 + pr] = lo | (hi << 16);
-        }
-    }
-}
-
-// Operand over a 32-query (or 32-key) chunk read from a transposed tile row,
-// in the chunk_row() order; zero-padded when the tile has only 16 entries.
-template <int BLK>
-__device__ inline bf16x8 ld_chunk_T(const uint16_t* row, int chunk, int g) {
-    const uint16_t* p = row + chunk * 32 + 4 * g;
-    if constexpr (BLK >= 32) {
-        return ld_bf16x4x2(p, p + 16);
-    } else {
-        u32x2 lo = *reinterpret_cast<const u32x2*>(p);
-        return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
-    }
-}
-
-template <int BLK>
-__device__ inline bf16x8 pack_chunk(const f32x4* x, int chunk) {
-    if constexpr (BLK >= 32) {
-        return pack_bf16x8(x[2 * chunk], x[2 * chunk + 1]);
-    } else {
-        return pack_bf16x8(x[0], zero4());
-    }
-}
-
-template <int D, int BLK>
-__global__ void __launch_bounds__(BLK * 4)
+__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                      const float* __restrict__ lse, const float* __restrict__ delta,
                      float* __restrict__ dq_acc, uint16_t* __restrict__ dk,
                      uint16_t* __restrict__ dv) {
     using C = BwdCfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t sQ[BLK * C::RP];
-    __shared__ __attribute__((aligned(16))) uint16_t sQt[D * C::TP];
-    __shared__ __attribute__((aligned(16))) uint16_t sdO[BLK * C::RP];
-    __shared__ __attribute__((aligned(16))) uint16_t sdOt[D * C::TP];
-    __shared__ __attribute__((aligned(16))) uint16_t sKt[D * C::TP];
-    __shared__ __attribute__((aligned(16))) uint16_t sdS[BLK * C::TP];
-    __shared__ float sL[BLK];
-    __shared__ float sDelta[BLK];
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[2][BLK * C::P];
+    __shared__ __attribute__((aligned(16))) uint16_t sdO[2][BLK * C::P];
+    __shared__ __attribute__((aligned(16))) uint16_t sK[BLK * C::P];
+    __shared__ __attribute__((aligned(16))) uint16_t sdS[BLK * C::SP];
+    __shared__ __attribute__((aligned(16))) float sL[2][BLK];
+    __shared__ __attribute__((aligned(16))) float sDl[2][BLK];
 
     const int kb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    const int part = part_of_head(a.mode, h);
+    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;  // LSE / D / dq_acc rows
-    const int j = kb * BLK + w * 16 + r;                        // this lane's key
+    const int key0 = kb * BLK + w * C::KW;                      // first key of this wave
 
-    // K and V rows of this lane's key, as B operands (d in 8g .. 8g+7 of each step)
-    bf16x8 kf[C::KS], vf[C::KS];
+    // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
+    bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
+    bool summary[C::KBW];
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-        kf[ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
-        vf[ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
-    }
-    // K^T of the whole key block for the dQ product
-    {
-        uint32_t* sKt32 = reinterpret_cast<uint32_t*>(sKt);
-        for (int u = tid; u < (BLK / 2) * (D / 8); u += C::NT) {
-            const int pr = u / (D / 8), col = (u % (D / 8)) * 8;
-            const int64_t r0 = base + (int64_t)(kb * BLK + 2 * pr) * a.ss + col;
-            u32x4 x0 = *reinterpret_cast<const u32x4*>(k + r0);
-            u32x4 x1 = *reinterpret_cast<const u32x4*>(k + r0 + a.ss);
+    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+        const int j = key0 + 16 * kbw + r;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                uint32_t lo = (x0[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                uint32_t hi = (x1[e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                sKt32[((col + e) * C::TP) / 2 + pr] = lo | (hi << 16);
-            }
+        for (int ks = 0; ks < C::KS; ++ks) {
+            kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+            vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
         }
+        summary[kbw] = a.pattern == FIXED && (j % a.l) >= a.l - a.c;
+    }
+    // the key block row-major, for the transposed operand of dQ = dS K
+    for (int ch = tid; ch < C::CH; ch += C::NT) {
+        const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+        *reinterpret_cast<u32x4*>(&sK[row * C::P + col]) =
+            *reinterpret_cast<const u32x4*>(k + base + (int64_t)(kb * BLK + row) * a.ss + col);
     }
 
-    f32x4 dvacc[C::DB], dkacc[C::DB];
+    f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db) {
-        dvacc[db] = zero4();
-        dkacc[db] = zero4();
-    }
+    for (int kbw = 0; kbw < C::KBW; ++kbw)
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {
+            dvacc[kbw][db] = zero4();
+            dkacc[kbw][db] = zero4();
+        }
 
     const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
     const int e0 = a.col_ptr[cp], e1 = a.col_ptr[cp + 1];
-    for (int e = e0; e < e1; ++e) {
+    const int len = e1 - e0;
+    // Start each column at its own offset so that the workgroups running at
+    // the same time add into different dQ rows.
+    const int rot = len > 0 ? (int)(((int64_t)kb * 37 + h * 11) % len) : 0;
+    auto entry = [&](int s) { int x = s + rot; return e0 + (x >= len ? x - len : x); };
+
+    u32x4 qreg[C::CPT], oreg[C::CPT];
+    float lreg = 0.f, dreg = 0.f;
+    auto load_block = [&](int qb) {
+        const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
+#pragma unroll
+        for (int t = 0; t < C::CPT; ++t) {
+            const int ch = tid + t * C::NT;
+            if (C::CH % C::NT == 0 || ch < C::CH) {
+                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+                qreg[t] = *reinterpret_cast<const u32x4*>(q + qbase + (int64_t)row * a.ss + col);
+                oreg[t] = *reinterpret_cast<const u32x4*>(dout + qbase + (int64_t)row * a.ss + col);
+            }
+        }
+        if (tid < BLK) {
+            lreg = lse[rowbase + (int64_t)qb * BLK + tid];
+            dreg = delta[rowbase + (int64_t)qb * BLK + tid];
+        }
+    };
+    auto store_block = [&](int buf) {
+#pragma unroll
+        for (int t = 0; t < C::CPT; ++t) {
+            const int ch = tid + t * C::NT;
+            if (C::CH % C::NT == 0 || ch < C::CH) {
+                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+                *reinterpret_cast<u32x4*>(&sQ[buf][row * C::P + col]) = qreg[t];
+                *reinterpret_cast<u32x4*>(&sdO[buf][row * C::P + col]) = oreg[t];
+            }
+        }
+        if (tid < BLK) {
+            sL[buf][tid] = lreg * kLog2e;  // -inf stays -inf
+            sDl[buf][tid] = dreg;
+        }
+    };
+
+    if (len > 0) {
+        load_block(a.row_idx[entry(0)]);
+        store_block(0);
+    }
+    __syncthreads();
+    const float c2 = a.scale_log2;
+    for (int st = 0; st < len; ++st) {
+        const int buf = st & 1;
+        const int e = entry(st);
         const int qb = a.row_idx[e];
         const bool masked = a.kind_t[e] != TILE_FULL;
-        const int64_t row0 = (int64_t)qb * BLK;
-        __syncthreads();  // every wave is done with the previous query block
-        stage_both<D, BLK>(q + base, row0, a.ss, sQ, sQt, tid);
-        stage_both<D, BLK>(dout + base, row0, a.ss, sdO, sdOt, tid);
-        for (int t = tid; t < BLK; t += C::NT) {
-            float L = lse[rowbase + row0 + t];
-            sL[t] = L * kLog2e;  // -inf stays -inf
-            sDelta[t] = delta[rowbase + row0 + t];
-        }
-        __syncthreads();
+        const int i0 = qb * BLK;
+        if (st + 1 < len) load_block(a.row_idx[entry(st + 1)]);
+        const uint16_t* tQ = sQ[buf];
+        const uint16_t* tO = sdO[buf];
 
-        // S and dP for the 16-query blocks: x[qblk][t] is query 16*qblk + 4g + t, key j
-        f32x4 p[C::QB], ds[C::QB];
+        // S and dP: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
+        f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
 #pragma unroll
         for (int qblk = 0; qblk < C::QB; ++qblk) {
-            f32x4 s = zero4(), dp = zero4();
+            bf16x8 qa[C::KS], oa[C::KS];
 #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
-                bf16x8 qa = ld_bf16x8(sQ + (qblk * 16 + r) * C::RP + ks * 32 + 8 * g);
-                bf16x8 oa = ld_bf16x8(sdO + (qblk * 16 + r) * C::RP + ks * 32 + 8 * g);
-                s = mfma_16x16x32(qa, kf[ks], s);
-                dp = mfma_16x16x32(oa, vf[ks], dp);
+                qa[ks] = ld_bf16x8(tQ + (qblk * 16 + r) * C::P + ks * 32 + 8 * g);
+                oa[ks] = ld_bf16x8(tO + (qblk * 16 + r) * C::P + ks * 32 + 8 * g);
             }
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int qi = qblk * 16 + 4 * g + t;
-                const float L = sL[qi];
-                bool on = true;
-                if (masked) on = attended(a.pattern, part, a.l, a.c, (int)row0 + qi, j);
-                const float pv = on ? exp2_fast(s[t] * a.scale_log2 - L) : 0.f;
-                p[qblk][t] = pv;
-                ds[qblk][t] = pv * (dp[t] - sDelta[qi]);
+            for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                f32x4 sacc = zero4(), dpacc = zero4();
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
+                    dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
+                }
+                p[kbw][qblk] = sacc;
+                ds[kbw][qblk] = dpacc;
+            }
+        }
+#pragma unroll
+        for (int kbw = 0; kbw < C::KBW; ++kbw) {
+            uint64_t bits = ~0ull;
+            if (masked) bits = col_mask(mp, key0 + 16 * kbw + r, i0, summary[kbw]) >> (4 * g);
+#pragma unroll
+            for (int qblk = 0; qblk < C::QB; ++qblk) {
+                const f32x4 L = *reinterpret_cast<const f32x4*>(&sL[buf][qblk * 16 + 4 * g]);
+                const f32x4 Dl = *reinterpret_cast<const f32x4*>(&sDl[buf][qblk * 16 + 4 * g]);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const bool on = (bits >> (16 * qblk + t)) & 1ull;
+                    const float pv = on ? exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t])) : 0.f;
+                    p[kbw][qblk][t] = pv;
+                    ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
+                }
             }
         }
 
-        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries
+        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries;
+        // dO^T and Q^T are read transposed from the row-major tiles
 #pragma unroll
         for (int qc = 0; qc < C::QC; ++qc) {
-            bf16x8 pb = pack_chunk<BLK>(p, qc);
-            bf16x8 sb = pack_chunk<BLK>(ds, qc);
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                bf16x8 oa = ld_chunk_T<BLK>(sdOt + (db * 16 + r) * C::TP, qc, g);
-                bf16x8 qa = ld_chunk_T<BLK>(sQt + (db * 16 + r) * C::TP, qc, g);
-                dvacc[db] = mfma_16x16x32(oa, pb, dvacc[db]);
-                dkacc[db] = mfma_16x16x32(qa, sb, dkacc[db]);
+                bf16x8 oT, qT;
+                if constexpr (BLK >= 32) {
+                    oT = ld_tr_operand(tO, C::P, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                    qT = ld_tr_operand(tQ, C::P, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                } else {
+                    u32x2 lo = ld_tr16(tO + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
+                    u32x2 lq = ld_tr16(tQ + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
+                    oT = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
+                    qT = __builtin_bit_cast(bf16x8, u32x4{lq.x, lq.y, 0u, 0u});
+                }
+#pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                    bf16x8 pb, sb;
+                    if constexpr (BLK >= 32) {
+                        pb = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
+                        sb = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                    } else {
+                        pb = pack_bf16x8(p[kbw][0], zero4());
+                        sb = pack_bf16x8(ds[kbw][0], zero4());
+                    }
+                    dvacc[kbw][db] = mfma_16x16x32(oT, pb, dvacc[kbw][db]);
+                    dkacc[kbw][db] = mfma_16x16x32(qT, sb, dkacc[kbw][db]);
+                }
             }
         }
 
         // dS to LDS as [query][key] for the dQ product
 #pragma unroll
-        for (int qblk = 0; qblk < C::QB; ++qblk)
+        for (int kbw = 0; kbw < C::KBW; ++kbw)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                sdS[(qblk * 16 + 4 * g + t) * C::TP + w * 16 + r] = bf16_bits(ds[qblk][t]);
+            for (int qblk = 0; qblk < C::QB; ++qblk)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    sdS[(qblk * 16 + 4 * g + t) * C::SP + w * C::KW + 16 * kbw + r] = bf16_bits(ds[kbw][qblk][t]);
         __syncthreads();
 
-        // dQ rows 16w .. 16w+15 of this query block: dS[q][:] K[:][d]
-        f32x4 dqa[C::DB];
+        // dQ rows w*QRW .. of this query block: dS[q][:] K[:][d], K read transposed
+        f32x4 dqa[C::QBQ][C::DB];
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db) dqa[db] = zero4();
+        for (int u = 0; u < C::QBQ; ++u)
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) dqa[u][db] = zero4();
+        // With 16-key blocks only lane groups g < 2 carry keys; the others
+        // read in-bounds rows and are zeroed by a data mask afterwards: the
+        // transposing LDS read is always issued with every lane active.
+        const int gk = (BLK >= 32) ? g : (g & 1);
+        const uint32_t keep = (BLK >= 32 || g < 2) ? 0xffffffffu : 0u;
 #pragma unroll
         for (int kc = 0; kc < C::QC; ++kc) {
-            bf16x8 sa;
-            if (BLK >= 32 || g < 2) sa = ld_bf16x8(sdS + (w * 16 + r) * C::TP + kc * 32 + 8 * g);
-            else sa = zero_bf16x8();
+            bf16x8 sa[C::QBQ];
+#pragma unroll
+            for (int u = 0; u < C::QBQ; ++u)
+                sa[u] = mask_bf16x8(ld_bf16x8(sdS + (w * C::QRW + 16 * u + r) * C::SP + kc * 32 + 8 * gk), keep);
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                bf16x8 kt;
-                if (BLK >= 32 || g < 2) kt = ld_bf16x8(sKt + (db * 16 + r) * C::TP + kc * 32 + 8 * g);
-                else kt = zero_bf16x8();
-                dqa[db] = mfma_16x16x32(sa, kt, dqa[db]);
+                const bf16x8 kt =
+                    mask_bf16x8(ld_tr_operand(sK, C::P, kc * 32 + 8 * gk, kc * 32 + 8 * gk + 4, db * 16, r), keep);
+#pragma unroll
+                for (int u = 0; u < C::QBQ; ++u) dqa[u][db] = mfma_16x16x32(sa[u], kt, dqa[u][db]);
             }
         }
-        float* dst = dq_acc + (rowbase + row0 + w * 16) * D;
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
+        for (int u = 0; u < C::QBQ; ++u) {
+            float* dst = dq_acc + (rowbase + i0 + w * C::QRW + 16 * u) * D;
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                atomicAdd(dst + (4 * g + t) * D + db * 16 + r, a.scale * dqa[db][t]);
+            for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    atomicAdd(dst + (4 * g + t) * D + db * 16 + r, a.scale * dqa[u][db][t]);
+        }
+
+        if (st + 1 < len) store_block(buf ^ 1);
+        __syncthreads();
     }
 
-    // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key j
-    uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
-    uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
+    // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db) {
-        *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[db]);
-        *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[db] * a.scale);
+    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+        const int j = key0 + 16 * kbw + r;
+        uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
+        uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {
+            *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[kbw][db]);
+            *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
+        }
     }
 }
 

@@ -14,6 +14,7 @@
 //
 // fp32 path: one thread per query row, same online softmax on the VALU.
 #include "sa_internal.h"
+#include "sa_mask.h"
 #include "sa_mfma.h"
 
 namespace sa {
@@ -25,180 +26,186 @@ namespace {
 // ---------------------------------------------------------------------------
 template <int D, int BLK>
 struct FwdCfg {
-    static constexpr int NW = BLK / 16;          // waves per workgroup
-    static constexpr int NT = NW * 64;           // threads
-    static constexpr int KS = D / 32;            // 32-deep steps over d for S
-    static constexpr int KB = BLK / 16;          // 16-key blocks per tile
-    static constexpr int KC = (BLK + 31) / 32;   // 32-key chunks for P V
-    static constexpr int DB = D / 16;            // 16-wide d blocks of O
-    static constexpr int KP = D + 8;             // sK row pitch (elements)
-    static constexpr int VP = BLK + 8;           // sVt row pitch (elements)
-    static constexpr int KCH = (BLK * D / 8 + NT - 1) / NT;        // 16-byte K chunks per thread
-    static constexpr int VU = ((BLK / 2) * (D / 8) + NT - 1) / NT;  // V (pair, chunk) units per thread
+    static constexpr int RW = BLK < 32 ? BLK : 32;  // query rows per wave
+    static constexpr int QBW = RW / 16;             // 16-row blocks per wave
+    static constexpr int NW = BLK / RW;             // waves per workgroup
+    static constexpr int NT = NW * 64;              // threads
+    static constexpr int KS = D / 32;               // 32-deep steps over d for S
+    static constexpr int KB = BLK / 16;             // 16-key blocks per tile
+    static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
+    static constexpr int DB = D / 16;               // 16-wide d blocks of O
+    static constexpr int P = D + 8;                 // LDS row pitch of K and V tiles (elements)
+    static constexpr int CH = BLK * D / 8;          // 16-byte chunks per K (or V) tile
+    static constexpr int CPT = (CH + NT - 1) / NT;  // chunks per thread per tensor
 };
 
 template <int D, int BLK>
-__global__ void __launch_bounds__(BLK * 4)
+__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
     using C = FwdCfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t sK[BLK * C::KP];
-    __shared__ __attribute__((aligned(16))) uint16_t sVt[D * C::VP];
+    // K and V tiles, row-major, double-buffered: one barrier per key block
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * C::P];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * C::P];
 
     const int qb = a.nq - 1 - (int)blockIdx.x;  // longest rows first
     const int h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    const int part = part_of_head(a.mode, h);
+    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-    const int i = qb * BLK + w * 16 + r;  // this lane's query row
+    const int row0 = qb * BLK + w * C::RW;  // first query row of this wave
 
-    bf16x8 qf[C::KS];
+    bf16x8 qf[C::QBW][C::KS];
+    f32x4 oacc[C::QBW][C::DB];
+    float m_run[C::QBW], l_run[C::QBW];
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) qf[ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
-
-    f32x4 oacc[C::DB];
+    for (int u = 0; u < C::QBW; ++u) {
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db) oacc[db] = zero4();
-    float m_run = -INFINITY, l_run = 0.f;
+        for (int ks = 0; ks < C::KS; ++ks)
+            qf[u][ks] = ld_bf16x8(q + base + (int64_t)(row0 + 16 * u + r) * a.ss + ks * 32 + 8 * g);
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) oacc[u][db] = zero4();
+        m_run[u] = -INFINITY;
+        l_run[u] = 0.f;
+    }
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
     const int e0 = a.row_ptr[rp], e1 = a.row_ptr[rp + 1];
 
-    // register staging of the next K / V block
-    u32x4 kreg[C::KCH];
-    u32x4 vreg[C::VU][2];
+    u32x4 kreg[C::CPT], vreg[C::CPT];
     auto load_block = [&](int kb) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
 #pragma unroll
-        for (int t = 0; t < C::KCH; ++t) {
-            int ch = tid + t * C::NT;
-            if (ch < BLK * D / 8) {
-                int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+        for (int t = 0; t < C::CPT; ++t) {
+            const int ch = tid + t * C::NT;
+            if (C::CH % C::NT == 0 || ch < C::CH) {
+                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
                 kreg[t] = *reinterpret_cast<const u32x4*>(k + kbase + (int64_t)row * a.ss + col);
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < C::VU; ++t) {
-            int u = tid + t * C::NT;
-            if (u < (BLK / 2) * (D / 8)) {
-                int pr = u / (D / 8), col = (u % (D / 8)) * 8;
-                vreg[t][0] = *reinterpret_cast<const u32x4*>(v + kbase + (int64_t)(2 * pr) * a.ss + col);
-                vreg[t][1] = *reinterpret_cast<const u32x4*>(v + kbase + (int64_t)(2 * pr + 1) * a.ss + col);
+                vreg[t] = *reinterpret_cast<const u32x4*>(v + kbase + (int64_t)row * a.ss + col);
             }
         }
     };
-    auto store_block = [&]() {
+    auto store_block = [&](int buf) {
 #pragma unroll
-        for (int t = 0; t < C::KCH; ++t) {
-            int ch = tid + t * C::NT;
-            if (ch < BLK * D / 8) {
-                int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-                *reinterpret_cast<u32x4*>(sK + row * C::KP + col) = kreg[t];
-            }
-        }
-        uint32_t* sVt32 = reinterpret_cast<uint32_t*>(sVt);
-#pragma unroll
-        for (int t = 0; t < C::VU; ++t) {
-            int u = tid + t * C::NT;
-            if (u < (BLK / 2) * (D / 8)) {
-                int pr = u / (D / 8), col = (u % (D / 8)) * 8;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    uint32_t lo = (vreg[t][0][e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                    uint32_t hi = (vreg[t][1][e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                    sVt32[((col + e) * C::VP) / 2 + pr] = lo | (hi << 16);
-                }
+        for (int t = 0; t < C::CPT; ++t) {
+            const int ch = tid + t * C::NT;
+            if (C::CH % C::NT == 0 || ch < C::CH) {
+                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+                *reinterpret_cast<u32x4*>(&sK[buf][row * C::P + col]) = kreg[t];
+                *reinterpret_cast<u32x4*>(&sV[buf][row * C::P + col]) = vreg[t];
             }
         }
     };
 
-    if (e0 < e1) load_block(a.col_idx[e0]);
+    if (e0 < e1) {
+        load_block(a.col_idx[e0]);
+        store_block(0);
+    }
+    __syncthreads();
+    const float c2 = a.scale_log2;
     for (int e = e0; e < e1; ++e) {
+        const int buf = (e - e0) & 1;
         const int kb = a.col_idx[e];
         const bool masked = a.kind[e] != TILE_FULL;
-        __syncthreads();  // previous block's LDS reads are done
-        store_block();
-        __syncthreads();
-        if (e + 1 < e1) load_block(a.col_idx[e + 1]);
+        if (e + 1 < e1) load_block(a.col_idx[e + 1]);  // in flight during this block's math
+        const uint16_t* tK = sK[buf];
+        const uint16_t* tV = sV[buf];
 
-        // S^T blocks: s[kblk][t] = score of key kb*BLK + 16*kblk + 4g + t against row i
-        f32x4 s[C::KB];
+        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(kb*BLK + 16 kb16 + 4g + t)
+        f32x4 s[C::QBW][C::KB];
 #pragma unroll
         for (int kblk = 0; kblk < C::KB; ++kblk) {
-            s[kblk] = zero4();
+            bf16x8 kf[C::KS];
 #pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) {
-                bf16x8 kf = ld_bf16x8(sK + (kblk * 16 + r) * C::KP + ks * 32 + 8 * g);
-                s[kblk] = mfma_16x16x32(kf, qf[ks], s[kblk]);
+            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = ld_bf16x8(tK + (kblk * 16 + r) * C::P + ks * 32 + 8 * g);
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) {
+                s[u][kblk] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
             }
         }
-        float mloc = -INFINITY;
+
+        bf16x8 pf[C::QBW][C::KC];
 #pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
+        for (int u = 0; u < C::QBW; ++u) {
+            if (masked) {
+                const int j0 = kb * BLK;
+                const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+                const uint64_t bits = row_mask(mp, row0 + 16 * u + r, j0, sum) >> (4 * g);
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                float x = s[kblk][t] * a.scale_log2;
-                if (masked) {
-                    int j = kb * BLK + kblk * 16 + 4 * g + t;
-                    if (!attended(a.pattern, part, a.l, a.c, i, j)) x = -INFINITY;
+                for (int kblk = 0; kblk < C::KB; ++kblk)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (!((bits >> (16 * kblk + t)) & 1ull)) s[u][kblk][t] = -INFINITY;
+            }
+            // running max in raw score units (the scale is positive)
+            float mloc = -INFINITY;
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk)
+                mloc = fmaxf(fmaxf(mloc, fmaxf(s[u][kblk][0], s[u][kblk][1])), fmaxf(s[u][kblk][2], s[u][kblk][3]));
+            mloc = max_over_g(mloc);
+            const float m_new = fmaxf(m_run[u], mloc);
+            // rows with nothing attended so far keep m = -inf; 0 as reference
+            // gives p = 0 and alpha = 0 without a branch around the MFMAs
+            const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
+            const float neg = -m_ref * c2;
+            m_run[u] = m_new;
+            float psum = 0.f;
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float pv = exp2_fast(fmaf(s[u][kblk][t], c2, neg));
+                    s[u][kblk][t] = pv;
+                    psum += pv;
                 }
-                s[kblk][t] = x;
-                mloc = fmaxf(mloc, x);
+            l_run[u] = l_run[u] * alpha + psum;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
+                else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
             }
         }
-        mloc = max_over_g(mloc);
-        const float m_new = fmaxf(m_run, mloc);
-        // A row with nothing attended so far keeps m = -inf; using 0 as its
-        // reference gives p = 0 and alpha = 0 without any branch around the MFMAs.
-        const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2_fast(m_run - m_ref);
-        m_run = m_new;
-        float psum = 0.f;
-#pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                float p = exp2_fast(s[kblk][t] - m_ref);
-                s[kblk][t] = p;
-                psum += p;
-            }
-        }
-        l_run = l_run * alpha + psum;
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) oacc[db] *= alpha;
 
+        // O^T += V^T P^T, V^T read transposed straight from the row-major tile
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
-            bf16x8 pf;
-            if constexpr (BLK >= 32) pf = pack_bf16x8(s[2 * kc], s[2 * kc + 1]);
-            else pf = pack_bf16x8(s[0], zero4());
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                const uint16_t* row = sVt + (db * 16 + r) * C::VP + kc * 32 + 4 * g;
                 bf16x8 vf;
                 if constexpr (BLK >= 32) {
-                    vf = ld_bf16x4x2(row, row + 16);
+                    vf = ld_tr_operand(tV, C::P, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
                 } else {
-                    u32x2 lo = *reinterpret_cast<const u32x2*>(row);
+                    u32x2 lo = ld_tr16(tV + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
                     vf = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
                 }
-                oacc[db] = mfma_16x16x32(vf, pf, oacc[db]);
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vf, pf[u][kc], oacc[u][db]);
             }
         }
+
+        if (e + 1 < e1) store_block(buf ^ 1);
+        __syncthreads();
     }
 
-    const float l_tot = sum_over_g(l_run);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    uint16_t* orow = o + base + (int64_t)i * a.ss;
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db) {
-        uint2 bits = pack_bf16x4_bits(oacc[db] * inv);
-        *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = bits;
-    }
-    if (g == 0) {
-        float val = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
-        lse[((int64_t)b * a.heads + h) * a.n + i] = val;
+    for (int u = 0; u < C::QBW; ++u) {
+        const int i = row0 + 16 * u + r;
+        const float l_tot = sum_over_g(l_run[u]);
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        uint16_t* orow = o + base + (int64_t)i * a.ss;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+            *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pack_bf16x4_bits(oacc[u][db] * inv);
+        if (g == 0) {
+            const float val = l_tot > 0.f ? m_run[u] * a.scale + __logf(l_tot) : -INFINITY;
+            lse[((int64_t)b * a.heads + h) * a.n + i] = val;
+        }
     }
 }
 

@@ -26,8 +26,9 @@ struct AttnArgs {
     int32_t n, nq, block;  // n < 2^31
     int32_t batch, heads, d;
     int64_t sb, sh, ss;    // element strides: batch, head, sequence
-    float scale;           // softmax scale
+    float scale;           // softmax scale (> 0)
     float scale_log2;      // scale * log2(e)
+    uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
     const int32_t* row_ptr;
     const int32_t* col_idx;
     const uint8_t* kind;

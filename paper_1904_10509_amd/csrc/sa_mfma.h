@@ -50,6 +50,13 @@ __device__ inline bf16x8 ld_bf16x4x2(const uint16_t* lo, const uint16_t* hi) {
 
 __device__ inline bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u}); }
 
+// x with every bit cleared unless keep is all ones (a data mask, not a branch).
+__device__ inline bf16x8 mask_bf16x8(bf16x8 x, uint32_t keep) {
+    u32x4 w = __builtin_bit_cast(u32x4, x);
+    w &= u32x4{keep, keep, keep, keep};
+    return __builtin_bit_cast(bf16x8, w);
+}
+
 // Round-to-nearest-even fp32 -> bf16 of two D results, as one operand.
 __device__ inline bf16x8 pack_bf16x8(f32x4 lo, f32x4 hi) {
     bf16x4 a = __builtin_convertvector(lo, bf16x4);
@@ -75,14 +82,44 @@ __device__ inline int chunk_row(int g, int t) { return t < 4 ? 4 * g + t : 16 + 
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Max / sum over the four lanes that share r = lane % 16.
+// Max / sum over the four lanes that share r = lane % 16, with the gfx950
+// row-swap permutes (16-lane rows 0<->1, 2<->3, then the two 32-lane halves).
 __device__ inline float max_over_g(float x) {
-    x = fmaxf(x, __shfl_xor(x, 16));
-    return fmaxf(x, __shfl_xor(x, 32));
+    auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ inline float sum_over_g(float x) {
-    x += __shfl_xor(x, 16);
-    return x + __shfl_xor(x, 32);
+    auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Transposing LDS read (ds_read_b64_tr_b16).  Within each 16-lane row of the
+// wave, output lane i receives element (i mod 4) of the 8 bytes addressed by
+// input lane 4u + i/4, as its item u (u = 0..3).  Issue it with every lane
+// active: under a partial exec mask the inactive lanes' destination registers
+// did not keep their old contents in testing.  So if lane L of the row
+// points at &T[row0 + L/4][col0 + 4 (L mod 4)] of a row-major bf16 tile T,
+// lane i receives T[row0 + u][col0 + i] for u = 0..3: four rows of one column.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ inline u32x2 ld_tr16(const uint16_t* lds_ptr) {
+    s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(lds_ptr));
+    return __builtin_bit_cast(u32x2, v);
+}
+
+// B/A operand over 32 rows (k = 8g + t) of column c0 + (lane % 16) of a
+// row-major tile with pitch `pitch`: rows row0 + kmap(g, t) where the first
+// four t come from rows base_lo + u and the last four from base_hi + u.
+__device__ inline bf16x8 ld_tr_operand(const uint16_t* tile, int pitch, int base_lo, int base_hi,
+                                       int col0, int r) {
+    const int off = (r >> 2) * pitch + col0 + 4 * (r & 3);
+    u32x2 lo = ld_tr16(tile + base_lo * pitch + off);
+    u32x2 hi = ld_tr16(tile + base_hi * pitch + off);
+    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
 }
 
 }  // namespace sa
