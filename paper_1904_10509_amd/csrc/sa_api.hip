@@ -2,7 +2,7 @@
 // status codes.  Nothing is enqueued unless every argument is valid.
 #include <math.h>
 
-#include "../../include/sparse_attn.h"
+#include "sparse_attn.h"
 #include "sa_internal.h"
 #include "sa_mask.h"
 

@@ -6,18 +6,24 @@
 //   dP   = dO V^T,  dS = P * (dP - D_i)
 //   dV   = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K
 //
-// bf16 path, three launches:
-//   1. pre:   D_i into the workspace, and the fp32 dQ accumulator cleared;
-//   2. dkdv:  one workgroup per (key block kb, head, batch), B/16 waves of 16
-//             keys each, walking the column view of the layout.  dK and dV
-//             stay in registers; the block's dQ contribution goes through
-//             LDS into fp32 atomics on the accumulator;
-//   3. dq:    the accumulator rounded to bf16 into dq.
+// bf16 path, three launches, no atomics (every output element has exactly
+// one writer, so results are reproducible bit for bit):
+//   1. pre:   D_i into the workspace;
+//   2. dq:    one workgroup per (head, query block, batch) walks the row view
+//             of the layout like the forward: S^T and dP^T recomputed, dS^T
+//             formed in registers and contracted with K into dQ;
+//   3. dkdv:  one workgroup per (head, key block, batch) walks the column
+//             view: S and dP recomputed, dV += P^T dO and dK += dS^T Q held in
+//             registers for the whole column.
+// The dq kernel repeats the S and dP products of the dkdv kernel; those two
+// extra products per block are the price of having no reduction across
+// workgroups.
 // fp32 path: the same quantities on the VALU, one thread per row for dq and
-// one thread per column for dk / dv, with no atomics.
+// one thread per column for dk / dv.
 #include "sa_internal.h"
 #include "sa_mask.h"
 #include "sa_mfma.h"
+#include "sa_tile.h"
 
 namespace sa {
 
@@ -26,55 +32,179 @@ namespace {
 // ---------------------------------------------------------------------------
 // shared pieces
 // ---------------------------------------------------------------------------
-struct Workspace {
-    float* dq_acc;  // [b, h, n, d]
-    float* delta;   // [b, h, n]
-};
-
-inline Workspace carve(void* ws, int64_t rows, int64_t d) {
-    Workspace w;
-    w.dq_acc = static_cast<float*>(ws);
-    w.delta = w.dq_acc + rows * d;
-    return w;
-}
-
-// One thread per row: D_i = sum_t dO[i,t] O[i,t] (fp32), and the dq
-// accumulator row cleared.
+// One thread per row: D_i = sum_t dO[i,t] O[i,t] (fp32).
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
-bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout,
-               float* __restrict__ delta, float* __restrict__ dq_acc) {
+bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, float* __restrict__ delta) {
     const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     if (row >= rows) return;
     const int64_t bh = row / a.n, i = row % a.n;
     const int64_t off = (bh / a.heads) * a.sb + (bh % a.heads) * a.sh + i * a.ss;
     float acc = 0.f;
-#pragma unroll 8
-    for (int t = 0; t < D; ++t) {
-        float x, y;
-        if constexpr (sizeof(T) == 2) {
-            x = bf16_to_f32(o[off + t]);
-            y = bf16_to_f32(dout[off + t]);
-        } else {
-            x = o[off + t];
-            y = dout[off + t];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int t = 0; t < D; t += 8) {
+            const u32x4 x = *reinterpret_cast<const u32x4*>(o + off + t);
+            const u32x4 y = *reinterpret_cast<const u32x4*>(dout + off + t);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc = fmaf(__uint_as_float(x[e] << 16), __uint_as_float(y[e] << 16), acc);
+                acc = fmaf(__uint_as_float(x[e] & 0xffff0000u), __uint_as_float(y[e] & 0xffff0000u), acc);
+            }
         }
-        acc = fmaf(x, y, acc);
+    } else {
+        for (int t = 0; t < D; ++t) acc = fmaf(o[off + t], dout[off + t], acc);
     }
     delta[row] = acc;
-    if (dq_acc) {
-        float4* dst = reinterpret_cast<float4*>(dq_acc + row * D);
+}
+
+// ---------------------------------------------------------------------------
+// bf16, matrix cores: dQ, row-parallel
+// ---------------------------------------------------------------------------
+template <int D, int BLK>
+struct DqCfg {
+    static constexpr int RW = BLK < 32 ? BLK : 32;  // query rows per wave
+    static constexpr int QBW = RW / 16;
+    static constexpr int NW = BLK / RW;
+    static constexpr int NT = NW * 64;
+    static constexpr int KS = D / 32;
+    static constexpr int KB = BLK / 16;
+    static constexpr int KC = (BLK + 31) / 32;
+    static constexpr int DB = D / 16;
+};
+
+template <int D, int BLK>
+__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
+bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                   const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
+                   const float* __restrict__ lse, const float* __restrict__ delta,
+                   uint16_t* __restrict__ dq) {
+    using C = DqCfg<D, BLK>;
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * D];
+
+    const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
+    const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
+    const int row0 = qb * BLK + w * C::RW;
+    const float c2 = a.scale_log2;
+
+    // this lane's query rows row0 + 16u + r: Q and dO as B operands, LSE (log2 units) and D
+    bf16x8 qf[C::QBW][C::KS], of[C::QBW][C::KS];
+    float L2[C::QBW], Dl[C::QBW];
+    f32x4 dqacc[C::QBW][C::DB];
 #pragma unroll
-        for (int t = 0; t < D / 4; ++t) dst[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int u = 0; u < C::QBW; ++u) {
+        const int i = row0 + 16 * u + r;
+#pragma unroll
+        for (int ks = 0; ks < C::KS; ++ks) {
+            qf[u][ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
+            of[u][ks] = ld_bf16x8(dout + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
+        }
+        L2[u] = lse[rowbase + i] * kLog2e;
+        Dl[u] = delta[rowbase + i];
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) dqacc[u][db] = zero4();
+    }
+
+    const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
+    const int e0 = a.row_ptr[rp], e1 = a.row_ptr[rp + 1];
+    auto load_block = [&](int kb, int buf) {
+        const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
+        load_tile_async<D, BLK, C::NW>(k + kbase, a.ss, sK[buf], w, lane);
+        load_tile_async<D, BLK, C::NW>(v + kbase, a.ss, sV[buf], w, lane);
+    };
+    if (e0 < e1) load_block(a.col_idx[e0], 0);
+    wait_tile_loads();
+    __syncthreads();
+    for (int e = e0; e < e1; ++e) {
+        const int buf = (e - e0) & 1;
+        const int kb = a.col_idx[e];
+        const bool masked = a.kind[e] != TILE_FULL;
+        if (e + 1 < e1) load_block(a.col_idx[e + 1], buf ^ 1);
+        const uint16_t* tK = sK[buf];
+        const uint16_t* tV = sV[buf];
+
+        // S^T and dP^T: x[u][kb16][t] for key kb*BLK + 16 kb16 + 4g + t, query row0 + 16u + r
+        f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
+#pragma unroll
+        for (int kblk = 0; kblk < C::KB; ++kblk) {
+            bf16x8 kf[C::KS], vf[C::KS];
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) {
+                kf[ks] = ld_row_swz<D>(tK, kblk * 16 + r, ks * 32 + 8 * g);
+                vf[ks] = ld_row_swz<D>(tV, kblk * 16 + r, ks * 32 + 8 * g);
+            }
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) {
+                s[u][kblk] = zero4();
+                dp[u][kblk] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+                    dp[u][kblk] = mfma_16x16x32(vf[ks], of[u][ks], dp[u][kblk]);
+                }
+            }
+        }
+        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - L2), masked
+        bf16x8 dsf[C::QBW][C::KC];
+#pragma unroll
+        for (int u = 0; u < C::QBW; ++u) {
+            uint64_t bits = ~0ull;
+            if (masked) {
+                const int j0 = kb * BLK;
+                const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+                bits = row_mask(mp, row0 + 16 * u + r, j0, sum) >> (4 * g);
+            }
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const bool on = (bits >> (16 * kblk + t)) & 1ull;
+                    const float pv = on ? exp2_fast(fmaf(s[u][kblk][t], c2, -L2[u])) : 0.f;
+                    s[u][kblk][t] = pv * (dp[u][kblk][t] - Dl[u]);
+                }
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if constexpr (BLK >= 32) dsf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
+                else dsf[u][kc] = pack_bf16x8(s[u][0], zero4());
+            }
+        }
+        // dQ^T += K^T dS^T, K^T read transposed from the row-major tile
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc) {
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                bf16x8 kt;
+                if constexpr (BLK >= 32) kt = ld_tr_swz<D>(tK, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
+                else kt = ld_tr_swz_half<D>(tK, 4 * g, db * 16, r);
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(kt, dsf[u][kc], dqacc[u][db]);
+            }
+        }
+        wait_tile_loads();
+        __syncthreads();
+    }
+
+    // this lane holds dQ^T at d = 16 db + 4g + t for query row0 + 16u + r
+#pragma unroll
+    for (int u = 0; u < C::QBW; ++u) {
+        uint16_t* drow = dq + base + (int64_t)(row0 + 16 * u + r) * a.ss;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+            *reinterpret_cast<uint2*>(drow + db * 16 + 4 * g) = pack_bf16x4_bits(dqacc[u][db] * a.scale);
     }
 }
 
 // ---------------------------------------------------------------------------
-// bf16, matrix cores
+// bf16, matrix cores: dK and dV, column-parallel
 // ---------------------------------------------------------------------------
 template <int D, int BLK>
-struct BwdCfg {
+struct DkvCfg {
     static constexpr int KW = BLK < 32 ? BLK : 32;  // keys per wave
     static constexpr int KBW = KW / 16;             // 16-key blocks per wave
     static constexpr int NW = BLK / KW;             // waves
@@ -83,12 +213,6 @@ struct BwdCfg {
     static constexpr int QB = BLK / 16;             // 16-query blocks per tile
     static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
-    static constexpr int P = D + 8;                 // pitch of row-major [BLK][D] tiles
-    static constexpr int SP = BLK + 8;              // pitch of dS [query][key]
-    static constexpr int CH = BLK * D / 8;          // 16-byte chunks per Q (or dO) tile
-    static constexpr int CPT = (CH + NT - 1) / NT;
-    static constexpr int QRW = BLK / NW;            // dQ rows per wave
-    static constexpr int QBQ = QRW / 16;            // their 16-row blocks
 };
 
 template <int D, int BLK>
@@ -96,23 +220,20 @@ __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                      const float* __restrict__ lse, const float* __restrict__ delta,
-                     float* __restrict__ dq_acc, uint16_t* __restrict__ dk,
-                     uint16_t* __restrict__ dv) {
-    using C = BwdCfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t sQ[2][BLK * C::P];
-    __shared__ __attribute__((aligned(16))) uint16_t sdO[2][BLK * C::P];
-    __shared__ __attribute__((aligned(16))) uint16_t sK[BLK * C::P];
-    __shared__ __attribute__((aligned(16))) uint16_t sdS[BLK * C::SP];
-    __shared__ __attribute__((aligned(16))) float sL[2][BLK];
-    __shared__ __attribute__((aligned(16))) float sDl[2][BLK];
+                     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+    using C = DkvCfg<D, BLK>;
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[2][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sdO[2][BLK * D];
+    __shared__ __attribute__((aligned(16))) float sL[2][64];
+    __shared__ __attribute__((aligned(16))) float sDl[2][64];
 
-    const int kb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const int h = blockIdx.x, kb = blockIdx.y, b = blockIdx.z;  // low key blocks have the longest columns
     const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
     MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-    const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;  // LSE / D / dq_acc rows
-    const int key0 = kb * BLK + w * C::KW;                      // first key of this wave
+    const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
+    const int key0 = kb * BLK + w * C::KW;  // first key of this wave
 
     // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
     bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
@@ -127,12 +248,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
         }
         summary[kbw] = a.pattern == FIXED && (j % a.l) >= a.l - a.c;
     }
-    // the key block row-major, for the transposed operand of dQ = dS K
-    for (int ch = tid; ch < C::CH; ch += C::NT) {
-        const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-        *reinterpret_cast<u32x4*>(&sK[row * C::P + col]) =
-            *reinterpret_cast<const u32x4*>(k + base + (int64_t)(kb * BLK + row) * a.ss + col);
-    }
 
     f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
 #pragma unroll
@@ -145,59 +260,24 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
 
     const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
     const int e0 = a.col_ptr[cp], e1 = a.col_ptr[cp + 1];
-    const int len = e1 - e0;
-    // Start each column at its own offset so that the workgroups running at
-    // the same time add into different dQ rows.
-    const int rot = len > 0 ? (int)(((int64_t)kb * 37 + h * 11) % len) : 0;
-    auto entry = [&](int s) { int x = s + rot; return e0 + (x >= len ? x - len : x); };
-
-    u32x4 qreg[C::CPT], oreg[C::CPT];
-    float lreg = 0.f, dreg = 0.f;
-    auto load_block = [&](int qb) {
+    auto load_block = [&](int qb, int buf) {
         const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
-#pragma unroll
-        for (int t = 0; t < C::CPT; ++t) {
-            const int ch = tid + t * C::NT;
-            if (C::CH % C::NT == 0 || ch < C::CH) {
-                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-                qreg[t] = *reinterpret_cast<const u32x4*>(q + qbase + (int64_t)row * a.ss + col);
-                oreg[t] = *reinterpret_cast<const u32x4*>(dout + qbase + (int64_t)row * a.ss + col);
-            }
-        }
-        if (tid < BLK) {
-            lreg = lse[rowbase + (int64_t)qb * BLK + tid];
-            dreg = delta[rowbase + (int64_t)qb * BLK + tid];
-        }
-    };
-    auto store_block = [&](int buf) {
-#pragma unroll
-        for (int t = 0; t < C::CPT; ++t) {
-            const int ch = tid + t * C::NT;
-            if (C::CH % C::NT == 0 || ch < C::CH) {
-                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-                *reinterpret_cast<u32x4*>(&sQ[buf][row * C::P + col]) = qreg[t];
-                *reinterpret_cast<u32x4*>(&sdO[buf][row * C::P + col]) = oreg[t];
-            }
-        }
-        if (tid < BLK) {
-            sL[buf][tid] = lreg * kLog2e;  // -inf stays -inf
-            sDl[buf][tid] = dreg;
-        }
+        load_tile_async<D, BLK, C::NW>(q + qbase, a.ss, sQ[buf], w, lane);
+        load_tile_async<D, BLK, C::NW>(dout + qbase, a.ss, sdO[buf], w, lane);
+        load_row_stats_async(lse + rowbase + (int64_t)qb * BLK, BLK, sL[buf], w, lane);
+        load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[buf], w, lane);
     };
 
-    if (len > 0) {
-        load_block(a.row_idx[entry(0)]);
-        store_block(0);
-    }
+    if (e0 < e1) load_block(a.row_idx[e0], 0);
+    wait_tile_loads();
     __syncthreads();
     const float c2 = a.scale_log2;
-    for (int st = 0; st < len; ++st) {
-        const int buf = st & 1;
-        const int e = entry(st);
+    for (int e = e0; e < e1; ++e) {
+        const int buf = (e - e0) & 1;
         const int qb = a.row_idx[e];
         const bool masked = a.kind_t[e] != TILE_FULL;
         const int i0 = qb * BLK;
-        if (st + 1 < len) load_block(a.row_idx[entry(st + 1)]);
+        if (e + 1 < e1) load_block(a.row_idx[e + 1], buf ^ 1);
         const uint16_t* tQ = sQ[buf];
         const uint16_t* tO = sdO[buf];
 
@@ -208,8 +288,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
             bf16x8 qa[C::KS], oa[C::KS];
 #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
-                qa[ks] = ld_bf16x8(tQ + (qblk * 16 + r) * C::P + ks * 32 + 8 * g);
-                oa[ks] = ld_bf16x8(tO + (qblk * 16 + r) * C::P + ks * 32 + 8 * g);
+                qa[ks] = ld_row_swz<D>(tQ, qblk * 16 + r, ks * 32 + 8 * g);
+                oa[ks] = ld_row_swz<D>(tO, qblk * 16 + r, ks * 32 + 8 * g);
             }
 #pragma unroll
             for (int kbw = 0; kbw < C::KBW; ++kbw) {
@@ -234,7 +314,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const bool on = (bits >> (16 * qblk + t)) & 1ull;
-                    const float pv = on ? exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t])) : 0.f;
+                    const float pv = on ? exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t] * kLog2e)) : 0.f;
                     p[kbw][qblk][t] = pv;
                     ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
                 }
@@ -249,13 +329,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
             for (int db = 0; db < C::DB; ++db) {
                 bf16x8 oT, qT;
                 if constexpr (BLK >= 32) {
-                    oT = ld_tr_operand(tO, C::P, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
-                    qT = ld_tr_operand(tQ, C::P, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                    oT = ld_tr_swz<D>(tO, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                    qT = ld_tr_swz<D>(tQ, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
                 } else {
-                    u32x2 lo = ld_tr16(tO + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
-                    u32x2 lq = ld_tr16(tQ + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
-                    oT = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
-                    qT = __builtin_bit_cast(bf16x8, u32x4{lq.x, lq.y, 0u, 0u});
+                    oT = ld_tr_swz_half<D>(tO, 4 * g, db * 16, r);
+                    qT = ld_tr_swz_half<D>(tQ, 4 * g, db * 16, r);
                 }
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
@@ -272,53 +350,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
                 }
             }
         }
-
-        // dS to LDS as [query][key] for the dQ product
-#pragma unroll
-        for (int kbw = 0; kbw < C::KBW; ++kbw)
-#pragma unroll
-            for (int qblk = 0; qblk < C::QB; ++qblk)
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    sdS[(qblk * 16 + 4 * g + t) * C::SP + w * C::KW + 16 * kbw + r] = bf16_bits(ds[kbw][qblk][t]);
-        __syncthreads();
-
-        // dQ rows w*QRW .. of this query block: dS[q][:] K[:][d], K read transposed
-        f32x4 dqa[C::QBQ][C::DB];
-#pragma unroll
-        for (int u = 0; u < C::QBQ; ++u)
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) dqa[u][db] = zero4();
-        // With 16-key blocks only lane groups g < 2 carry keys; the others
-        // read in-bounds rows and are zeroed by a data mask afterwards: the
-        // transposing LDS read is always issued with every lane active.
-        const int gk = (BLK >= 32) ? g : (g & 1);
-        const uint32_t keep = (BLK >= 32 || g < 2) ? 0xffffffffu : 0u;
-#pragma unroll
-        for (int kc = 0; kc < C::QC; ++kc) {
-            bf16x8 sa[C::QBQ];
-#pragma unroll
-            for (int u = 0; u < C::QBQ; ++u)
-                sa[u] = mask_bf16x8(ld_bf16x8(sdS + (w * C::QRW + 16 * u + r) * C::SP + kc * 32 + 8 * gk), keep);
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                const bf16x8 kt =
-                    mask_bf16x8(ld_tr_operand(sK, C::P, kc * 32 + 8 * gk, kc * 32 + 8 * gk + 4, db * 16, r), keep);
-#pragma unroll
-                for (int u = 0; u < C::QBQ; ++u) dqa[u][db] = mfma_16x16x32(sa[u], kt, dqa[u][db]);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < C::QBQ; ++u) {
-            float* dst = dq_acc + (rowbase + i0 + w * C::QRW + 16 * u) * D;
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    atomicAdd(dst + (4 * g + t) * D + db * 16 + r, a.scale * dqa[u][db][t]);
-        }
-
-        if (st + 1 < len) store_block(buf ^ 1);
+        wait_tile_loads();
         __syncthreads();
     }
 
@@ -334,20 +366,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
             *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
         }
     }
-}
-
-template <int D>
-__global__ void __launch_bounds__(256)
-bwd_dq_convert_kernel(AttnArgs a, const float* __restrict__ dq_acc, uint16_t* __restrict__ dq) {
-    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // one thread per 4 elements
-    const int64_t rows = (int64_t)a.batch * a.heads * a.n;
-    if (idx >= rows * (D / 4)) return;
-    const int64_t row = idx / (D / 4);
-    const int c4 = (int)(idx % (D / 4)) * 4;
-    const int64_t bh = row / a.n, i = row % a.n;
-    const int64_t off = (bh / a.heads) * a.sb + (bh % a.heads) * a.sh + i * a.ss + c4;
-    f32x4 x = *reinterpret_cast<const f32x4*>(dq_acc + row * D + c4);
-    *reinterpret_cast<uint2*>(dq + off) = pack_bf16x4_bits(x);
 }
 
 // ---------------------------------------------------------------------------
@@ -443,75 +461,70 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
 template <int D>
 hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const void* v,
                           const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                          void* dv, Workspace ws, hipStream_t stream) {
+                          void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     hipLaunchKernelGGL((bwd_pre_kernel<D, float>), dim3((unsigned)((rows + 255) / 256)), dim3(256),
-                       0, stream, a, (const float*)o, (const float*)dout, ws.delta, (float*)nullptr);
+                       0, stream, a, (const float*)o, (const float*)dout, delta);
     dim3 grid((unsigned)((a.n + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
-                       (const float*)k, (const float*)v, (const float*)dout, lse, ws.delta,
-                       (float*)dq);
+                       (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dq);
     hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
-                       (const float*)k, (const float*)v, (const float*)dout, lse, ws.delta,
-                       (float*)dk, (float*)dv);
+                       (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dk,
+                       (float*)dv);
     return hipGetLastError();
 }
 
 template <int D, int BLK>
 hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                           void* dv, Workspace ws, hipStream_t stream) {
+                           void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)((rows + 255) / 256)),
-                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, ws.delta,
-                       ws.dq_acc);
-    dim3 grid((unsigned)a.nq, (unsigned)a.heads, (unsigned)a.batch);
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), grid, dim3(BwdCfg<D, BLK>::NT), 0, stream,
+                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, delta);
+    dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
+                       (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                       (const uint16_t*)dout, lse, delta, (uint16_t*)dq);
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), grid, dim3(DkvCfg<D, BLK>::NT), 0, stream,
                        a, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse, ws.delta, ws.dq_acc, (uint16_t*)dk,
-                       (uint16_t*)dv);
-    const int64_t quads = rows * (D / 4);
-    hipLaunchKernelGGL((bwd_dq_convert_kernel<D>), dim3((unsigned)((quads + 255) / 256)), dim3(256),
-                       0, stream, a, ws.dq_acc, (uint16_t*)dq);
+                       (const uint16_t*)dout, lse, delta, (uint16_t*)dk, (uint16_t*)dv);
     return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, const void* v,
                              const void* o, const void* dout, const float* lse, void* dq,
-                             void* dk, void* dv, Workspace ws, hipStream_t stream) {
+                             void* dk, void* dv, float* delta, hipStream_t stream) {
     switch (a.block) {
-    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
     }
 }
 
 }  // namespace
 
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype) {
-    const int64_t rows = batch * heads * n;
-    const int64_t acc = dtype == 1 ? rows * d : 0;  // fp32 dq accumulator (bf16 path only)
-    return (size_t)((acc + rows) * (int64_t)sizeof(float));
+    (void)d;
+    (void)dtype;
+    return (size_t)(batch * heads * n * (int64_t)sizeof(float));  // D_i, one fp32 per row
 }
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
                       void* dv, void* workspace, hipStream_t stream) {
-    const int64_t rows = (int64_t)a.batch * a.heads * a.n;
+    float* delta = static_cast<float*>(workspace);
     if (dtype == 1) {
-        Workspace ws = carve(workspace, rows, a.d);
         switch (a.d) {
-        case 32: return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-        case 64: return launch_bwd_bf16_d<64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-        default: return launch_bwd_bf16_d<128>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+        case 32: return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+        case 64: return launch_bwd_bf16_d<64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+        default: return launch_bwd_bf16_d<128>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
         }
     }
-    Workspace ws = carve(workspace, rows, 0);
     switch (a.d) {
-    case 32: return launch_bwd_f32<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    case 64: return launch_bwd_f32<64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    default: return launch_bwd_f32<128>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    case 32: return launch_bwd_f32<32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    case 64: return launch_bwd_f32<64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    default: return launch_bwd_f32<128>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
     }
 }
 

@@ -16,6 +16,7 @@
 #include "sa_internal.h"
 #include "sa_mask.h"
 #include "sa_mfma.h"
+#include "sa_tile.h"
 
 namespace sa {
 
@@ -34,22 +35,21 @@ struct FwdCfg {
     static constexpr int KB = BLK / 16;             // 16-key blocks per tile
     static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
     static constexpr int DB = D / 16;               // 16-wide d blocks of O
-    static constexpr int P = D + 8;                 // LDS row pitch of K and V tiles (elements)
-    static constexpr int CH = BLK * D / 8;          // 16-byte chunks per K (or V) tile
-    static constexpr int CPT = (CH + NT - 1) / NT;  // chunks per thread per tensor
 };
 
+// grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
+// over the XCDs) share a query block index across heads, so with heads a
+// multiple of 8 each head stays on one XCD and its keys stay in that L2.
 template <int D, int BLK>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
     using C = FwdCfg<D, BLK>;
-    // K and V tiles, row-major, double-buffered: one barrier per key block
-    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * C::P];
-    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * C::P];
+    // K and V tiles, double-buffered: one barrier per key block
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * D];
 
-    const int qb = a.nq - 1 - (int)blockIdx.x;  // longest rows first
-    const int h = blockIdx.y, b = blockIdx.z;
+    const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
     const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
     MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
@@ -72,43 +72,21 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
     const int e0 = a.row_ptr[rp], e1 = a.row_ptr[rp + 1];
-
-    u32x4 kreg[C::CPT], vreg[C::CPT];
-    auto load_block = [&](int kb) {
+    auto load_block = [&](int kb, int buf) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-#pragma unroll
-        for (int t = 0; t < C::CPT; ++t) {
-            const int ch = tid + t * C::NT;
-            if (C::CH % C::NT == 0 || ch < C::CH) {
-                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-                kreg[t] = *reinterpret_cast<const u32x4*>(k + kbase + (int64_t)row * a.ss + col);
-                vreg[t] = *reinterpret_cast<const u32x4*>(v + kbase + (int64_t)row * a.ss + col);
-            }
-        }
-    };
-    auto store_block = [&](int buf) {
-#pragma unroll
-        for (int t = 0; t < C::CPT; ++t) {
-            const int ch = tid + t * C::NT;
-            if (C::CH % C::NT == 0 || ch < C::CH) {
-                const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-                *reinterpret_cast<u32x4*>(&sK[buf][row * C::P + col]) = kreg[t];
-                *reinterpret_cast<u32x4*>(&sV[buf][row * C::P + col]) = vreg[t];
-            }
-        }
+        load_tile_async<D, BLK, C::NW>(k + kbase, a.ss, sK[buf], w, lane);
+        load_tile_async<D, BLK, C::NW>(v + kbase, a.ss, sV[buf], w, lane);
     };
 
-    if (e0 < e1) {
-        load_block(a.col_idx[e0]);
-        store_block(0);
-    }
+    if (e0 < e1) load_block(a.col_idx[e0], 0);
+    wait_tile_loads();
     __syncthreads();
     const float c2 = a.scale_log2;
     for (int e = e0; e < e1; ++e) {
         const int buf = (e - e0) & 1;
         const int kb = a.col_idx[e];
         const bool masked = a.kind[e] != TILE_FULL;
-        if (e + 1 < e1) load_block(a.col_idx[e + 1]);  // in flight during this block's math
+        if (e + 1 < e1) load_block(a.col_idx[e + 1], buf ^ 1);  // lands during this block's math
         const uint16_t* tK = sK[buf];
         const uint16_t* tV = sV[buf];
 
@@ -118,7 +96,7 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
         for (int kblk = 0; kblk < C::KB; ++kblk) {
             bf16x8 kf[C::KS];
 #pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = ld_bf16x8(tK + (kblk * 16 + r) * C::P + ks * 32 + 8 * g);
+            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = ld_row_swz<D>(tK, kblk * 16 + r, ks * 32 + 8 * g);
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
                 s[u][kblk] = zero4();
@@ -172,24 +150,20 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
             }
         }
 
-        // O^T += V^T P^T, V^T read transposed straight from the row-major tile
+        // O^T += V^T P^T, V^T read transposed from the row-major tile
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 bf16x8 vf;
-                if constexpr (BLK >= 32) {
-                    vf = ld_tr_operand(tV, C::P, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
-                } else {
-                    u32x2 lo = ld_tr16(tV + (4 * g + (r >> 2)) * C::P + db * 16 + 4 * (r & 3));
-                    vf = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
-                }
+                if constexpr (BLK >= 32) vf = ld_tr_swz<D>(tV, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
+                else vf = ld_tr_swz_half<D>(tV, 4 * g, db * 16, r);
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vf, pf[u][kc], oacc[u][db]);
             }
         }
 
-        if (e + 1 < e1) store_block(buf ^ 1);
+        wait_tile_loads();
         __syncthreads();
     }
 
@@ -261,7 +235,7 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
 template <int D, int BLK>
 hipError_t launch_bf16(const AttnArgs& a, const void* q, const void* k, const void* v, void* o,
                        float* lse, hipStream_t stream) {
-    dim3 grid((unsigned)a.nq, (unsigned)a.heads, (unsigned)a.batch);
+    dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK>), grid, dim3(FwdCfg<D, BLK>::NT), 0, stream, a,
                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
     return hipGetLastError();
