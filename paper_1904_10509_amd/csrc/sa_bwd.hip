@@ -32,10 +32,12 @@ namespace {
 // ---------------------------------------------------------------------------
 // shared pieces
 // ---------------------------------------------------------------------------
-// One thread per row: D_i = sum_t dO[i,t] O[i,t] (fp32).
+// One thread per row: D_i = sum_t dO[i,t] O[i,t] (fp32), and the saved LSE in
+// base-2 units (LSE * log2 e) for the exp2 recomputation of P.
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
-bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, float* __restrict__ delta) {
+bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, const float* __restrict__ lse,
+               float* __restrict__ delta, float* __restrict__ lse2) {
     const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     if (row >= rows) return;
@@ -57,6 +59,7 @@ bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, 
         for (int t = 0; t < D; ++t) acc = fmaf(o[off + t], dout[off + t], acc);
     }
     delta[row] = acc;
+    lse2[row] = lse[row] * kLog2e;  // -inf stays -inf
 }
 
 // ---------------------------------------------------------------------------
@@ -72,22 +75,26 @@ struct DqCfg {
     static constexpr int KB = BLK / 16;
     static constexpr int KC = (BLK + 31) / 32;
     static constexpr int DB = D / 16;
+    static constexpr int NS = 3;
+    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;
 };
 
 template <int D, int BLK>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
-bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
+                   const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                    const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
-                   const float* __restrict__ lse, const float* __restrict__ delta,
+                   const float* __restrict__ lse2, const float* __restrict__ delta,
                    uint16_t* __restrict__ dq) {
     using C = DqCfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * D];
-    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
-    const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
@@ -96,6 +103,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* _
     // this lane's query rows row0 + 16u + r: Q and dO as B operands, LSE (log2 units) and D
     bf16x8 qf[C::QBW][C::KS], of[C::QBW][C::KS];
     float L2[C::QBW], Dl[C::QBW];
+    RowLane rl[C::QBW];
     f32x4 dqacc[C::QBW][C::DB];
 #pragma unroll
     for (int u = 0; u < C::QBW; ++u) {
@@ -105,31 +113,39 @@ bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* _
             qf[u][ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
             of[u][ks] = ld_bf16x8(dout + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
         }
-        L2[u] = lse[rowbase + i] * kLog2e;
+        L2[u] = lse2[rowbase + i];
         Dl[u] = delta[rowbase + i];
+        rl[u] = row_lane(i, a.l);
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) dqacc[u][db] = zero4();
     }
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = a.row_ptr[rp], e1 = a.row_ptr[rp + 1];
-    auto load_block = [&](int kb, int buf) {
+    const int e0 = row_ptr[rp], e1 = row_ptr[rp + 1];
+    TileLoader<D, BLK, C::NW> ld;
+    ld.init(a.ss, w, lane);
+    auto load_block = [&](int kb, int stage) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-        load_tile_async<D, BLK, C::NW>(k + kbase, a.ss, sK[buf], w, lane);
-        load_tile_async<D, BLK, C::NW>(v + kbase, a.ss, sV[buf], w, lane);
+        ld.issue(k + kbase, sK[stage]);
+        ld.issue(v + kbase, sV[stage]);
     };
-    if (e0 < e1) load_block(a.col_idx[e0], 0);
-    wait_tile_loads();
-    __syncthreads();
+    wait_loads_upto<0>();  // register loads done before the ring starts
+#pragma unroll
+    for (int p = 0; p < C::NS - 1; ++p)
+        if (e0 + p < e1) load_block(col_idx[e0 + p], p);
+    int st = 0;
     for (int e = e0; e < e1; ++e) {
-        const int buf = (e - e0) & 1;
-        const int kb = a.col_idx[e];
-        const bool masked = a.kind[e] != TILE_FULL;
-        if (e + 1 < e1) load_block(a.col_idx[e + 1], buf ^ 1);
-        const uint16_t* tK = sK[buf];
-        const uint16_t* tV = sV[buf];
+        const int kb = col_idx[e];
+        const int j0 = kb * BLK;
+        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        pipeline_wait<C::NS, C::NI>(e1 - 1 - e);
+        __syncthreads();
+        if (e + C::NS - 1 < e1) load_block(col_idx[e + C::NS - 1], st == 0 ? C::NS - 1 : st - 1);
+        const uint16_t* tK = sK[st];
+        const uint16_t* tV = sV[st];
+        st = st + 1 == C::NS ? 0 : st + 1;
 
-        // S^T and dP^T: x[u][kb16][t] for key kb*BLK + 16 kb16 + 4g + t, query row0 + 16u + r
+        // S^T and dP^T: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
         f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
 #pragma unroll
         for (int kblk = 0; kblk < C::KB; ++kblk) {
@@ -150,24 +166,44 @@ bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* _
                 }
             }
         }
-        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - L2), masked
+        int cls[C::KB];
+        uint64_t bits[C::QBW];
+#pragma unroll
+        for (int kblk = 0; kblk < C::KB; ++kblk) cls[kblk] = SUB_ALL;
+        if (masked) {
+            const int j0_mod = j0 % a.l;
+            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) bits[u] = row_mask(mp, rl[u], j0, j0_mod, sum) >> (4 * g);
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                uint32_t any = 0u, all = 0xFu;
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    const uint32_t nib = (uint32_t)(bits[u] >> (16 * kblk)) & 0xFu;
+                    any |= nib;
+                    all &= nib;
+                }
+                cls[kblk] = classify_sub(any, all);
+            }
+        }
+        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - L2)
         bf16x8 dsf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
-            uint64_t bits = ~0ull;
-            if (masked) {
-                const int j0 = kb * BLK;
-                const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
-                bits = row_mask(mp, row0 + 16 * u + r, j0, sum) >> (4 * g);
-            }
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk)
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                if (cls[kblk] == SUB_NONE) {
+                    s[u][kblk] = zero4();
+                    continue;
+                }
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const bool on = (bits >> (16 * kblk + t)) & 1ull;
-                    const float pv = on ? exp2_fast(fmaf(s[u][kblk][t], c2, -L2[u])) : 0.f;
+                    float pv = exp2_fast(fmaf(s[u][kblk][t], c2, -L2[u]));
+                    if (cls[kblk] == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
                     s[u][kblk][t] = pv * (dp[u][kblk][t] - Dl[u]);
                 }
+            }
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
                 if constexpr (BLK >= 32) dsf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
@@ -186,8 +222,6 @@ bwd_dq_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* _
                 for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(kt, dsf[u][kc], dqacc[u][db]);
             }
         }
-        wait_tile_loads();
-        __syncthreads();
     }
 
     // this lane holds dQ^T at d = 16 db + 4g + t for query row0 + 16u + r
@@ -213,31 +247,37 @@ struct DkvCfg {
     static constexpr int QB = BLK / 16;             // 16-query blocks per tile
     static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
+    static constexpr int NS = 3;
+    // Q and dO tiles, plus the row statistics (wave 0 loads the LSE, the last
+    // wave D; a single wave loads both)
+    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER + (NW == 1 ? 2 : 1);
 };
 
 template <int D, int BLK>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
-bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int32_t* __restrict__ row_idx,
+                     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
-                     const float* __restrict__ lse, const float* __restrict__ delta,
+                     const float* __restrict__ lse2, const float* __restrict__ delta,
                      uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
     using C = DkvCfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t sQ[2][BLK * D];
-    __shared__ __attribute__((aligned(16))) uint16_t sdO[2][BLK * D];
-    __shared__ __attribute__((aligned(16))) float sL[2][64];
-    __shared__ __attribute__((aligned(16))) float sDl[2][64];
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
+    __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
+    __shared__ __attribute__((aligned(16))) float sDl[C::NS][64];
 
     const int h = blockIdx.x, kb = blockIdx.y, b = blockIdx.z;  // low key blocks have the longest columns
-    const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int key0 = kb * BLK + w * C::KW;  // first key of this wave
 
     // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
     bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
-    bool summary[C::KBW];
+    ColLane cl[C::KBW];
 #pragma unroll
     for (int kbw = 0; kbw < C::KBW; ++kbw) {
         const int j = key0 + 16 * kbw + r;
@@ -246,7 +286,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
             kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
             vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
         }
-        summary[kbw] = a.pattern == FIXED && (j % a.l) >= a.l - a.c;
+        cl[kbw] = col_lane(j, a.l, a.c);
     }
 
     f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
@@ -259,27 +299,40 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
         }
 
     const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
-    const int e0 = a.col_ptr[cp], e1 = a.col_ptr[cp + 1];
-    auto load_block = [&](int qb, int buf) {
+    const int e0 = col_ptr[cp], len = col_ptr[cp + 1] - e0;
+    // The column is walked from its last query block down: the key blocks of
+    // a head then visit the same query blocks at about the same time, which
+    // keeps those Q / dO tiles shared in L2.
+    auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
+    TileLoader<D, BLK, C::NW> ld;
+    ld.init(a.ss, w, lane);
+    auto load_block = [&](int qb, int stage) {
         const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
-        load_tile_async<D, BLK, C::NW>(q + qbase, a.ss, sQ[buf], w, lane);
-        load_tile_async<D, BLK, C::NW>(dout + qbase, a.ss, sdO[buf], w, lane);
-        load_row_stats_async(lse + rowbase + (int64_t)qb * BLK, BLK, sL[buf], w, lane);
-        load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[buf], w, lane);
+        ld.issue(q + qbase, sQ[stage]);
+        ld.issue(dout + qbase, sdO[stage]);
+        if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL[stage], lane);
+        if (w == C::NW - 1) load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[stage], lane);
     };
 
-    if (e0 < e1) load_block(a.row_idx[e0], 0);
-    wait_tile_loads();
-    __syncthreads();
+    wait_loads_upto<0>();  // register loads done before the ring starts
+#pragma unroll
+    for (int p = 0; p < C::NS - 1; ++p)
+        if (p < len) load_block(row_idx[entry(p)], p);
     const float c2 = a.scale_log2;
-    for (int e = e0; e < e1; ++e) {
-        const int buf = (e - e0) & 1;
-        const int qb = a.row_idx[e];
-        const bool masked = a.kind_t[e] != TILE_FULL;
+    int st = 0;
+    for (int sidx = 0; sidx < len; ++sidx) {
+        const int e = entry(sidx);
+        const int qb = row_idx[e];
         const int i0 = qb * BLK;
-        if (e + 1 < e1) load_block(a.row_idx[e + 1], buf ^ 1);
-        const uint16_t* tQ = sQ[buf];
-        const uint16_t* tO = sdO[buf];
+        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+        pipeline_wait<C::NS, C::NI>(len - 1 - sidx);
+        __syncthreads();
+        if (sidx + C::NS - 1 < len) load_block(row_idx[entry(sidx + C::NS - 1)], st == 0 ? C::NS - 1 : st - 1);
+        const uint16_t* tQ = sQ[st];
+        const uint16_t* tO = sdO[st];
+        const float* tL = sL[st];
+        const float* tD = sDl[st];
+        st = st + 1 == C::NS ? 0 : st + 1;
 
         // S and dP: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
         f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
@@ -303,18 +356,26 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
                 ds[kbw][qblk] = dpacc;
             }
         }
+        const int i0_mod = i0 % a.l;
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
             uint64_t bits = ~0ull;
-            if (masked) bits = col_mask(mp, key0 + 16 * kbw + r, i0, summary[kbw]) >> (4 * g);
+            if (masked) bits = col_mask(mp, cl[kbw], i0, i0_mod) >> (4 * g);
 #pragma unroll
             for (int qblk = 0; qblk < C::QB; ++qblk) {
-                const f32x4 L = *reinterpret_cast<const f32x4*>(&sL[buf][qblk * 16 + 4 * g]);
-                const f32x4 Dl = *reinterpret_cast<const f32x4*>(&sDl[buf][qblk * 16 + 4 * g]);
+                const uint32_t nib = (uint32_t)(bits >> (16 * qblk)) & 0xFu;
+                const int cls = masked ? classify_sub(nib, nib) : SUB_ALL;
+                if (cls == SUB_NONE) {
+                    p[kbw][qblk] = zero4();
+                    ds[kbw][qblk] = zero4();
+                    continue;
+                }
+                const f32x4 L = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
+                const f32x4 Dl = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const bool on = (bits >> (16 * qblk + t)) & 1ull;
-                    const float pv = on ? exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t] * kLog2e)) : 0.f;
+                    float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t]));
+                    if (cls == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits, 16 * qblk + t), pv);
                     p[kbw][qblk][t] = pv;
                     ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
                 }
@@ -325,6 +386,17 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
         // dO^T and Q^T are read transposed from the row-major tiles
 #pragma unroll
         for (int qc = 0; qc < C::QC; ++qc) {
+            bf16x8 pb[C::KBW], sb[C::KBW];
+#pragma unroll
+            for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                if constexpr (BLK >= 32) {
+                    pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
+                    sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                } else {
+                    pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
+                    sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
+                }
+            }
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 bf16x8 oT, qT;
@@ -337,21 +409,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t*
                 }
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    bf16x8 pb, sb;
-                    if constexpr (BLK >= 32) {
-                        pb = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
-                        sb = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
-                    } else {
-                        pb = pack_bf16x8(p[kbw][0], zero4());
-                        sb = pack_bf16x8(ds[kbw][0], zero4());
-                    }
-                    dvacc[kbw][db] = mfma_16x16x32(oT, pb, dvacc[kbw][db]);
-                    dkacc[kbw][db] = mfma_16x16x32(qT, sb, dkacc[kbw][db]);
+                    dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
+                    dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
                 }
             }
         }
-        wait_tile_loads();
-        __syncthreads();
     }
 
     // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
@@ -464,7 +526,7 @@ hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const
                           void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     hipLaunchKernelGGL((bwd_pre_kernel<D, float>), dim3((unsigned)((rows + 255) / 256)), dim3(256),
-                       0, stream, a, (const float*)o, (const float*)dout, delta);
+                       0, stream, a, (const float*)o, (const float*)dout, lse, delta, delta + rows);
     dim3 grid((unsigned)((a.n + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
                        (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dq);
@@ -479,15 +541,16 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                            const void* o, const void* dout, const float* lse, void* dq, void* dk,
                            void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
+    float* lse2 = delta + rows;
     hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)((rows + 255) / 256)),
-                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, delta);
+                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, delta, lse2);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
-                       (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse, delta, (uint16_t*)dq);
+                       a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dq);
     hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), grid, dim3(DkvCfg<D, BLK>::NT), 0, stream,
-                       a, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse, delta, (uint16_t*)dk, (uint16_t*)dv);
+                       a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dk, (uint16_t*)dv);
     return hipGetLastError();
 }
 
@@ -507,7 +570,7 @@ hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, co
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype) {
     (void)d;
     (void)dtype;
-    return (size_t)(batch * heads * n * (int64_t)sizeof(float));  // D_i, one fp32 per row
+    return (size_t)(2 * batch * heads * n * (int64_t)sizeof(float));  // D_i and LSE_i log2 e per row
 }
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,

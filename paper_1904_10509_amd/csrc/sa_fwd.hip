@@ -35,6 +35,8 @@ struct FwdCfg {
     static constexpr int KB = BLK / 16;             // 16-key blocks per tile
     static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
     static constexpr int DB = D / 16;               // 16-wide d blocks of O
+    static constexpr int NS = 3;                    // K/V pipeline stages
+    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;  // loads per wave per stage
 };
 
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
@@ -42,23 +44,27 @@ struct FwdCfg {
 // multiple of 8 each head stays on one XCD and its keys stay in that L2.
 template <int D, int BLK>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
-fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
+                const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
     using C = FwdCfg<D, BLK>;
-    // K and V tiles, double-buffered: one barrier per key block
-    __shared__ __attribute__((aligned(16))) uint16_t sK[2][BLK * D];
-    __shared__ __attribute__((aligned(16))) uint16_t sV[2][BLK * D];
+    // K and V tiles in an NS-stage ring: the next NS-1 key blocks are in
+    // flight while one is computed; one barrier per key block
+    __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
-    const int tid = threadIdx.x, w = tid / 64, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int row0 = qb * BLK + w * C::RW;  // first query row of this wave
 
     bf16x8 qf[C::QBW][C::KS];
     f32x4 oacc[C::QBW][C::DB];
     float m_run[C::QBW], l_run[C::QBW];
+    RowLane rl[C::QBW];
 #pragma unroll
     for (int u = 0; u < C::QBW; ++u) {
 #pragma unroll
@@ -68,29 +74,40 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
         for (int db = 0; db < C::DB; ++db) oacc[u][db] = zero4();
         m_run[u] = -INFINITY;
         l_run[u] = 0.f;
+        rl[u] = row_lane(row0 + 16 * u + r, a.l);
     }
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = a.row_ptr[rp], e1 = a.row_ptr[rp + 1];
-    auto load_block = [&](int kb, int buf) {
+    const int e0 = row_ptr[rp], e1 = row_ptr[rp + 1];
+    TileLoader<D, BLK, C::NW> ld;
+    ld.init(a.ss, w, lane);
+    auto load_block = [&](int kb, int stage) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-        load_tile_async<D, BLK, C::NW>(k + kbase, a.ss, sK[buf], w, lane);
-        load_tile_async<D, BLK, C::NW>(v + kbase, a.ss, sV[buf], w, lane);
+        ld.issue(k + kbase, sK[stage]);
+        ld.issue(v + kbase, sV[stage]);
     };
 
-    if (e0 < e1) load_block(a.col_idx[e0], 0);
-    wait_tile_loads();
-    __syncthreads();
+    // The register loads above complete before the ring starts, so no
+    // compiler-tracked load is outstanding inside the loop (a wait for one
+    // would also drain the ring).
+    wait_loads_upto<0>();
+#pragma unroll
+    for (int p = 0; p < C::NS - 1; ++p)
+        if (e0 + p < e1) load_block(col_idx[e0 + p], p);
     const float c2 = a.scale_log2;
+    int st = 0;  // ring stage of block e
     for (int e = e0; e < e1; ++e) {
-        const int buf = (e - e0) & 1;
-        const int kb = a.col_idx[e];
-        const bool masked = a.kind[e] != TILE_FULL;
-        if (e + 1 < e1) load_block(a.col_idx[e + 1], buf ^ 1);  // lands during this block's math
-        const uint16_t* tK = sK[buf];
-        const uint16_t* tV = sV[buf];
+        const int kb = col_idx[e];
+        const int j0 = kb * BLK;
+        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        pipeline_wait<C::NS, C::NI>(e1 - 1 - e);
+        __syncthreads();  // this block is in LDS everywhere; the previous stage is free
+        if (e + C::NS - 1 < e1) load_block(col_idx[e + C::NS - 1], st == 0 ? C::NS - 1 : st - 1);
+        const uint16_t* tK = sK[st];
+        const uint16_t* tV = sV[st];
+        st = st + 1 == C::NS ? 0 : st + 1;
 
-        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(kb*BLK + 16 kb16 + 4g + t)
+        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
         f32x4 s[C::QBW][C::KB];
 #pragma unroll
         for (int kblk = 0; kblk < C::KB; ++kblk) {
@@ -105,48 +122,80 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
             }
         }
 
+        // mask bits of this lane's rows, and the per-sub-block treatment
+        int cls[C::KB];
+        uint64_t bits[C::QBW];
+#pragma unroll
+        for (int kblk = 0; kblk < C::KB; ++kblk) cls[kblk] = SUB_ALL;
+        if (masked) {
+            const int j0_mod = j0 % a.l;
+            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) bits[u] = row_mask(mp, rl[u], j0, j0_mod, sum) >> (4 * g);
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                uint32_t any = 0u, all = 0xFu;
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    const uint32_t nib = (uint32_t)(bits[u] >> (16 * kblk)) & 0xFu;
+                    any |= nib;
+                    all &= nib;
+                }
+                cls[kblk] = classify_sub(any, all);
+            }
+        }
+
         bf16x8 pf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
-            if (masked) {
-                const int j0 = kb * BLK;
-                const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
-                const uint64_t bits = row_mask(mp, row0 + 16 * u + r, j0, sum) >> (4 * g);
-#pragma unroll
-                for (int kblk = 0; kblk < C::KB; ++kblk)
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        if (!((bits >> (16 * kblk + t)) & 1ull)) s[u][kblk][t] = -INFINITY;
-            }
-            // running max in raw score units (the scale is positive)
+            // running max in raw score units (the scale is positive), over
+            // the sub-blocks that hold attended keys
             float mloc = -INFINITY;
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk)
-                mloc = fmaxf(fmaxf(mloc, fmaxf(s[u][kblk][0], s[u][kblk][1])), fmaxf(s[u][kblk][2], s[u][kblk][3]));
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                if (cls[kblk] == SUB_NONE) continue;
+                if (cls[kblk] == SUB_MIXED) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        s[u][kblk][t] = select_or_neg_inf(bit_lane_mask(bits[u], 16 * kblk + t), s[u][kblk][t]);
+                }
+                mloc = fmaxf(mloc, fmaxf(fmaxf(s[u][kblk][0], s[u][kblk][1]), fmaxf(s[u][kblk][2], s[u][kblk][3])));
+            }
             mloc = max_over_g(mloc);
             const float m_new = fmaxf(m_run[u], mloc);
+            const bool grew = m_new > m_run[u];
             // rows with nothing attended so far keep m = -inf; 0 as reference
-            // gives p = 0 and alpha = 0 without a branch around the MFMAs
+            // gives p = 0 without a branch around the MFMAs
             const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-            const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
             const float neg = -m_ref * c2;
-            m_run[u] = m_new;
             float psum = 0.f;
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk)
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                if (cls[kblk] == SUB_NONE) {
+                    s[u][kblk] = zero4();
+                    continue;
+                }
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const float pv = exp2_fast(fmaf(s[u][kblk][t], c2, neg));
                     s[u][kblk][t] = pv;
                     psum += pv;
                 }
-            l_run[u] = l_run[u] * alpha + psum;
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
+            }
+            // alpha rescales the state kept for the old maximum (0 when it was -inf)
+            const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
+            l_run[u] = fmaf(l_run[u], alpha, psum);
+            m_run[u] = m_new;
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
                 if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
                 else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
+            }
+            // O is rescaled only in the blocks where some row's maximum grew
+            // (a wave-uniform branch); everywhere else alpha is exactly 1.
+            if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {
+#pragma unroll
+                for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
             }
         }
 
@@ -162,9 +211,6 @@ fwd_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __re
                 for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vf, pf[u][kc], oacc[u][db]);
             }
         }
-
-        wait_tile_loads();
-        __syncthreads();
     }
 
 #pragma unroll
@@ -237,7 +283,7 @@ hipError_t launch_bf16(const AttnArgs& a, const void* q, const void* k, const vo
                        float* lse, hipStream_t stream) {
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK>), grid, dim3(FwdCfg<D, BLK>::NT), 0, stream, a,
-                       (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
+                       a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
     return hipGetLastError();
 }
 

@@ -52,41 +52,88 @@ struct MaskParams {
     uint64_t period_bits;  // bits at multiples of l below 64
 };
 
-// Row view: attended keys j0 + jj (bit jj) of query row i.  The caller
-// guarantees j0 <= i, and passes `sum` = summary_bits(j0, l, c) for the fixed
-// pattern (it depends on the block only).
-__device__ inline uint64_t row_mask(const MaskParams& p, int i, int j0, uint64_t sum) {
-    const int D = i - j0;  // key offset of the diagonal, >= 0
-    uint64_t causal = bit_range(0, D);
+// Row view (the lane owns query row i): constants of the lane.
+struct RowLane {
+    int i;      // query row
+    int i_mod;  // i mod l
+    int blk0;   // first column of i's l-block
+};
+__device__ inline RowLane row_lane(int i, int l) { return RowLane{i, i % l, i - i % l}; }
+
+// Attended keys j0 + jj (bit jj) of the lane's row, j0 <= i.  j0_mod is
+// j0 mod l and sum = summary_bits(j0, l, c) (fixed pattern); both depend on
+// the block only.
+__device__ inline uint64_t row_mask(const MaskParams& p, const RowLane& x, int j0, int j0_mod, uint64_t sum) {
+    const int D = x.i - j0;  // key offset of the diagonal, >= 0
+    const uint64_t causal = bit_range(0, D);
     uint64_t a1, a2;
     if (p.pattern == STRIDED) {
         a1 = bit_range(D - p.l, D);
-        a2 = periodic_from(p.period_bits, D % p.l);
+        int m = x.i_mod - j0_mod;  // D mod l
+        m += m < 0 ? p.l : 0;
+        a2 = periodic_from(p.period_bits, m);
     } else {
-        const int bs = i - i % p.l;  // first column of i's l-block
-        a1 = bit_range(bs - j0, D);
+        a1 = bit_range(x.blk0 - j0, D);
         a2 = sum;
     }
-    uint64_t m = p.part == PART_A1 ? a1 : (p.part == PART_A2 ? a2 : (a1 | a2));
+    const uint64_t m = p.part == PART_A1 ? a1 : (p.part == PART_A2 ? a2 : (a1 | a2));
     return m & causal;
 }
 
-// Column view: attended queries i0 + ii (bit ii) of key column j.  `summary`
-// is whether j is a fixed-pattern summary column.
-__device__ inline uint64_t col_mask(const MaskParams& p, int j, int i0, bool summary) {
-    const int D = j - i0;  // query offset of the diagonal (may be negative)
-    uint64_t causal = bit_range(D, 63);
+// Column view (the lane owns key column j): constants of the lane.
+struct ColLane {
+    int j;         // key column
+    int j_mod;     // j mod l
+    int blk0;      // first row of j's l-block
+    bool summary;  // fixed pattern: j mod l >= l - c
+};
+__device__ inline ColLane col_lane(int j, int l, int c) {
+    return ColLane{j, j % l, j - j % l, (j % l) >= l - c};
+}
+
+// Attended queries i0 + ii (bit ii) of the lane's column; i0_mod = i0 mod l.
+__device__ inline uint64_t col_mask(const MaskParams& p, const ColLane& y, int i0, int i0_mod) {
+    const int D = y.j - i0;  // query offset of the diagonal (may be negative)
+    const uint64_t causal = bit_range(D, 63);
     uint64_t a1, a2;
     if (p.pattern == STRIDED) {
         a1 = bit_range(D, D + p.l);
-        a2 = periodic_from(p.period_bits, mod_pos(D, p.l));
+        int m = y.j_mod - i0_mod;  // D mod l, non-negative
+        m += m < 0 ? p.l : 0;
+        a2 = periodic_from(p.period_bits, m);
     } else {
-        const int bs = j - j % p.l;  // j's l-block
-        a1 = bit_range(bs - i0, bs + p.l - 1 - i0);
-        a2 = summary ? ~0ull : 0ull;
+        a1 = bit_range(y.blk0 - i0, y.blk0 + p.l - 1 - i0);
+        a2 = (p.pattern == FIXED && y.summary) ? ~0ull : 0ull;
     }
-    uint64_t m = p.part == PART_A1 ? a1 : (p.part == PART_A2 ? a2 : (a1 | a2));
+    const uint64_t m = p.part == PART_A1 ? a1 : (p.part == PART_A2 ? a2 : (a1 | a2));
     return m & causal;
+}
+
+// All ones when bit pos (0..63, a constant after unrolling) of bits is set, else 0.
+__device__ inline int32_t bit_lane_mask(uint64_t bits, int pos) {
+    const uint32_t half = pos < 32 ? (uint32_t)bits : (uint32_t)(bits >> 32);
+    return __builtin_amdgcn_sbfe((int32_t)half, (uint32_t)(pos & 31), 1u);
+}
+
+// x where the mask is all ones, -inf where it is zero (one bitfield select).
+__device__ inline float select_or_neg_inf(int32_t m, float x) {
+    return __int_as_float((m & __float_as_int(x)) | (~m & (int32_t)0xff800000));
+}
+
+// x where the mask is all ones, +0 where it is zero.
+__device__ inline float select_or_zero(int32_t m, float x) { return __int_as_float(m & __float_as_int(x)); }
+
+// How a 16 x 16 sub-block of a masked block is treated, decided for the whole
+// wave: nothing attended (its probabilities are zero and no exponential is
+// evaluated), everything attended (no masking), or mixed (per element).
+enum { SUB_NONE = 0, SUB_MIXED = 1, SUB_ALL = 2 };
+
+// `nib_any` / `nib_all`: OR / AND over this lane's rows (or columns) of the
+// four mask bits it holds in the sub-block.
+__device__ inline int classify_sub(uint32_t nib_any, uint32_t nib_all) {
+    if (__builtin_amdgcn_ballot_w64(nib_any != 0u) == 0ull) return SUB_NONE;
+    if (__builtin_amdgcn_ballot_w64(nib_all != 0xFu) == 0ull) return SUB_ALL;
+    return SUB_MIXED;
 }
 
 inline uint64_t host_period_bits(int64_t l) {

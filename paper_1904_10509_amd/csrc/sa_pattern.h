@@ -104,6 +104,39 @@ __host__ __device__ inline int64_t attended_in_range(const Pattern& p, int64_t i
     return own + earlier;
 }
 
+// True when every pair of the block rows [r0, r1] x columns [c0, c1] is
+// attended, evaluated in O(1) on the scalar unit by the kernels (the layout
+// builder counts pairs instead).  Exact for every part except fixed merged,
+// where it may answer false for a full block, which only costs masking work.
+__host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int64_t c, int64_t r0,
+                                           int64_t r1, int64_t c0, int64_t c1) {
+    if (r0 < c1) return false;  // meets the diagonal: the causal cut runs through it
+    if (pattern == STRIDED) {
+        if (part == PART_A2) return l == 1;
+        return r1 - c0 <= l || (part == PART_MERGED && l == 1);
+    }
+    const bool one_block = c0 / l == r1 / l;                                   // all pairs in one l-block
+    const bool all_summary = c == l || (c0 / l == c1 / l && c0 % l >= l - c);  // every column a summary
+    if (part == PART_A1) return one_block;
+    if (part == PART_A2) return all_summary;
+    return one_block || all_summary;
+}
+
+// block_full in 32-bit arithmetic (all coordinates below 2^31).
+__host__ __device__ inline bool block_full32(int pattern, int part, int32_t l, int32_t c, int32_t r0, int32_t r1,
+                                             int32_t c0, int32_t c1) {
+    if (r0 < c1) return false;
+    if (pattern == STRIDED) {
+        if (part == PART_A2) return l == 1;
+        return r1 - c0 <= l || (part == PART_MERGED && l == 1);
+    }
+    const bool one_block = c0 / l == r1 / l;
+    const bool all_summary = c == l || (c0 / l == c1 / l && c0 % l >= l - c);
+    if (part == PART_A1) return one_block;
+    if (part == PART_A2) return all_summary;
+    return one_block || all_summary;
+}
+
 // Element predicate in 32-bit arithmetic (0 <= i, j < 2^31).
 __host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32_t c, int32_t i,
                                          int32_t j) {

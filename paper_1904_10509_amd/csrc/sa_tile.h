@@ -7,10 +7,18 @@
 // reads (ds_read_b128) and the transposing reads (ds_read_b64_tr_b16).
 //
 // Filling uses global_load_lds_dwordx4: lane L of a wave writes bytes
-// [16 L, 16 L + 16) of a 1 KiB LDS window, from any global address, without
-// passing through registers.  So each lane fetches the global chunk that
-// belongs at its slot.  The loads complete asynchronously; wait_tile_loads()
-// waits for this wave's loads, after which a barrier publishes the tile.
+// [16 L, 16 L + 16) of a 1 KiB LDS window (base in M0), from any global
+// address, without passing through registers.  So each lane fetches the
+// global chunk that belongs at its slot.  The loads complete asynchronously
+// and in issue order; wait_loads_upto<N>() waits until at most N of this
+// wave's loads are outstanding, after which a barrier publishes the tile.
+//
+// The loads are issued from inline assembly on purpose: the compiler then
+// does not track them, and so does not put a full wait before every LDS
+// read (it cannot tell which ring stage a read touches).  Every read of a
+// stage sits behind an explicit wait and a workgroup barrier instead.  A
+// compiler-issued wait for its own loads stays correct with these extra
+// loads outstanding, since waits count completed loads in issue order.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -33,31 +41,100 @@ struct Swz {
 
 // Issue the loads of rows [0, BLK) of a [., D] bf16 tensor whose row 0 is at
 // `src` (row stride `ss` elements) into `tile`, spread over the NW waves.
+// LDS byte address of a pointer into a __shared__ array, made wave-uniform.
+__device__ inline uint32_t lds_addr(const void* p) {
+    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+    return __builtin_amdgcn_readfirstlane(a);
+}
+
+// A wave-uniform global pointer, kept in scalar registers.
+__device__ inline const void* uniform_ptr(const void* p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One direct-to-LDS load per lane: 16 (or 4) bytes from sbase + voff (sbase
+// wave-uniform, voff a 32-bit byte offset) into the LDS window lds_window.
+__device__ inline void dma_b128(const void* sbase, uint32_t voff, uint32_t lds_window) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "s"(lds_window)
+                 : "memory");
+}
+
+__device__ inline void dma_b32(const void* sbase, uint32_t voff, uint32_t lds_window) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" : : "v"(voff), "s"(sbase), "s"(lds_window)
+                 : "memory");
+}
+
+// Issues the direct-to-LDS loads of one BLK x D tile (rows 0..BLK-1 at row
+// stride ss elements) spread over NW waves.  Each lane's byte offsets inside
+// the tile are the same for every tile and computed once.
 template <int D, int BLK, int NW>
-__device__ inline void load_tile_async(const uint16_t* src, int64_t ss, uint16_t* tile, int w, int lane) {
-    constexpr int NB = BLK * D / 512;  // 1 KiB windows per tile
+struct TileLoader {
+    static constexpr int NB = BLK * D / 512;  // 1 KiB windows per tile
+    static constexpr int PER = NB / NW;       // windows per wave
+    static_assert(NB % NW == 0, "every wave issues the same number of loads");
+    uint32_t off[PER];
+    int w;
+
+    __device__ void init(int64_t ss, int wave, int lane) {
+        w = wave;
 #pragma unroll
-    for (int k = w; k < NB; k += NW) {
-        const int oe = 512 * k + 8 * lane;  // element offset of this lane's slot
-        const int row = oe / D, pos = (oe % D) / 8;
-        const int chunk = pos ^ Swz<D>::perm(row);
-        __builtin_amdgcn_global_load_lds(src + row * ss + 8 * chunk,
-                                         (__attribute__((address_space(3))) void*)(tile + 512 * k), 16, 0,
-                                         0);
+        for (int kk = 0; kk < PER; ++kk) {
+            const int k = w + NW * kk;
+            const int oe = 512 * k + 8 * lane;  // element offset of this lane's slot
+            const int row = oe / D, pos = (oe % D) / 8;
+            const int chunk = pos ^ Swz<D>::perm(row);
+            off[kk] = (uint32_t)((row * ss + 8 * chunk) * 2);
+        }
     }
+    // src: first element of the tile's row 0 (wave-uniform)
+    __device__ void issue(const uint16_t* src, uint16_t* tile) const {
+        const uint32_t base = lds_addr(tile);
+        const void* s = uniform_ptr(src);
+#pragma unroll
+        for (int kk = 0; kk < PER; ++kk) dma_b128(s, off[kk], base + 1024 * (w + NW * kk));
+    }
+};
+
+// 64 consecutive fp32 values starting at src (one per lane, lanes past
+// n_valid repeat the last value) into `dst`: one direct-to-LDS load.
+__device__ inline void load_row_stats_async(const float* src, int n_valid, float* dst, int lane) {
+    const uint32_t i = (uint32_t)(lane < n_valid ? lane : n_valid - 1);
+    dma_b32(uniform_ptr(src), 4u * i, lds_addr(dst));
 }
 
-// 64 consecutive fp32 values (one per lane) into `dst`, by wave 0 only.
-__device__ inline void load_row_stats_async(const float* src, int n_valid, float* dst, int w, int lane) {
-    if (w == 0) {
-        const int i = lane < n_valid ? lane : n_valid - 1;
-        __builtin_amdgcn_global_load_lds(src + i, (__attribute__((address_space(3))) void*)dst, 4, 0, 0);
-    }
+// s_waitcnt vmcnt(N): at most N of this wave's global loads (including the
+// ones that write LDS) are still outstanding; loads complete in issue order.
+template <int N>
+__device__ inline void wait_loads_upto() {
+    static_assert(N >= 0 && N < 64, "vmcnt field holds 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ inline void wait_tile_loads() { wait_loads_upto<0>(); }
+
+// Direct-to-LDS loads one wave issues for one tile (TileLoader::PER).
+template <int D, int BLK, int NW>
+constexpr int tile_loads_per_wave() {
+    static_assert((BLK * D / 512) % NW == 0, "every wave issues the same number of loads");
+    return BLK * D / 512 / NW;
 }
 
-// s_waitcnt vmcnt(0): this wave's outstanding global loads (including the
-// ones that write LDS) have completed.
-__device__ inline void wait_tile_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Ring of NS stages with NI loads per wave per stage: wait until the stage
+// being consumed has landed, while the stages of the next `later` blocks
+// (at most NS-2 of them) may still be in flight.
+template <int NS, int NI>
+__device__ inline void pipeline_wait(int later) {
+    static_assert(NS >= 2 && NS <= 4, "pipeline depth");
+    if constexpr (NS >= 4) {
+        if (later >= 2) { wait_loads_upto<2 * NI>(); return; }
+    }
+    if constexpr (NS >= 3) {
+        if (later >= 1) { wait_loads_upto<NI>(); return; }
+    }
+    wait_loads_upto<0>();
+}
 
 // Transposed operand over 32 rows of column col0 + (lane % 16): the first
 // four contraction items from rows row_lo .. row_lo+3, the last four from
