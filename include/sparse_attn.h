@@ -155,7 +155,8 @@ int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
  * (col_ptr, row_idx, kind_t).  dq, dk, dv are device outputs with the
  * strides of q.  workspace is caller-owned device memory of at least
  * sparse_attn_bwd_workspace_size bytes (SA_ERR_BUFFER_TOO_SMALL otherwise);
- * its contents on entry are ignored.
+ * its contents on entry are ignored, and calls that share one workspace
+ * must not overlap (it holds per-call row statistics and a work counter).
  */
 int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
                     int32_t pattern, int32_t head_mode, const int32_t* row_ptr,

@@ -12,14 +12,23 @@
 //   2. dq:    one workgroup per (head, query block, batch) walks the row view
 //             of the layout like the forward: S^T and dP^T recomputed, dS^T
 //             formed in registers and contracted with K into dQ;
-//   3. dkdv:  one workgroup per (head, key block, batch) walks the column
-//             view: S and dP recomputed, dV += P^T dO and dK += dS^T Q held in
-//             registers for the whole column.
+//   3. dkdv:  a workgroup takes one (key block, batch, head) column at a
+//             time from a queue and walks its column view: S and dP
+//             recomputed, dV += P^T dO and dK += dS^T Q held in registers for
+//             the whole column.
+// Column lengths can vary with a short period (in the fixed pattern only the
+// key blocks holding summary columns are long), and a hardware placement of
+// one workgroup per column can then pile the long columns onto a few compute
+// units.  The dkdv grid is therefore sized to the resident capacity of the
+// device and each workgroup claims columns from an atomic counter in the
+// workspace, longest-first order (ascending key block).
 // The dq kernel repeats the S and dP products of the dkdv kernel; those two
 // extra products per block are the price of having no reduction across
 // workgroups.
 // fp32 path: the same quantities on the VALU, one thread per row for dq and
 // one thread per column for dk / dv.
+#include <atomic>
+
 #include "sa_internal.h"
 #include "sa_mask.h"
 #include "sa_mfma.h"
@@ -37,8 +46,9 @@ namespace {
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
 bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, const float* __restrict__ lse,
-               float* __restrict__ delta, float* __restrict__ lse2) {
+               float* __restrict__ delta, float* __restrict__ lse2, unsigned long long* __restrict__ queue) {
     const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (row == 0 && queue) *queue = 0ull;  // the dkdv column queue starts empty
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     if (row >= rows) return;
     const int64_t bh = row / a.n, i = row % a.n;
@@ -259,174 +269,195 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                      const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                      const float* __restrict__ lse2, const float* __restrict__ delta,
-                     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+                     uint16_t* __restrict__ dk, uint16_t* __restrict__ dv,
+                     unsigned long long* __restrict__ queue) {
     using C = DkvCfg<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
     __shared__ __attribute__((aligned(16))) float sDl[C::NS][64];
+    __shared__ unsigned long long sItem[2];
 
-    const int h = blockIdx.x, kb = blockIdx.y, b = blockIdx.z;  // low key blocks have the longest columns
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
-    const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-    const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
-    const int key0 = kb * BLK + w * C::KW;  // first key of this wave
-
-    // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
-    bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
-    ColLane cl[C::KBW];
-#pragma unroll
-    for (int kbw = 0; kbw < C::KBW; ++kbw) {
-        const int j = key0 + 16 * kbw + r;
-#pragma unroll
-        for (int ks = 0; ks < C::KS; ++ks) {
-            kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
-            vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
-        }
-        cl[kbw] = col_lane(j, a.l, a.c);
-    }
-
-    f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
-#pragma unroll
-    for (int kbw = 0; kbw < C::KBW; ++kbw)
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) {
-            dvacc[kbw][db] = zero4();
-            dkacc[kbw][db] = zero4();
-        }
-
-    const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
-    const int e0 = col_ptr[cp], len = col_ptr[cp + 1] - e0;
-    // The column is walked from its last query block down: the key blocks of
-    // a head then visit the same query blocks at about the same time, which
-    // keeps those Q / dO tiles shared in L2.
-    auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
+    const int64_t bh_count = (int64_t)a.batch * a.heads;
+    const uint64_t items = (uint64_t)a.nq * bh_count;
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
-    auto load_block = [&](int qb, int stage) {
-        const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
-        ld.issue(q + qbase, sQ[stage]);
-        ld.issue(dout + qbase, sdO[stage]);
-        if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL[stage], lane);
-        if (w == C::NW - 1) load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[stage], lane);
-    };
+    if (tid == 0) sItem[0] = atomicAdd(queue, 1ull);
+    __syncthreads();
+    // Every wave leaves the loop at the same claim: the claimed index is
+    // shared through LDS and is past the end once the queue has run dry.
+    for (int it = 0;; ++it) {
+        const uint64_t item = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sItem[it & 1] >> 32)) << 32) |
+                              __builtin_amdgcn_readfirstlane((uint32_t)sItem[it & 1]);
+        if (item >= items) break;
+        unsigned long long next = 0ull;
+        if (tid == 0) next = atomicAdd(queue, 1ull);  // claimed now, published after the column
+        // ascending key block: under causality the low key blocks have the longest columns
+        const int kb = (int)(item / (uint64_t)bh_count);
+        const int bh = (int)(item - (uint64_t)kb * bh_count);
+        const int h = bh % a.heads, b = bh / a.heads;
+        const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+        const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+        const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
+        const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
+        const int key0 = kb * BLK + w * C::KW;  // first key of this wave
 
-    wait_loads_upto<0>();  // register loads done before the ring starts
-#pragma unroll
-    for (int p = 0; p < C::NS - 1; ++p)
-        if (p < len) load_block(row_idx[entry(p)], p);
-    const float c2 = a.scale_log2;
-    int st = 0;
-    for (int sidx = 0; sidx < len; ++sidx) {
-        const int e = entry(sidx);
-        const int qb = row_idx[e];
-        const int i0 = qb * BLK;
-        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
-        pipeline_wait<C::NS, C::NI>(len - 1 - sidx);
-        __syncthreads();
-        if (sidx + C::NS - 1 < len) load_block(row_idx[entry(sidx + C::NS - 1)], st == 0 ? C::NS - 1 : st - 1);
-        const uint16_t* tQ = sQ[st];
-        const uint16_t* tO = sdO[st];
-        const float* tL = sL[st];
-        const float* tD = sDl[st];
-        st = st + 1 == C::NS ? 0 : st + 1;
-
-        // S and dP: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
-        f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
-#pragma unroll
-        for (int qblk = 0; qblk < C::QB; ++qblk) {
-            bf16x8 qa[C::KS], oa[C::KS];
-#pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) {
-                qa[ks] = ld_row_swz<D>(tQ, qblk * 16 + r, ks * 32 + 8 * g);
-                oa[ks] = ld_row_swz<D>(tO, qblk * 16 + r, ks * 32 + 8 * g);
-            }
-#pragma unroll
-            for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                f32x4 sacc = zero4(), dpacc = zero4();
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) {
-                    sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
-                    dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
-                }
-                p[kbw][qblk] = sacc;
-                ds[kbw][qblk] = dpacc;
-            }
-        }
-        const int i0_mod = i0 % a.l;
-#pragma unroll
+        // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
+        bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
+        ColLane cl[C::KBW];
+    #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
-            uint64_t bits = ~0ull;
-            if (masked) bits = col_mask(mp, cl[kbw], i0, i0_mod) >> (4 * g);
-#pragma unroll
-            for (int qblk = 0; qblk < C::QB; ++qblk) {
-                const uint32_t nib = (uint32_t)(bits >> (16 * qblk)) & 0xFu;
-                const int cls = masked ? classify_sub(nib, nib) : SUB_ALL;
-                if (cls == SUB_NONE) {
-                    p[kbw][qblk] = zero4();
-                    ds[kbw][qblk] = zero4();
-                    continue;
-                }
-                const f32x4 L = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
-                const f32x4 Dl = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t]));
-                    if (cls == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits, 16 * qblk + t), pv);
-                    p[kbw][qblk][t] = pv;
-                    ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
-                }
+            const int j = key0 + 16 * kbw + r;
+    #pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) {
+                kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
             }
+            cl[kbw] = col_lane(j, a.l, a.c);
         }
 
-        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries;
-        // dO^T and Q^T are read transposed from the row-major tiles
-#pragma unroll
-        for (int qc = 0; qc < C::QC; ++qc) {
-            bf16x8 pb[C::KBW], sb[C::KBW];
-#pragma unroll
-            for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                if constexpr (BLK >= 32) {
-                    pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
-                    sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
-                } else {
-                    pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
-                    sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
-                }
-            }
-#pragma unroll
+        f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
+    #pragma unroll
+        for (int kbw = 0; kbw < C::KBW; ++kbw)
+    #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                bf16x8 oT, qT;
-                if constexpr (BLK >= 32) {
-                    oT = ld_tr_swz<D>(tO, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
-                    qT = ld_tr_swz<D>(tQ, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
-                } else {
-                    oT = ld_tr_swz_half<D>(tO, 4 * g, db * 16, r);
-                    qT = ld_tr_swz_half<D>(tQ, 4 * g, db * 16, r);
+                dvacc[kbw][db] = zero4();
+                dkacc[kbw][db] = zero4();
+            }
+
+        const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
+        const int e0 = col_ptr[cp], len = col_ptr[cp + 1] - e0;
+        // The column is walked from its last query block down: the key blocks of
+        // a head then visit the same query blocks at about the same time, which
+        // keeps those Q / dO tiles shared in L2.
+        auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
+        auto load_block = [&](int qb, int stage) {
+            const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
+            ld.issue(q + qbase, sQ[stage]);
+            ld.issue(dout + qbase, sdO[stage]);
+            if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL[stage], lane);
+            if (w == C::NW - 1) load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[stage], lane);
+        };
+
+        wait_loads_upto<0>();  // register loads done before the ring starts
+    #pragma unroll
+        for (int p = 0; p < C::NS - 1; ++p)
+            if (p < len) load_block(row_idx[entry(p)], p);
+        const float c2 = a.scale_log2;
+        int st = 0;
+        for (int sidx = 0; sidx < len; ++sidx) {
+            const int e = entry(sidx);
+            const int qb = row_idx[e];
+            const int i0 = qb * BLK;
+            const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+            pipeline_wait<C::NS, C::NI>(len - 1 - sidx);
+            __syncthreads();
+            if (sidx + C::NS - 1 < len) load_block(row_idx[entry(sidx + C::NS - 1)], st == 0 ? C::NS - 1 : st - 1);
+            const uint16_t* tQ = sQ[st];
+            const uint16_t* tO = sdO[st];
+            const float* tL = sL[st];
+            const float* tD = sDl[st];
+            st = st + 1 == C::NS ? 0 : st + 1;
+
+            // S and dP: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
+            f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
+    #pragma unroll
+            for (int qblk = 0; qblk < C::QB; ++qblk) {
+                bf16x8 qa[C::KS], oa[C::KS];
+    #pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    qa[ks] = ld_row_swz<D>(tQ, qblk * 16 + r, ks * 32 + 8 * g);
+                    oa[ks] = ld_row_swz<D>(tO, qblk * 16 + r, ks * 32 + 8 * g);
                 }
-#pragma unroll
+    #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
-                    dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
+                    f32x4 sacc = zero4(), dpacc = zero4();
+    #pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) {
+                        sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
+                        dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
+                    }
+                    p[kbw][qblk] = sacc;
+                    ds[kbw][qblk] = dpacc;
+                }
+            }
+            const int i0_mod = i0 % a.l;
+    #pragma unroll
+            for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                uint64_t bits = ~0ull;
+                if (masked) bits = col_mask(mp, cl[kbw], i0, i0_mod) >> (4 * g);
+    #pragma unroll
+                for (int qblk = 0; qblk < C::QB; ++qblk) {
+                    const uint32_t nib = (uint32_t)(bits >> (16 * qblk)) & 0xFu;
+                    const int cls = masked ? classify_sub(nib, nib) : SUB_ALL;
+                    if (cls == SUB_NONE) {
+                        p[kbw][qblk] = zero4();
+                        ds[kbw][qblk] = zero4();
+                        continue;
+                    }
+                    const f32x4 L = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
+                    const f32x4 Dl = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
+    #pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t]));
+                        if (cls == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits, 16 * qblk + t), pv);
+                        p[kbw][qblk][t] = pv;
+                        ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
+                    }
+                }
+            }
+
+            // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries;
+            // dO^T and Q^T are read transposed from the row-major tiles
+    #pragma unroll
+            for (int qc = 0; qc < C::QC; ++qc) {
+                bf16x8 pb[C::KBW], sb[C::KBW];
+    #pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                    if constexpr (BLK >= 32) {
+                        pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
+                        sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                    } else {
+                        pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
+                        sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
+                    }
+                }
+    #pragma unroll
+                for (int db = 0; db < C::DB; ++db) {
+                    bf16x8 oT, qT;
+                    if constexpr (BLK >= 32) {
+                        oT = ld_tr_swz<D>(tO, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                        qT = ld_tr_swz<D>(tQ, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                    } else {
+                        oT = ld_tr_swz_half<D>(tO, 4 * g, db * 16, r);
+                        qT = ld_tr_swz_half<D>(tQ, 4 * g, db * 16, r);
+                    }
+    #pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                        dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
+                        dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
+                    }
                 }
             }
         }
-    }
 
-    // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
-#pragma unroll
-    for (int kbw = 0; kbw < C::KBW; ++kbw) {
-        const int j = key0 + 16 * kbw + r;
-        uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
-        uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) {
-            *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[kbw][db]);
-            *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
+        // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
+    #pragma unroll
+        for (int kbw = 0; kbw < C::KBW; ++kbw) {
+            const int j = key0 + 16 * kbw + r;
+            uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
+            uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
+    #pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[kbw][db]);
+                *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
+            }
         }
+        if (tid == 0) sItem[(it + 1) & 1] = next;
+        // the ring is free again and the next claim is visible to every wave
+        __syncthreads();
     }
 }
 
@@ -520,13 +551,41 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
     }
 }
 
+// Byte offset of the queue counter inside the workspace (16-byte aligned).
+constexpr int64_t queue_offset(int64_t stats_bytes) { return (stats_bytes + 15) / 16 * 16; }
+
+unsigned long long* bwd_queue(float* workspace, int64_t rows) {
+    return reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(workspace) +
+                                                 queue_offset(2 * rows * (int64_t)sizeof(float)));
+}
+
+// Workgroups of `kernel` the current device holds at once (0 if unknown),
+// cached per device.
+template <typename K>
+int64_t resident_workgroups(K kernel, int threads) {
+    static std::atomic<int64_t> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    if (dev < 64) {
+        const int64_t v = cache[dev].load(std::memory_order_relaxed);
+        if (v > 0) return v;
+    }
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
+    const int64_t v = (int64_t)cus * per_cu;
+    if (dev < 64 && v > 0) cache[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
 template <int D>
 hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const void* v,
                           const void* o, const void* dout, const float* lse, void* dq, void* dk,
                           void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     hipLaunchKernelGGL((bwd_pre_kernel<D, float>), dim3((unsigned)((rows + 255) / 256)), dim3(256),
-                       0, stream, a, (const float*)o, (const float*)dout, lse, delta, delta + rows);
+                       0, stream, a, (const float*)o, (const float*)dout, lse, delta, delta + rows,
+                       (unsigned long long*)nullptr);
     dim3 grid((unsigned)((a.n + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
                        (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dq);
@@ -542,15 +601,20 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                            void* dv, float* delta, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     float* lse2 = delta + rows;
+    unsigned long long* queue = bwd_queue(delta, rows);
     hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)((rows + 255) / 256)),
-                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, delta, lse2);
+                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, delta, lse2,
+                       queue);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
                        a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
                        (const uint16_t*)dout, lse2, delta, (uint16_t*)dq);
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), grid, dim3(DkvCfg<D, BLK>::NT), 0, stream,
+    const int64_t items = (int64_t)a.nq * a.batch * a.heads;
+    const int64_t slots = resident_workgroups(bwd_dkdv_bf16_kernel<D, BLK>, DkvCfg<D, BLK>::NT);
+    const unsigned qgrid = (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), dim3(qgrid), dim3(DkvCfg<D, BLK>::NT), 0, stream,
                        a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dk, (uint16_t*)dv);
+                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dk, (uint16_t*)dv, queue);
     return hipGetLastError();
 }
 
@@ -570,7 +634,8 @@ hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, co
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype) {
     (void)d;
     (void)dtype;
-    return (size_t)(2 * batch * heads * n * (int64_t)sizeof(float));  // D_i and LSE_i log2 e per row
+    // D_i and LSE_i log2 e per row, then a 16-byte block holding the column queue
+    return (size_t)(queue_offset(2 * batch * heads * n * (int64_t)sizeof(float)) + 16);
 }
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,

@@ -41,7 +41,8 @@ struct AttnArgs {
 hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream);
 
-// Backward workspace: fp32 dq accumulator [b, h, n, d] and D [b, h, n].
+// Backward workspace: D and the base-2 LSE per row [b, h, n] (fp32), then a
+// 16-byte block for the column queue of the dK / dV kernel.
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype);
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
