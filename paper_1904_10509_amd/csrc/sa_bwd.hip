@@ -85,7 +85,7 @@ struct DqCfg {
     static constexpr int KB = BLK / 16;
     static constexpr int KC = (BLK + 31) / 32;
     static constexpr int DB = D / 16;
-    static constexpr int NS = 3;
+    static constexpr int NS = 2;
     static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;
 };
 
@@ -99,6 +99,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     using C = DqCfg<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
+    constexpr uint32_t kTileBytes = BLK * D * 2;
+    const uint32_t sK_base = lds_addr(&sK[0][0]), sV_base = lds_addr(&sV[0][0]);
 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
@@ -136,8 +138,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     ld.init(a.ss, w, lane);
     auto load_block = [&](int kb, int stage) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-        ld.issue(k + kbase, sK[stage]);
-        ld.issue(v + kbase, sV[stage]);
+        ld.issue(k + kbase, sK_base + stage * kTileBytes);
+        ld.issue(v + kbase, sV_base + stage * kTileBytes);
     };
     wait_loads_upto<0>();  // register loads done before the ring starts
 #pragma unroll
@@ -257,7 +259,7 @@ struct DkvCfg {
     static constexpr int QB = BLK / 16;             // 16-query blocks per tile
     static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
-    static constexpr int NS = 3;
+    static constexpr int NS = 2;
     // Q and dO tiles, plus the row statistics (wave 0 loads the LSE, the last
     // wave D; a single wave loads both)
     static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER + (NW == 1 ? 2 : 1);
@@ -277,6 +279,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
     __shared__ __attribute__((aligned(16))) float sDl[C::NS][64];
     __shared__ unsigned long long sItem[2];
+    constexpr uint32_t kTileBytes = BLK * D * 2;
+    const uint32_t sQ_base = lds_addr(&sQ[0][0]), sdO_base = lds_addr(&sdO[0][0]);
+    const uint32_t sL_base = lds_addr(&sL[0][0]), sDl_base = lds_addr(&sDl[0][0]);
 
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
@@ -335,10 +340,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
         auto load_block = [&](int qb, int stage) {
             const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
-            ld.issue(q + qbase, sQ[stage]);
-            ld.issue(dout + qbase, sdO[stage]);
-            if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL[stage], lane);
-            if (w == C::NW - 1) load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl[stage], lane);
+            ld.issue(q + qbase, sQ_base + stage * kTileBytes);
+            ld.issue(dout + qbase, sdO_base + stage * kTileBytes);
+            if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL_base + stage * 256u, lane);
+            if (w == C::NW - 1)
+                load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl_base + stage * 256u, lane);
         };
 
         wait_loads_upto<0>();  // register loads done before the ring starts

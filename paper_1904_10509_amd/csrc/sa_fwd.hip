@@ -35,7 +35,7 @@ struct FwdCfg {
     static constexpr int KB = BLK / 16;             // 16-key blocks per tile
     static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
     static constexpr int DB = D / 16;               // 16-wide d blocks of O
-    static constexpr int NS = 3;                    // K/V pipeline stages
+    static constexpr int NS = 2;                    // K/V pipeline stages
     static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;  // loads per wave per stage
 };
 
@@ -52,6 +52,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     // flight while one is computed; one barrier per key block
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
+    constexpr uint32_t kTileBytes = BLK * D * 2;
+    const uint32_t sK_base = lds_addr(&sK[0][0]), sV_base = lds_addr(&sV[0][0]);
 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
@@ -83,8 +85,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     ld.init(a.ss, w, lane);
     auto load_block = [&](int kb, int stage) {
         const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-        ld.issue(k + kbase, sK[stage]);
-        ld.issue(v + kbase, sV[stage]);
+        ld.issue(k + kbase, sK_base + stage * kTileBytes);
+        ld.issue(v + kbase, sV_base + stage * kTileBytes);
     };
 
     // The register loads above complete before the ring starts, so no

@@ -39,9 +39,10 @@ struct Swz {
     }
 };
 
-// Issue the loads of rows [0, BLK) of a [., D] bf16 tensor whose row 0 is at
-// `src` (row stride `ss` elements) into `tile`, spread over the NW waves.
 // LDS byte address of a pointer into a __shared__ array, made wave-uniform.
+// Ring stages are addressed as this base plus a stage offset: selecting
+// between generic pointers to different stages would make the compiler test
+// the pointer against the LDS aperture.
 __device__ inline uint32_t lds_addr(const void* p) {
     const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
     return __builtin_amdgcn_readfirstlane(a);
@@ -89,9 +90,9 @@ struct TileLoader {
             off[kk] = (uint32_t)((row * ss + 8 * chunk) * 2);
         }
     }
-    // src: first element of the tile's row 0 (wave-uniform)
-    __device__ void issue(const uint16_t* src, uint16_t* tile) const {
-        const uint32_t base = lds_addr(tile);
+    // src: first element of the tile's row 0 (wave-uniform); base: LDS byte
+    // address of the tile
+    __device__ void issue(const uint16_t* src, uint32_t base) const {
         const void* s = uniform_ptr(src);
 #pragma unroll
         for (int kk = 0; kk < PER; ++kk) dma_b128(s, off[kk], base + 1024 * (w + NW * kk));
@@ -99,10 +100,10 @@ struct TileLoader {
 };
 
 // 64 consecutive fp32 values starting at src (one per lane, lanes past
-// n_valid repeat the last value) into `dst`: one direct-to-LDS load.
-__device__ inline void load_row_stats_async(const float* src, int n_valid, float* dst, int lane) {
+// n_valid repeat the last value) to LDS byte address dst: one direct-to-LDS load.
+__device__ inline void load_row_stats_async(const float* src, int n_valid, uint32_t dst, int lane) {
     const uint32_t i = (uint32_t)(lane < n_valid ? lane : n_valid - 1);
-    dma_b32(uniform_ptr(src), 4u * i, lds_addr(dst));
+    dma_b32(uniform_ptr(src), 4u * i, dst);
 }
 
 // s_waitcnt vmcnt(N): at most N of this wave's global loads (including the
