@@ -35,10 +35,74 @@ def credited_flops(w, nnz):
     return 14.0 * w.block * w.block * w.d_head * blocks, 4.0 * w.block * w.block * w.d_head * blocks
 
 
+def executed_mfma_flops(w, nnz):
+    """MFMA work the kernels issue per present block and (batch, head): forward
+    2 products (QK^T, PV), dQ kernel 3 (QK^T, dO V^T, dS K), dK/dV kernel 4
+    (QK^T, dO V^T, P^T dO, dS^T Q).  Every block is computed whole."""
+    heads_per_layout = [w.heads] if len(nnz) == 1 else [(w.heads + 1) // 2, w.heads // 2]
+    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout))
+    return 18.0 * w.block * w.block * w.d_head * blocks
+
+
+def attended_pairs(w):
+    """sum_i |S_i| per (batch, head) for the merged sets of Sec. 4.3 (closed forms)."""
+    import numpy as np
+    from paper_1904_10509_amd.inputs import MODE_MERGED, STRIDED
+    if w.mode != MODE_MERGED:
+        return None
+    i = np.arange(w.n, dtype=np.int64)
+    if w.pattern == STRIDED:
+        cnt = np.minimum(i, w.stride) + 1 + np.maximum(0, i // w.stride - 1)
+    else:
+        cnt = i % w.stride + 1 + (i // w.stride) * w.summary
+    return int(cnt.sum())
+
+
 def algorithmic_bwd_bytes(w):
     """Backward call: read Q, K, V, O, dO, LSE; write dQ, dK, dV; D written and read."""
     e = w.batch * w.heads * w.n
     return 8 * e * w.d_head * 2 + 3 * e * 4
+
+
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic_sparse_attn_bwd_fixed_n65536.json")
+
+
+def kernel_sources_sha256():
+    """Digest of the HIP sources, to tell whether stored counter data is current."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_1904_10509_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per backward call from the stored rocprofv3 FETCH_SIZE / WRITE_SIZE
+    passes (copy-calibrated), or None when absent or taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_RECORD) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload_name or rec.get("source_sha256") != kernel_sources_sha256():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def copy_calibration(torch, dev):
+    """A copy-like elementwise kernel of known size (torch.neg: 256 MiB read,
+    256 MiB written), run when counters are collected so FETCH_SIZE /
+    WRITE_SIZE can be scaled to bytes."""
+    src = torch.empty(128 << 20, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def cpu_baseline(workloads, inputs):
@@ -73,6 +137,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -87,6 +153,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        copy_calibration(torch, dev)
 
     runs = []
     for name in BENCH_WORKLOADS:
@@ -137,8 +205,11 @@ def main():
         total_credited += cred
         fwd_ms_all.append(fwd_ms)
         bwd_ms_all.append(bwd_ms)
+        pairs = attended_pairs(w)
         per[w.name] = {
             "n": w.n, "nnz_blocks": r["lay"].nnz, "credited_flop": cred,
+            "element_level_flop": None if pairs is None else 14.0 * w.d_head * pairs * w.batch * w.heads,
+            "executed_mfma_flop": executed_mfma_flops(w, r["lay"].nnz),
             "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
             "fwd_tflops": cred_fwd / (fwd_ms * 1e-3) / 1e12,
             "bwd_tflops": (cred - cred_fwd) / (bwd_ms * 1e-3) / 1e12,
@@ -154,9 +225,9 @@ def main():
     cred, cred_fwd = credited_flops(dw, runs[dom]["lay"].nnz)
     achieved = (cred - cred_fwd) / (bwd_ms_all[dom] * 1e-3) / 1e12
     roofline = {
-        "kernel": f"sparse_attn_bwd on {dw.name} (bwd_pre + bwd_dkdv_bf16 + bwd_dq_convert launches)",
+        "kernel": f"sparse_attn_bwd on {dw.name} (bwd_pre + bwd_dq_bf16 + bwd_dkdv_bf16 launches)",
         "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(dw.name),
         "avg_ms": bwd_ms_all[dom], "algorithmic_bytes": algorithmic_bwd_bytes(dw),
     }
 

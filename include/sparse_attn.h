@@ -140,7 +140,9 @@ int sparse_attn_fwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     void* stream);
 
 /*
- * Bytes of device workspace that sparse_attn_bwd needs (host only).
+ * Bytes of device workspace that sparse_attn_bwd needs (host only): row
+ * statistics (8 bytes per query row and head), work-queue counters and the
+ * per-layout order in which the dK / dV kernel takes key blocks.
  */
 int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
                                    int32_t summary_c, int32_t pattern, int32_t head_mode,

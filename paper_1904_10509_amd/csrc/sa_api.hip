@@ -83,6 +83,7 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.scale = scale;
     a.scale_log2 = scale * sa::kLog2eHost;
     a.period_bits = sa::host_period_bits(p.l);
+    a.dl = sa::make_divl(p.l);
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;
     a.kind = kind;
@@ -159,7 +160,7 @@ int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
     if (st != SA_OK) return st;
     if (batch < 1 || heads < 1 || (dtype != SA_F32 && dtype != SA_BF16) || !bytes) return SA_ERR_INVALID;
     if (d_head != 32 && d_head != 64 && d_head != 128) return SA_ERR_UNSUPPORTED;
-    *bytes = sa::bwd_workspace_bytes(batch, heads, n, d_head, dtype);
+    *bytes = sa::bwd_workspace_bytes(batch, heads, n, p.nq, p.n_layouts);
     return SA_OK;
 }
 
@@ -182,7 +183,7 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return SA_ERR_INVALID;
     if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
-    const size_t need = sa::bwd_workspace_bytes(batch, heads, n, d_head, dtype);
+    const size_t need = sa::bwd_workspace_bytes(batch, heads, n, p.nq, p.n_layouts);
     if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
     if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;
     sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,

@@ -20,8 +20,15 @@
 // key blocks holding summary columns are long), and a hardware placement of
 // one workgroup per column can then pile the long columns onto a few compute
 // units.  The dkdv grid is therefore sized to the resident capacity of the
-// device and each workgroup claims columns from an atomic counter in the
-// workspace, longest-first order (ascending key block).
+// device and workgroups claim columns from atomic counters in the workspace:
+//   - one queue per XCD (the die whose L2 serves the workgroup), holding the
+//     heads bh = x (mod 8), so the columns of a head share one L2;
+//   - inside a queue, longest columns first (the pre kernel sorts the key
+//     blocks of each layout by column length into length classes), so the
+//     long columns of a head start together and walk the same Q / dO tiles
+//     at about the same time;
+//   - a workgroup whose own queue is empty takes work from the others, so
+//     every column is processed whatever the placement of workgroups is.
 // The dq kernel repeats the S and dP products of the dkdv kernel; those two
 // extra products per block are the price of having no reduction across
 // workgroups.
@@ -41,14 +48,64 @@ namespace {
 // ---------------------------------------------------------------------------
 // shared pieces
 // ---------------------------------------------------------------------------
-// One thread per row: D_i = sum_t dO[i,t] O[i,t] (fp32), and the saved LSE in
-// base-2 units (LSE * log2 e) for the exp2 recomputation of P.
+// One thread per row: -D_i = -sum_t dO[i,t] O[i,t] (fp32), and the saved LSE
+// in base-2 units, negated (-LSE * log2 e), for the exp2 recomputation of P.
+// Both are stored negated because the kernels add them: -D_i is where the
+// dP accumulation starts, and P = exp2(scale log2 e * s - LSE log2 e) is one
+// fused multiply-add.
+// Schedule of the dK / dV kernel.
+constexpr int kQueues = 8;          // one per XCD
+constexpr int kLengthClasses = 128;  // four per octave of column length
+
+// Length class of a column of `len` blocks; longer columns get lower classes.
+__device__ inline int length_class(int len) {
+    if (len <= 0) return kLengthClasses - 1;
+    const int lg = 31 - __builtin_clz((unsigned)len);
+    const int frac = lg >= 2 ? (len >> (lg - 2)) & 3 : (len << (2 - lg)) & 3;
+    return kLengthClasses - 2 - (4 * lg + frac);
+}
+
+// Queue x holds the (batch, head) pairs bh = x (mod kQueues).
+__device__ inline int64_t queue_heads(int64_t bh_count, int x) {
+    return bh_count > x ? (bh_count - 1 - x) / kQueues + 1 : 0;
+}
+
+// Workgroup 0 of the pre kernel: empty queues, and per layout the key blocks
+// ordered by length class (order inside a class is arbitrary; it only
+// affects scheduling).
+__device__ void build_schedule(const AttnArgs& a, unsigned long long* queue, int32_t* order) {
+    __shared__ int cls_pos[kLengthClasses];
+    const int tid = threadIdx.x;
+    if (tid < kQueues) queue[tid] = 0ull;
+    const int n_layouts = a.mode == MODE_INTERLEAVED ? 2 : 1;
+    for (int g = 0; g < n_layouts; ++g) {
+        const int32_t* cp = a.col_ptr + (int64_t)g * (a.nq + 1);
+        for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
+        __syncthreads();
+        for (int kb = tid; kb < a.nq; kb += blockDim.x) atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+        __syncthreads();
+        if (tid == 0) {
+            int run = 0;
+            for (int i = 0; i < kLengthClasses; ++i) {
+                const int c = cls_pos[i];
+                cls_pos[i] = run;
+                run += c;
+            }
+        }
+        __syncthreads();
+        for (int kb = tid; kb < a.nq; kb += blockDim.x)
+            order[(int64_t)g * a.nq + atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = kb;
+        __syncthreads();
+    }
+}
+
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
 bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, const float* __restrict__ lse,
-               float* __restrict__ delta, float* __restrict__ lse2, unsigned long long* __restrict__ queue) {
+               float* __restrict__ ndelta, float* __restrict__ nlse2, unsigned long long* __restrict__ queue,
+               int32_t* __restrict__ order) {
+    if (blockIdx.x == 0 && queue) build_schedule(a, queue, order);
     const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (row == 0 && queue) *queue = 0ull;  // the dkdv column queue starts empty
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     if (row >= rows) return;
     const int64_t bh = row / a.n, i = row % a.n;
@@ -68,8 +125,8 @@ bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, 
     } else {
         for (int t = 0; t < D; ++t) acc = fmaf(o[off + t], dout[off + t], acc);
     }
-    delta[row] = acc;
-    lse2[row] = lse[row] * kLog2e;  // -inf stays -inf
+    ndelta[row] = -acc;
+    nlse2[row] = -lse[row] * kLog2e;  // an empty row (LSE = -inf) gives +inf; its items are all masked
 }
 
 // ---------------------------------------------------------------------------
@@ -85,8 +142,7 @@ struct DqCfg {
     static constexpr int KB = BLK / 16;
     static constexpr int KC = (BLK + 31) / 32;
     static constexpr int DB = D / 16;
-    static constexpr int NS = 2;
-    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;
+    static constexpr int NS = 2;  // K / V ring stages
 };
 
 template <int D, int BLK>
@@ -94,7 +150,7 @@ __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                    const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
-                   const float* __restrict__ lse2, const float* __restrict__ delta,
+                   const float* __restrict__ nlse2, const float* __restrict__ ndelta,
                    uint16_t* __restrict__ dq) {
     using C = DqCfg<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
@@ -111,10 +167,13 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
     const float c2 = a.scale_log2;
+    constexpr uint64_t kTileBits = BLK == 64 ? ~0ull : (1ull << BLK) - 1;
 
-    // this lane's query rows row0 + 16u + r: Q and dO as B operands, LSE (log2 units) and D
+    // this lane's query rows row0 + 16u + r: Q and dO as B operands, -LSE log2 e,
+    // and -D splat over a D-result quad (where dP^T accumulation starts)
     bf16x8 qf[C::QBW][C::KS], of[C::QBW][C::KS];
-    float L2[C::QBW], Dl[C::QBW];
+    float nl2[C::QBW];
+    f32x4 nd4[C::QBW];
     RowLane rl[C::QBW];
     f32x4 dqacc[C::QBW][C::DB];
 #pragma unroll
@@ -125,15 +184,16 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             qf[u][ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
             of[u][ks] = ld_bf16x8(dout + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
         }
-        L2[u] = lse2[rowbase + i];
-        Dl[u] = delta[rowbase + i];
-        rl[u] = row_lane(i, a.l);
+        nl2[u] = nlse2[rowbase + i];
+        const float nd = ndelta[rowbase + i];
+        nd4[u] = f32x4{nd, nd, nd, nd};
+        rl[u] = row_lane(i, a.dl);
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) dqacc[u][db] = zero4();
     }
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = row_ptr[rp], e1 = row_ptr[rp + 1];
+    const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
     auto load_block = [&](int kb, int stage) {
@@ -142,22 +202,22 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         ld.issue(v + kbase, sV_base + stage * kTileBytes);
     };
     wait_loads_upto<0>();  // register loads done before the ring starts
-#pragma unroll
-    for (int p = 0; p < C::NS - 1; ++p)
-        if (e0 + p < e1) load_block(col_idx[e0 + p], p);
-    int st = 0;
+    // two-stage ring; the next block's index is read one step ahead
+    int kb_next = e0 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e0]) : 0;
+    if (e0 < e1) load_block(kb_next, 0);
     for (int e = e0; e < e1; ++e) {
-        const int kb = col_idx[e];
+        const int kb = kb_next;
+        const int st = (e - e0) & 1;
+        kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
-        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
-        pipeline_wait<C::NS, C::NI>(e1 - 1 - e);
-        __syncthreads();
-        if (e + C::NS - 1 < e1) load_block(col_idx[e + C::NS - 1], st == 0 ? C::NS - 1 : st - 1);
+        const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        wait_loads_upto<0>();
+        __syncthreads();  // block e is in LDS everywhere; the other stage is free
+        if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        st = st + 1 == C::NS ? 0 : st + 1;
 
-        // S^T and dP^T: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
+        // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
         f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
 #pragma unroll
         for (int kblk = 0; kblk < C::KB; ++kblk) {
@@ -170,7 +230,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
                 s[u][kblk] = zero4();
-                dp[u][kblk] = zero4();
+                dp[u][kblk] = nd4[u];
 #pragma unroll
                 for (int ks = 0; ks < C::KS; ++ks) {
                     s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
@@ -178,46 +238,48 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                 }
             }
         }
-        int cls[C::KB];
+        // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
+        // which 32-key chunks hold an attended item anywhere in the wave
         uint64_t bits[C::QBW];
+        bool live[C::QBW][C::KC];
 #pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) cls[kblk] = SUB_ALL;
+        for (int u = 0; u < C::QBW; ++u) {
+            bits[u] = ~0ull;
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = true;
+        }
         if (masked) {
-            const int j0_mod = j0 % a.l;
-            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+            const int j0_mod = mod_l(a.dl, j0);
+            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
 #pragma unroll
-            for (int u = 0; u < C::QBW; ++u) bits[u] = row_mask(mp, rl[u], j0, j0_mod, sum) >> (4 * g);
+            for (int u = 0; u < C::QBW; ++u) {
+                bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk) {
-                uint32_t any = 0u, all = 0xFu;
-#pragma unroll
-                for (int u = 0; u < C::QBW; ++u) {
-                    const uint32_t nib = (uint32_t)(bits[u] >> (16 * kblk)) & 0xFu;
-                    any |= nib;
-                    all &= nib;
-                }
-                cls[kblk] = classify_sub(any, all);
+                for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = wave_any(chunk_bits(bits[u], kc, C::KB >= 2));
             }
         }
-        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - L2)
+        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
         bf16x8 dsf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk) {
-                if (cls[kblk] == SUB_NONE) {
-                    s[u][kblk] = zero4();
-                    continue;
-                }
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    float pv = exp2_fast(fmaf(s[u][kblk][t], c2, -L2[u]));
-                    if (cls[kblk] == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
-                    s[u][kblk][t] = pv * (dp[u][kblk][t] - Dl[u]);
-                }
-            }
-#pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
+                constexpr int HK = C::KB >= 2 ? 2 : 1;
+                if (live[u][kc]) {
+#pragma unroll
+                    for (int hk = 0; hk < HK; ++hk) {
+                        const int kblk = 2 * kc + hk;
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            float pv = exp2_fast(fmaf(s[u][kblk][t], c2, nl2[u]));
+                            if (masked) pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
+                            s[u][kblk][t] = pv * dp[u][kblk][t];
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
+                }
                 if constexpr (BLK >= 32) dsf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
                 else dsf[u][kc] = pack_bf16x8(s[u][0], zero4());
             }
@@ -259,10 +321,7 @@ struct DkvCfg {
     static constexpr int QB = BLK / 16;             // 16-query blocks per tile
     static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
-    static constexpr int NS = 2;
-    // Q and dO tiles, plus the row statistics (wave 0 loads the LSE, the last
-    // wave D; a single wave loads both)
-    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER + (NW == 1 ? 2 : 1);
+    static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
 };
 
 template <int D, int BLK>
@@ -270,9 +329,9 @@ __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int32_t* __restrict__ row_idx,
                      const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
-                     const float* __restrict__ lse2, const float* __restrict__ delta,
+                     const float* __restrict__ nlse2, const float* __restrict__ ndelta,
                      uint16_t* __restrict__ dk, uint16_t* __restrict__ dv,
-                     unsigned long long* __restrict__ queue) {
+                     unsigned long long* __restrict__ queue, const int32_t* __restrict__ order) {
     using C = DkvCfg<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
@@ -280,30 +339,54 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     __shared__ __attribute__((aligned(16))) float sDl[C::NS][64];
     __shared__ unsigned long long sItem[2];
     constexpr uint32_t kTileBytes = BLK * D * 2;
+    constexpr uint64_t kTileBits = BLK == 64 ? ~0ull : (1ull << BLK) - 1;
     const uint32_t sQ_base = lds_addr(&sQ[0][0]), sdO_base = lds_addr(&sdO[0][0]);
     const uint32_t sL_base = lds_addr(&sL[0][0]), sDl_base = lds_addr(&sDl[0][0]);
 
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int64_t bh_count = (int64_t)a.batch * a.heads;
-    const uint64_t items = (uint64_t)a.nq * bh_count;
+    const float c2 = a.scale_log2;
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
-    if (tid == 0) sItem[0] = atomicAdd(queue, 1ull);
+    // Claims are made by thread 0, which walks the queues from its own XCD's
+    // on; a claim is (queue << 56 | index), kNoWork once all queues are dry.
+    constexpr unsigned long long kNoWork = ~0ull;
+    int qx = 0, q_left = kQueues;
+    if (tid == 0) {
+        unsigned xcc;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
+        qx = (int)(xcc % kQueues);
+    }
+    auto claim = [&]() -> unsigned long long {
+        while (q_left > 0) {
+            const uint64_t t = atomicAdd(queue + qx, 1ull);
+            if (t < (uint64_t)a.nq * (uint64_t)queue_heads(bh_count, qx)) return ((uint64_t)qx << 56) | t;
+            qx = qx + 1 == kQueues ? 0 : qx + 1;
+            --q_left;
+        }
+        return kNoWork;
+    };
+    if (tid == 0) sItem[0] = claim();
     __syncthreads();
-    // Every wave leaves the loop at the same claim: the claimed index is
-    // shared through LDS and is past the end once the queue has run dry.
+    // Every wave leaves the loop at the same claim: the claim is shared
+    // through LDS and is kNoWork once every queue has run dry.
     for (int it = 0;; ++it) {
         const uint64_t item = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sItem[it & 1] >> 32)) << 32) |
                               __builtin_amdgcn_readfirstlane((uint32_t)sItem[it & 1]);
-        if (item >= items) break;
+        if (item == kNoWork) break;
         unsigned long long next = 0ull;
-        if (tid == 0) next = atomicAdd(queue, 1ull);  // claimed now, published after the column
-        // ascending key block: under causality the low key blocks have the longest columns
-        const int kb = (int)(item / (uint64_t)bh_count);
-        const int bh = (int)(item - (uint64_t)kb * bh_count);
+        if (tid == 0) next = claim();  // claimed now, published after the column
+        const int x = (int)(item >> 56);
+        const uint64_t t = item & ((1ull << 56) - 1);
+        const int64_t nx = queue_heads(bh_count, x);
+        // (the scalar unit holds every index of the column walk; the
+        // readfirstlane calls only tell the compiler so)
+        const int rank = __builtin_amdgcn_readfirstlane((int)(t / (uint64_t)nx));  // position in the length order
+        const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
         const int h = bh % a.heads, b = bh / a.heads;
         const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+        const int kb = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * a.nq + rank]);
         const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
@@ -312,75 +395,82 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
         bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
         ColLane cl[C::KBW];
-    #pragma unroll
+#pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
             const int j = key0 + 16 * kbw + r;
-    #pragma unroll
+#pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
                 kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
                 vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
             }
-            cl[kbw] = col_lane(j, a.l, a.c);
+            cl[kbw] = col_lane(j, a.dl, a.c);
         }
-
         f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
-    #pragma unroll
+#pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw)
-    #pragma unroll
+#pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 dvacc[kbw][db] = zero4();
                 dkacc[kbw][db] = zero4();
             }
 
         const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
-        const int e0 = col_ptr[cp], len = col_ptr[cp + 1] - e0;
-        // The column is walked from its last query block down: the key blocks of
-        // a head then visit the same query blocks at about the same time, which
-        // keeps those Q / dO tiles shared in L2.
+        const int e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
+        const int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
+        // The column is walked from its last query block down: the long
+        // columns of a head, started together, then visit the same query
+        // blocks at about the same time and share those Q / dO tiles in L2.
         auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
         auto load_block = [&](int qb, int stage) {
             const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
             ld.issue(q + qbase, sQ_base + stage * kTileBytes);
             ld.issue(dout + qbase, sdO_base + stage * kTileBytes);
-            if (w == 0) load_row_stats_async(lse2 + rowbase + (int64_t)qb * BLK, BLK, sL_base + stage * 256u, lane);
+            if (w == 0) load_row_stats_async(nlse2 + rowbase + (int64_t)qb * BLK, BLK, sL_base + stage * 256u, lane);
             if (w == C::NW - 1)
-                load_row_stats_async(delta + rowbase + (int64_t)qb * BLK, BLK, sDl_base + stage * 256u, lane);
+                load_row_stats_async(ndelta + rowbase + (int64_t)qb * BLK, BLK, sDl_base + stage * 256u, lane);
         };
 
         wait_loads_upto<0>();  // register loads done before the ring starts
-    #pragma unroll
-        for (int p = 0; p < C::NS - 1; ++p)
-            if (p < len) load_block(row_idx[entry(p)], p);
-        const float c2 = a.scale_log2;
-        int st = 0;
+        // two-stage ring: the next block's index is read one step ahead (a
+        // scalar load, off the vector-memory counter the ring waits on)
+        int qb_next = len > 0 ? __builtin_amdgcn_readfirstlane(row_idx[entry(0)]) : 0;
+        if (len > 0) load_block(qb_next, 0);
         for (int sidx = 0; sidx < len; ++sidx) {
-            const int e = entry(sidx);
-            const int qb = row_idx[e];
+            const int qb = qb_next;
+            const int st = sidx & 1;
+            qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
-            const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
-            pipeline_wait<C::NS, C::NI>(len - 1 - sidx);
-            __syncthreads();
-            if (sidx + C::NS - 1 < len) load_block(row_idx[entry(sidx + C::NS - 1)], st == 0 ? C::NS - 1 : st - 1);
+            const bool masked =
+                !block_full32(a.pattern, mp.part, a.dl, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+            wait_loads_upto<0>();
+            __syncthreads();  // block sidx is in LDS everywhere; the other stage is free
+            if (sidx + 1 < len) load_block(qb_next, st ^ 1);
             const uint16_t* tQ = sQ[st];
             const uint16_t* tO = sdO[st];
             const float* tL = sL[st];
             const float* tD = sDl[st];
-            st = st + 1 == C::NS ? 0 : st + 1;
 
-            // S and dP: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
+            // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
+            f32x4 nl[C::QB], nd[C::QB];
+#pragma unroll
+            for (int qblk = 0; qblk < C::QB; ++qblk) {
+                nl[qblk] = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
+                nd[qblk] = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
+            }
+            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
             f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
-    #pragma unroll
+#pragma unroll
             for (int qblk = 0; qblk < C::QB; ++qblk) {
                 bf16x8 qa[C::KS], oa[C::KS];
-    #pragma unroll
+#pragma unroll
                 for (int ks = 0; ks < C::KS; ++ks) {
                     qa[ks] = ld_row_swz<D>(tQ, qblk * 16 + r, ks * 32 + 8 * g);
                     oa[ks] = ld_row_swz<D>(tO, qblk * 16 + r, ks * 32 + 8 * g);
                 }
-    #pragma unroll
+#pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    f32x4 sacc = zero4(), dpacc = zero4();
-    #pragma unroll
+                    f32x4 sacc = zero4(), dpacc = nd[qblk];
+#pragma unroll
                     for (int ks = 0; ks < C::KS; ++ks) {
                         sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
                         dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
@@ -389,39 +479,54 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     ds[kbw][qblk] = dpacc;
                 }
             }
-            const int i0_mod = i0 % a.l;
-    #pragma unroll
+            // mask bits of this lane's column (bit 16 qblk + t after the shift),
+            // and which 32-query chunks hold an attended item anywhere in the wave
+            uint64_t bits[C::KBW];
+            bool live[C::KBW][C::QC];
+#pragma unroll
             for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                uint64_t bits = ~0ull;
-                if (masked) bits = col_mask(mp, cl[kbw], i0, i0_mod) >> (4 * g);
-    #pragma unroll
-                for (int qblk = 0; qblk < C::QB; ++qblk) {
-                    const uint32_t nib = (uint32_t)(bits >> (16 * qblk)) & 0xFu;
-                    const int cls = masked ? classify_sub(nib, nib) : SUB_ALL;
-                    if (cls == SUB_NONE) {
-                        p[kbw][qblk] = zero4();
-                        ds[kbw][qblk] = zero4();
-                        continue;
-                    }
-                    const f32x4 L = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
-                    const f32x4 Dl = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
-    #pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, -L[t]));
-                        if (cls == SUB_MIXED) pv = select_or_zero(bit_lane_mask(bits, 16 * qblk + t), pv);
-                        p[kbw][qblk][t] = pv;
-                        ds[kbw][qblk][t] = pv * (ds[kbw][qblk][t] - Dl[t]);
-                    }
+                bits[kbw] = ~0ull;
+#pragma unroll
+                for (int qc = 0; qc < C::QC; ++qc) live[kbw][qc] = true;
+            }
+            if (masked) {
+                const int i0_mod = mod_l(a.dl, i0);
+#pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                    bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
+#pragma unroll
+                    for (int qc = 0; qc < C::QC; ++qc) live[kbw][qc] = wave_any(chunk_bits(bits[kbw], qc, C::QB >= 2));
                 }
             }
 
-            // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries;
-            // dO^T and Q^T are read transposed from the row-major tiles
-    #pragma unroll
+            // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then
+            // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's
+            // queries; dO^T and Q^T are read transposed from the row-major tiles
+#pragma unroll
             for (int qc = 0; qc < C::QC; ++qc) {
+                constexpr int HQ = C::QB >= 2 ? 2 : 1;
                 bf16x8 pb[C::KBW], sb[C::KBW];
-    #pragma unroll
+#pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                    if (live[kbw][qc]) {
+#pragma unroll
+                        for (int hq = 0; hq < HQ; ++hq) {
+                            const int qblk = 2 * qc + hq;
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) {
+                                float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[qblk][t]));
+                                if (masked) pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
+                                p[kbw][qblk][t] = pv;
+                                ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
+                            }
+                        }
+                    } else {
+#pragma unroll
+                        for (int hq = 0; hq < HQ; ++hq) {
+                            p[kbw][2 * qc + hq] = zero4();
+                            ds[kbw][2 * qc + hq] = zero4();
+                        }
+                    }
                     if constexpr (BLK >= 32) {
                         pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
                         sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
@@ -430,7 +535,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                         sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
                     }
                 }
-    #pragma unroll
+#pragma unroll
                 for (int db = 0; db < C::DB; ++db) {
                     bf16x8 oT, qT;
                     if constexpr (BLK >= 32) {
@@ -440,7 +545,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                         oT = ld_tr_swz_half<D>(tO, 4 * g, db * 16, r);
                         qT = ld_tr_swz_half<D>(tQ, 4 * g, db * 16, r);
                     }
-    #pragma unroll
+#pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
                         dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
                         dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
@@ -450,12 +555,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         }
 
         // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
-    #pragma unroll
+#pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
             const int j = key0 + 16 * kbw + r;
             uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
-    #pragma unroll
+#pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[kbw][db]);
                 *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
@@ -474,7 +579,7 @@ template <int D>
 __global__ void __launch_bounds__(64)
 bwd_dq_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict__ k,
                   const float* __restrict__ v, const float* __restrict__ dout,
-                  const float* __restrict__ lse, const float* __restrict__ delta,
+                  const float* __restrict__ lse, const float* __restrict__ ndelta,
                   float* __restrict__ dq) {
     const int h = blockIdx.y, b = blockIdx.z;
     const int i = blockIdx.x * 64 + threadIdx.x;
@@ -484,7 +589,7 @@ bwd_dq_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restri
     const int part = part_of_head(a.mode, h);
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowid = ((int64_t)b * a.heads + h) * a.n + i;
-    const float L = lse[rowid], Di = delta[rowid];
+    const float L = lse[rowid], nDi = ndelta[rowid];
     const float* qr = q + base + (int64_t)i * a.ss;
     const float* gr = dout + base + (int64_t)i * a.ss;
     float acc[D];
@@ -504,7 +609,7 @@ bwd_dq_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restri
                 dp = fmaf(gr[t], vr[t], dp);
             }
             const float p = expf(s * a.scale - L);
-            const float dsv = p * (dp - Di);
+            const float dsv = p * (dp + nDi);
             for (int t = 0; t < D; ++t) acc[t] = fmaf(dsv, kr[t], acc[t]);
         }
     }
@@ -515,7 +620,7 @@ template <int D>
 __global__ void __launch_bounds__(64)
 bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict__ k,
                     const float* __restrict__ v, const float* __restrict__ dout,
-                    const float* __restrict__ lse, const float* __restrict__ delta,
+                    const float* __restrict__ lse, const float* __restrict__ ndelta,
                     float* __restrict__ dk, float* __restrict__ dv) {
     const int h = blockIdx.y, b = blockIdx.z;
     const int jx = blockIdx.x * 64 + threadIdx.x;
@@ -544,7 +649,7 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
                 dp = fmaf(gr[t], vr[t], dp);
             }
             const float p = expf(s * a.scale - lse[rowbase + i]);
-            const float dsv = p * (dp - delta[rowbase + i]);
+            const float dsv = p * (dp + ndelta[rowbase + i]);
             for (int t = 0; t < D; ++t) {
                 av[t] = fmaf(p, gr[t], av[t]);
                 ak[t] = fmaf(dsv, qr[t], ak[t]);
@@ -557,12 +662,29 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
     }
 }
 
-// Byte offset of the queue counter inside the workspace (16-byte aligned).
-constexpr int64_t queue_offset(int64_t stats_bytes) { return (stats_bytes + 15) / 16 * 16; }
+// Workspace: -D [rows] and -LSE log2 e [rows] (fp32), then (16-byte aligned)
+// the kQueues queue counters and the key-block order of each layout.
+struct BwdWorkspace {
+    float* ndelta;  // -D
+    float* nlse2;   // -LSE log2 e
+    unsigned long long* queue;
+    int32_t* order;
+};
 
-unsigned long long* bwd_queue(float* workspace, int64_t rows) {
-    return reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(workspace) +
-                                                 queue_offset(2 * rows * (int64_t)sizeof(float)));
+constexpr int64_t align16(int64_t x) { return (x + 15) / 16 * 16; }
+
+int64_t bwd_workspace_size(int64_t rows, int64_t nq, int n_layouts) {
+    return align16(2 * rows * (int64_t)sizeof(float)) + kQueues * 8 + n_layouts * nq * 4;
+}
+
+BwdWorkspace bwd_workspace(void* ws, int64_t rows) {
+    char* p = static_cast<char*>(ws);
+    BwdWorkspace w;
+    w.ndelta = reinterpret_cast<float*>(p);
+    w.nlse2 = w.ndelta + rows;
+    w.queue = reinterpret_cast<unsigned long long*>(p + align16(2 * rows * (int64_t)sizeof(float)));
+    w.order = reinterpret_cast<int32_t*>(w.queue + kQueues);
+    return w;
 }
 
 // Workgroups of `kernel` the current device holds at once (0 if unknown),
@@ -587,16 +709,17 @@ int64_t resident_workgroups(K kernel, int threads) {
 template <int D>
 hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const void* v,
                           const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                          void* dv, float* delta, hipStream_t stream) {
+                          void* dv, const BwdWorkspace& ws, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
+    float* ndelta = ws.ndelta;
     hipLaunchKernelGGL((bwd_pre_kernel<D, float>), dim3((unsigned)((rows + 255) / 256)), dim3(256),
-                       0, stream, a, (const float*)o, (const float*)dout, lse, delta, delta + rows,
-                       (unsigned long long*)nullptr);
+                       0, stream, a, (const float*)o, (const float*)dout, lse, ndelta, ws.nlse2,
+                       (unsigned long long*)nullptr, (int32_t*)nullptr);
     dim3 grid((unsigned)((a.n + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
-                       (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dq);
+                       (const float*)k, (const float*)v, (const float*)dout, lse, ndelta, (float*)dq);
     hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
-                       (const float*)k, (const float*)v, (const float*)dout, lse, delta, (float*)dk,
+                       (const float*)k, (const float*)v, (const float*)dout, lse, ndelta, (float*)dk,
                        (float*)dv);
     return hipGetLastError();
 }
@@ -604,61 +727,58 @@ hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const
 template <int D, int BLK>
 hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                           void* dv, float* delta, hipStream_t stream) {
+                           void* dv, const BwdWorkspace& ws, hipStream_t stream) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
-    float* lse2 = delta + rows;
-    unsigned long long* queue = bwd_queue(delta, rows);
+    float* ndelta = ws.ndelta;
+    float* nlse2 = ws.nlse2;
     hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)((rows + 255) / 256)),
-                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, delta, lse2,
-                       queue);
+                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2,
+                       ws.queue, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
                        a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dq);
+                       (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     const int64_t slots = resident_workgroups(bwd_dkdv_bf16_kernel<D, BLK>, DkvCfg<D, BLK>::NT);
     const unsigned qgrid = (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
     hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), dim3(qgrid), dim3(DkvCfg<D, BLK>::NT), 0, stream,
                        a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, lse2, delta, (uint16_t*)dk, (uint16_t*)dv, queue);
+                       (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv, ws.queue, ws.order);
     return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, const void* v,
                              const void* o, const void* dout, const float* lse, void* dq,
-                             void* dk, void* dv, float* delta, hipStream_t stream) {
+                             void* dk, void* dv, const BwdWorkspace& ws, hipStream_t stream) {
     switch (a.block) {
-    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
     }
 }
 
 }  // namespace
 
-size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype) {
-    (void)d;
-    (void)dtype;
-    // D_i and LSE_i log2 e per row, then a 16-byte block holding the column queue
-    return (size_t)(queue_offset(2 * batch * heads * n * (int64_t)sizeof(float)) + 16);
+size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, int n_layouts) {
+    return (size_t)bwd_workspace_size(batch * heads * n, nq, n_layouts);
 }
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
                       void* dv, void* workspace, hipStream_t stream) {
-    float* delta = static_cast<float*>(workspace);
+    const BwdWorkspace ws = bwd_workspace(workspace, (int64_t)a.batch * a.heads * a.n);
     if (dtype == 1) {
         switch (a.d) {
-        case 32: return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-        case 64: return launch_bwd_bf16_d<64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-        default: return launch_bwd_bf16_d<128>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+        case 32: return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+        case 64: return launch_bwd_bf16_d<64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+        default: return launch_bwd_bf16_d<128>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
         }
     }
     switch (a.d) {
-    case 32: return launch_bwd_f32<32>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-    case 64: return launch_bwd_f32<64>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
-    default: return launch_bwd_f32<128>(a, q, k, v, o, dout, lse, dq, dk, dv, delta, stream);
+    case 32: return launch_bwd_f32<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    case 64: return launch_bwd_f32<64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    default: return launch_bwd_f32<128>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
     }
 }
 

@@ -4,8 +4,8 @@
 // one running maximum and sum per row (online softmax) and saves
 // LSE = log(sum_j exp(s_ij)) for the recomputing backward (Sec. 5.4).
 //
-// bf16 path: one workgroup per (query block qb, head, batch), B/16 waves of
-// 16 query rows each.  Per present key block kb:
+// bf16 path: one workgroup per (query block qb, head, batch), waves of 32
+// query rows (one wave of 16 rows for B = 16).  Per present key block kb:
 //   S^T = K_kb Q^T        (MFMA 16x16x32, K from LDS, Q fragment in VGPRs)
 //   mask (MASKED blocks), running max over the row, P = exp2(S - m)
 //   O^T += V_kb^T P^T     (MFMA; P^T is fed from the S^T results directly)
@@ -35,8 +35,7 @@ struct FwdCfg {
     static constexpr int KB = BLK / 16;             // 16-key blocks per tile
     static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
     static constexpr int DB = D / 16;               // 16-wide d blocks of O
-    static constexpr int NS = 2;                    // K/V pipeline stages
-    static constexpr int NI = 2 * TileLoader<D, BLK, NW>::PER;  // loads per wave per stage
+    static constexpr int NS = 2;                    // K / V ring stages
 };
 
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
@@ -48,11 +47,12 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                 const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
     using C = FwdCfg<D, BLK>;
-    // K and V tiles in an NS-stage ring: the next NS-1 key blocks are in
-    // flight while one is computed; one barrier per key block
+    // K and V tiles in a two-stage ring: the next key block is in flight
+    // while one is computed; one barrier per key block
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
     constexpr uint32_t kTileBytes = BLK * D * 2;
+    constexpr uint64_t kTileBits = BLK == 64 ? ~0ull : (1ull << BLK) - 1;
     const uint32_t sK_base = lds_addr(&sK[0][0]), sV_base = lds_addr(&sV[0][0]);
 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
@@ -76,11 +76,11 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         for (int db = 0; db < C::DB; ++db) oacc[u][db] = zero4();
         m_run[u] = -INFINITY;
         l_run[u] = 0.f;
-        rl[u] = row_lane(row0 + 16 * u + r, a.l);
+        rl[u] = row_lane(row0 + 16 * u + r, a.dl);
     }
 
     const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = row_ptr[rp], e1 = row_ptr[rp + 1];
+    const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
     auto load_block = [&](int kb, int stage) {
@@ -93,21 +93,22 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     // compiler-tracked load is outstanding inside the loop (a wait for one
     // would also drain the ring).
     wait_loads_upto<0>();
-#pragma unroll
-    for (int p = 0; p < C::NS - 1; ++p)
-        if (e0 + p < e1) load_block(col_idx[e0 + p], p);
     const float c2 = a.scale_log2;
-    int st = 0;  // ring stage of block e
+    // two-stage ring; the next block's index is read one step ahead (a scalar
+    // load, off the vector-memory counter the ring waits on)
+    int kb_next = e0 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e0]) : 0;
+    if (e0 < e1) load_block(kb_next, 0);
     for (int e = e0; e < e1; ++e) {
-        const int kb = col_idx[e];
+        const int kb = kb_next;
+        const int st = (e - e0) & 1;  // ring stage of block e
+        kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
-        const bool masked = !block_full32(a.pattern, mp.part, a.l, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
-        pipeline_wait<C::NS, C::NI>(e1 - 1 - e);
-        __syncthreads();  // this block is in LDS everywhere; the previous stage is free
-        if (e + C::NS - 1 < e1) load_block(col_idx[e + C::NS - 1], st == 0 ? C::NS - 1 : st - 1);
+        const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        wait_loads_upto<0>();
+        __syncthreads();  // block e is in LDS everywhere; the other stage is free
+        if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        st = st + 1 == C::NS ? 0 : st + 1;
 
         // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
         f32x4 s[C::QBW][C::KB];
@@ -124,44 +125,47 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             }
         }
 
-        // mask bits of this lane's rows, and the per-sub-block treatment
-        int cls[C::KB];
+        // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
+        // which 32-key chunks hold an attended item anywhere in the wave
         uint64_t bits[C::QBW];
+        bool live[C::QBW][C::KC];
 #pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) cls[kblk] = SUB_ALL;
+        for (int u = 0; u < C::QBW; ++u) {
+            bits[u] = ~0ull;
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = true;
+        }
         if (masked) {
-            const int j0_mod = j0 % a.l;
-            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0, a.l, a.c) : 0ull;
+            const int j0_mod = mod_l(a.dl, j0);
+            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
 #pragma unroll
-            for (int u = 0; u < C::QBW; ++u) bits[u] = row_mask(mp, rl[u], j0, j0_mod, sum) >> (4 * g);
+            for (int u = 0; u < C::QBW; ++u) {
+                bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk) {
-                uint32_t any = 0u, all = 0xFu;
-#pragma unroll
-                for (int u = 0; u < C::QBW; ++u) {
-                    const uint32_t nib = (uint32_t)(bits[u] >> (16 * kblk)) & 0xFu;
-                    any |= nib;
-                    all &= nib;
-                }
-                cls[kblk] = classify_sub(any, all);
+                for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = wave_any(chunk_bits(bits[u], kc, C::KB >= 2));
             }
         }
 
+        constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
         bf16x8 pf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
-            // running max in raw score units (the scale is positive), over
-            // the sub-blocks that hold attended keys
+            // running max in raw score units (the scale is positive) over the
+            // chunks that hold attended keys; masked items become -inf
             float mloc = -INFINITY;
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk) {
-                if (cls[kblk] == SUB_NONE) continue;
-                if (cls[kblk] == SUB_MIXED) {
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if (!live[u][kc]) continue;
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        s[u][kblk][t] = select_or_neg_inf(bit_lane_mask(bits[u], 16 * kblk + t), s[u][kblk][t]);
+                for (int hk = 0; hk < HK; ++hk) {
+                    const int kblk = 2 * kc + hk;
+                    if (masked) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            s[u][kblk][t] = select_or_neg_inf(bit_lane_mask(bits[u], 16 * kblk + t), s[u][kblk][t]);
+                    }
+                    mloc = fmaxf(mloc, fmaxf(fmaxf(s[u][kblk][0], s[u][kblk][1]), fmaxf(s[u][kblk][2], s[u][kblk][3])));
                 }
-                mloc = fmaxf(mloc, fmaxf(fmaxf(s[u][kblk][0], s[u][kblk][1]), fmaxf(s[u][kblk][2], s[u][kblk][3])));
             }
             mloc = max_over_g(mloc);
             const float m_new = fmaxf(m_run[u], mloc);
@@ -172,27 +176,28 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             const float neg = -m_ref * c2;
             float psum = 0.f;
 #pragma unroll
-            for (int kblk = 0; kblk < C::KB; ++kblk) {
-                if (cls[kblk] == SUB_NONE) {
-                    s[u][kblk] = zero4();
-                    continue;
-                }
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if (live[u][kc]) {
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const float pv = exp2_fast(fmaf(s[u][kblk][t], c2, neg));
-                    s[u][kblk][t] = pv;
-                    psum += pv;
+                    for (int hk = 0; hk < HK; ++hk) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const float pv = exp2_fast(fmaf(s[u][2 * kc + hk][t], c2, neg));
+                            s[u][2 * kc + hk][t] = pv;
+                            psum += pv;
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
                 }
+                if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
+                else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
             }
             // alpha rescales the state kept for the old maximum (0 when it was -inf)
             const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
             l_run[u] = fmaf(l_run[u], alpha, psum);
             m_run[u] = m_new;
-#pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) {
-                if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
-                else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
-            }
             // O is rescaled only in the blocks where some row's maximum grew
             // (a wave-uniform branch); everywhere else alpha is exactly 1.
             if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {

@@ -29,6 +29,7 @@ struct AttnArgs {
     float scale;           // softmax scale (> 0)
     float scale_log2;      // scale * log2(e)
     uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
+    DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;
     const uint8_t* kind;
@@ -41,9 +42,9 @@ struct AttnArgs {
 hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream);
 
-// Backward workspace: D and the base-2 LSE per row [b, h, n] (fp32), then a
-// 16-byte block for the column queue of the dK / dV kernel.
-size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t d, int dtype);
+// Backward workspace: D and the base-2 LSE per row [b, h, n] (fp32), then
+// the work queues and the column order of the dK / dV kernel.
+size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, int n_layouts);
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,

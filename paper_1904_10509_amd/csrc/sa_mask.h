@@ -19,12 +19,12 @@
 
 namespace sa {
 
-// Bits lo..hi of a 64-bit word (empty when hi < lo); lo, hi may lie outside [0, 63].
+// Bits lo..hi of a 64-bit word (empty when hi < lo); lo, hi may lie outside
+// [0, 63].  Written with selects only, so per-lane bounds cause no branch.
 __device__ inline uint64_t bit_range(int lo, int hi) {
-    lo = lo < 0 ? 0 : lo;
-    hi = hi > 63 ? 63 : hi;
-    if (hi < lo) return 0ull;
-    return (~0ull >> (63 - hi)) & (~0ull << lo);
+    const uint64_t upper = hi < 0 ? 0ull : (~0ull >> (63 - (hi > 63 ? 63 : hi)));
+    const uint64_t lower = lo > 63 ? 0ull : (~0ull << (lo < 0 ? 0 : lo));
+    return upper & lower;
 }
 
 // Bits at positions m, m + l, m + 2l, ... below 64, from `period_bits`
@@ -39,9 +39,9 @@ __device__ inline int mod_pos(int x, int l) {
     return r < 0 ? r + l : r;
 }
 
-// Summary columns (j mod l >= l - c) among j0 .. j0 + 63, as bits over j - j0.
-__device__ inline uint64_t summary_bits(int j0, int l, int c) {
-    const int r0 = j0 % l;
+// Summary columns (j mod l >= l - c) among j0 .. j0 + 63, as bits over j - j0;
+// r0 = j0 mod l.  Wave-uniform arguments: evaluated on the scalar unit.
+__device__ inline uint64_t summary_bits(int r0, int l, int c) {
     uint64_t bits = 0ull;
     for (int s = l - c - r0; s <= 63; s += l) bits |= bit_range(s, s + c - 1);
     return bits;
@@ -52,13 +52,25 @@ struct MaskParams {
     uint64_t period_bits;  // bits at multiples of l below 64
 };
 
+// Bits of the 32-row (or 32-column) chunk qc of a lane's mask after the
+// lane's shift by 4 (lane / 16): items 16 q + t, q = 2 qc, 2 qc + 1, t < 4.
+__device__ inline uint32_t chunk_bits(uint64_t bits, int qc, bool two_blocks) {
+    return (uint32_t)(bits >> (32 * qc)) & (two_blocks ? 0x000F000Fu : 0x0000000Fu);
+}
+
+// Does any lane of the wave hold an attended item in these bits?
+__device__ inline bool wave_any(uint32_t lane_bits) { return __builtin_amdgcn_ballot_w64(lane_bits != 0u) != 0ull; }
+
 // Row view (the lane owns query row i): constants of the lane.
 struct RowLane {
     int i;      // query row
     int i_mod;  // i mod l
     int blk0;   // first column of i's l-block
 };
-__device__ inline RowLane row_lane(int i, int l) { return RowLane{i, i % l, i - i % l}; }
+__device__ inline RowLane row_lane(int i, const DivL& dl) {
+    const int m = mod_l(dl, i);
+    return RowLane{i, m, i - m};
+}
 
 // Attended keys j0 + jj (bit jj) of the lane's row, j0 <= i.  j0_mod is
 // j0 mod l and sum = summary_bits(j0, l, c) (fixed pattern); both depend on
@@ -87,8 +99,9 @@ struct ColLane {
     int blk0;      // first row of j's l-block
     bool summary;  // fixed pattern: j mod l >= l - c
 };
-__device__ inline ColLane col_lane(int j, int l, int c) {
-    return ColLane{j, j % l, j - j % l, (j % l) >= l - c};
+__device__ inline ColLane col_lane(int j, const DivL& dl, int c) {
+    const int m = mod_l(dl, j);
+    return ColLane{j, m, j - m, m >= dl.l - c};
 }
 
 // Attended queries i0 + ii (bit ii) of the lane's column; i0_mod = i0 mod l.
@@ -122,19 +135,6 @@ __device__ inline float select_or_neg_inf(int32_t m, float x) {
 
 // x where the mask is all ones, +0 where it is zero.
 __device__ inline float select_or_zero(int32_t m, float x) { return __int_as_float(m & __float_as_int(x)); }
-
-// How a 16 x 16 sub-block of a masked block is treated, decided for the whole
-// wave: nothing attended (its probabilities are zero and no exponential is
-// evaluated), everything attended (no masking), or mixed (per element).
-enum { SUB_NONE = 0, SUB_MIXED = 1, SUB_ALL = 2 };
-
-// `nib_any` / `nib_all`: OR / AND over this lane's rows (or columns) of the
-// four mask bits it holds in the sub-block.
-__device__ inline int classify_sub(uint32_t nib_any, uint32_t nib_all) {
-    if (__builtin_amdgcn_ballot_w64(nib_any != 0u) == 0ull) return SUB_NONE;
-    if (__builtin_amdgcn_ballot_w64(nib_all != 0xFu) == 0ull) return SUB_ALL;
-    return SUB_MIXED;
-}
 
 inline uint64_t host_period_bits(int64_t l) {
     uint64_t bits = 0ull;

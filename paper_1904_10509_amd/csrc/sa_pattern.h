@@ -122,16 +122,42 @@ __host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int
     return one_block || all_summary;
 }
 
+// Division by the stride l for 0 <= x < 2^31 with one multiply-high: with
+// s = ceil(log2 l) and m = ceil(2^(31+s) / l) < 2^32, floor(x / l) equals
+// floor(x m / 2^(31+s)), because m l - 2^(31+s) < l makes the error term
+// x (m l - 2^(31+s)) / (l 2^(31+s)) smaller than 2^-s <= 1/l.
+struct DivL {
+    int32_t l;
+    int32_t s;   // ceil(log2 l); 0 for l = 1
+    uint32_t m;  // unused for l = 1
+};
+
+inline DivL make_divl(int32_t l) {
+    DivL d{l, 0, 0u};
+    while ((1ll << d.s) < l) ++d.s;
+    if (d.s > 0) d.m = (uint32_t)(((1ull << (31 + d.s)) + (uint64_t)l - 1) / (uint64_t)l);
+    return d;
+}
+
+__host__ __device__ inline uint32_t mulhi32(uint32_t a, uint32_t b) { return (uint32_t)(((uint64_t)a * b) >> 32); }
+
+__host__ __device__ inline int32_t div_l(const DivL& d, int32_t x) {
+    return d.s == 0 ? x : (int32_t)(mulhi32((uint32_t)x, d.m) >> (d.s - 1));
+}
+__host__ __device__ inline int32_t mod_l(const DivL& d, int32_t x) { return x - div_l(d, x) * d.l; }
+
 // block_full in 32-bit arithmetic (all coordinates below 2^31).
-__host__ __device__ inline bool block_full32(int pattern, int part, int32_t l, int32_t c, int32_t r0, int32_t r1,
+__host__ __device__ inline bool block_full32(int pattern, int part, const DivL& dl, int32_t c, int32_t r0, int32_t r1,
                                              int32_t c0, int32_t c1) {
+    const int32_t l = dl.l;
     if (r0 < c1) return false;
     if (pattern == STRIDED) {
         if (part == PART_A2) return l == 1;
         return r1 - c0 <= l || (part == PART_MERGED && l == 1);
     }
-    const bool one_block = c0 / l == r1 / l;
-    const bool all_summary = c == l || (c0 / l == c1 / l && c0 % l >= l - c);
+    const int32_t c0_blk = div_l(dl, c0);
+    const bool one_block = c0_blk == div_l(dl, r1);
+    const bool all_summary = c == l || (c0_blk == div_l(dl, c1) && c0 - c0_blk * l >= l - c);
     if (part == PART_A1) return one_block;
     if (part == PART_A2) return all_summary;
     return one_block || all_summary;

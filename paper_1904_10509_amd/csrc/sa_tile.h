@@ -113,29 +113,6 @@ __device__ inline void wait_loads_upto() {
     static_assert(N >= 0 && N < 64, "vmcnt field holds 6 bits");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
-__device__ inline void wait_tile_loads() { wait_loads_upto<0>(); }
-
-// Direct-to-LDS loads one wave issues for one tile (TileLoader::PER).
-template <int D, int BLK, int NW>
-constexpr int tile_loads_per_wave() {
-    static_assert((BLK * D / 512) % NW == 0, "every wave issues the same number of loads");
-    return BLK * D / 512 / NW;
-}
-
-// Ring of NS stages with NI loads per wave per stage: wait until the stage
-// being consumed has landed, while the stages of the next `later` blocks
-// (at most NS-2 of them) may still be in flight.
-template <int NS, int NI>
-__device__ inline void pipeline_wait(int later) {
-    static_assert(NS >= 2 && NS <= 4, "pipeline depth");
-    if constexpr (NS >= 4) {
-        if (later >= 2) { wait_loads_upto<2 * NI>(); return; }
-    }
-    if constexpr (NS >= 3) {
-        if (later >= 1) { wait_loads_upto<NI>(); return; }
-    }
-    wait_loads_upto<0>();
-}
 
 // Transposed operand over 32 rows of column col0 + (lane % 16): the first
 // four contraction items from rows row_lo .. row_lo+3, the last four from
