@@ -35,6 +35,7 @@
 // fp32 path: the same quantities on the VALU, one thread per row for dq and
 // one thread per column for dk / dv.
 #include <atomic>
+#include <type_traits>
 
 #include "sa_internal.h"
 #include "sa_mask.h"
@@ -146,7 +147,7 @@ struct DqCfg {
 };
 
 template <int D, int BLK>
-__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
+__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                    const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
@@ -205,9 +206,12 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     // two-stage ring; the next block's index is read one step ahead
     int kb_next = e0 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e0]) : 0;
     if (e0 < e1) load_block(kb_next, 0);
-    for (int e = e0; e < e1; ++e) {
+    TileReader<D> rd;
+    rd.init(g, r);
+    two_stage_loop(e1 - e0, [&](auto stage, int idx) {
+        constexpr int st = decltype(stage)::value;
+        const int e = e0 + idx;
         const int kb = kb_next;
-        const int st = (e - e0) & 1;
         kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
         const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
@@ -224,8 +228,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             bf16x8 kf[C::KS], vf[C::KS];
 #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
-                kf[ks] = ld_row_swz<D>(tK, kblk * 16 + r, ks * 32 + 8 * g);
-                vf[ks] = ld_row_swz<D>(tV, kblk * 16 + r, ks * 32 + 8 * g);
+                kf[ks] = rd.row(tK, kblk * 16, ks);
+                vf[ks] = rd.row(tV, kblk * 16, ks);
             }
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
@@ -239,14 +243,14 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             }
         }
         // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
-        // which 32-key chunks hold an attended item anywhere in the wave
+        // the treatment of each 32-key chunk
         uint64_t bits[C::QBW];
-        bool live[C::QBW][C::KC];
+        int cls[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
             bits[u] = ~0ull;
 #pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = true;
+            for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
         }
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
@@ -255,7 +259,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             for (int u = 0; u < C::QBW; ++u) {
                 bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
 #pragma unroll
-                for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = wave_any(chunk_bits(bits[u], kc, C::KB >= 2));
+                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
             }
         }
         // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
@@ -265,17 +269,23 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
                 constexpr int HK = C::KB >= 2 ? 2 : 1;
-                if (live[u][kc]) {
+                auto chunk = [&](auto part) {
 #pragma unroll
                     for (int hk = 0; hk < HK; ++hk) {
                         const int kblk = 2 * kc + hk;
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
                             float pv = exp2_fast(fmaf(s[u][kblk][t], c2, nl2[u]));
-                            if (masked) pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
+                            if constexpr (decltype(part)::value)
+                                pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
                             s[u][kblk][t] = pv * dp[u][kblk][t];
                         }
                     }
+                };
+                if (cls[u][kc] == CHUNK_ALL) {
+                    chunk(std::false_type{});
+                } else if (cls[u][kc] == CHUNK_PART) {
+                    chunk(std::true_type{});
                 } else {
 #pragma unroll
                     for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
@@ -290,13 +300,13 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 bf16x8 kt;
-                if constexpr (BLK >= 32) kt = ld_tr_swz<D>(tK, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
-                else kt = ld_tr_swz_half<D>(tK, 4 * g, db * 16, r);
+                if constexpr (BLK >= 32) kt = rd.tr(tK, kc * 32, kc * 32 + 16, db);
+                else kt = rd.tr_half(tK, 0, db);
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(kt, dsf[u][kc], dqacc[u][db]);
             }
         }
-    }
+    });
 
     // this lane holds dQ^T at d = 16 db + 4g + t for query row0 + 16u + r
 #pragma unroll
@@ -325,7 +335,7 @@ struct DkvCfg {
 };
 
 template <int D, int BLK>
-__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
+__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int32_t* __restrict__ row_idx,
                      const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
@@ -349,6 +359,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     const float c2 = a.scale_log2;
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
+    TileReader<D> rd;
+    rd.init(g, r);
     // Claims are made by thread 0, which walks the queues from its own XCD's
     // on; a claim is (queue << 56 | index), kNoWork once all queues are dry.
     constexpr unsigned long long kNoWork = ~0ull;
@@ -390,14 +402,17 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
-        const int key0 = kb * BLK + w * C::KW;  // first key of this wave
+        // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
+        // that the waves share the summary columns of the fixed pattern (which
+        // sit at the end of a block) and with them the softmax work.
+        auto key_of = [&](int kbw) { return kb * BLK + 16 * (C::NW * kbw + w) + r; };
 
-        // this lane's keys j = key0 + 16 kbw + r as B operands (d = 32 ks + 8g + t)
+        // this lane's keys j = key_of(kbw) as B operands (d = 32 ks + 8g + t)
         bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
         ColLane cl[C::KBW];
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
-            const int j = key0 + 16 * kbw + r;
+            const int j = key_of(kbw);
 #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
                 kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
@@ -435,9 +450,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         // scalar load, off the vector-memory counter the ring waits on)
         int qb_next = len > 0 ? __builtin_amdgcn_readfirstlane(row_idx[entry(0)]) : 0;
         if (len > 0) load_block(qb_next, 0);
-        for (int sidx = 0; sidx < len; ++sidx) {
+        two_stage_loop(len, [&](auto stage, int sidx) {
+            constexpr int st = decltype(stage)::value;
             const int qb = qb_next;
-            const int st = sidx & 1;
             qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
             const bool masked =
@@ -451,25 +466,22 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const float* tD = sDl[st];
 
             // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
-            f32x4 nl[C::QB], nd[C::QB];
-#pragma unroll
-            for (int qblk = 0; qblk < C::QB; ++qblk) {
-                nl[qblk] = *reinterpret_cast<const f32x4*>(&tL[qblk * 16 + 4 * g]);
-                nd[qblk] = *reinterpret_cast<const f32x4*>(&tD[qblk * 16 + 4 * g]);
-            }
-            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key0 + 16 kbw + r
+            auto row_stat = [&](const float* tile, int qblk) {
+                return *reinterpret_cast<const f32x4*>(&tile[qblk * 16 + 4 * g]);
+            };
+            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
             f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
 #pragma unroll
             for (int qblk = 0; qblk < C::QB; ++qblk) {
                 bf16x8 qa[C::KS], oa[C::KS];
 #pragma unroll
                 for (int ks = 0; ks < C::KS; ++ks) {
-                    qa[ks] = ld_row_swz<D>(tQ, qblk * 16 + r, ks * 32 + 8 * g);
-                    oa[ks] = ld_row_swz<D>(tO, qblk * 16 + r, ks * 32 + 8 * g);
+                    qa[ks] = rd.row(tQ, qblk * 16, ks);
+                    oa[ks] = rd.row(tO, qblk * 16, ks);
                 }
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    f32x4 sacc = zero4(), dpacc = nd[qblk];
+                    f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
 #pragma unroll
                     for (int ks = 0; ks < C::KS; ++ks) {
                         sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
@@ -482,12 +494,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             // mask bits of this lane's column (bit 16 qblk + t after the shift),
             // and which 32-query chunks hold an attended item anywhere in the wave
             uint64_t bits[C::KBW];
-            bool live[C::KBW][C::QC];
+            int cls[C::KBW][C::QC];
 #pragma unroll
             for (int kbw = 0; kbw < C::KBW; ++kbw) {
                 bits[kbw] = ~0ull;
 #pragma unroll
-                for (int qc = 0; qc < C::QC; ++qc) live[kbw][qc] = true;
+                for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = CHUNK_ALL;
             }
             if (masked) {
                 const int i0_mod = mod_l(a.dl, i0);
@@ -495,7 +507,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
                     bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
 #pragma unroll
-                    for (int qc = 0; qc < C::QC; ++qc) live[kbw][qc] = wave_any(chunk_bits(bits[kbw], qc, C::QB >= 2));
+                    for (int qc = 0; qc < C::QC; ++qc)
+                        cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
                 }
             }
 
@@ -508,18 +521,25 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 bf16x8 pb[C::KBW], sb[C::KBW];
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    if (live[kbw][qc]) {
+                    auto chunk = [&](auto part) {
 #pragma unroll
                         for (int hq = 0; hq < HQ; ++hq) {
                             const int qblk = 2 * qc + hq;
+                            const f32x4 nl = row_stat(tL, qblk);
 #pragma unroll
                             for (int t = 0; t < 4; ++t) {
-                                float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[qblk][t]));
-                                if (masked) pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
+                                float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[t]));
+                                if constexpr (decltype(part)::value)
+                                    pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
                                 p[kbw][qblk][t] = pv;
                                 ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
                             }
                         }
+                    };
+                    if (cls[kbw][qc] == CHUNK_ALL) {
+                        chunk(std::false_type{});
+                    } else if (cls[kbw][qc] == CHUNK_PART) {
+                        chunk(std::true_type{});
                     } else {
 #pragma unroll
                         for (int hq = 0; hq < HQ; ++hq) {
@@ -539,11 +559,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 for (int db = 0; db < C::DB; ++db) {
                     bf16x8 oT, qT;
                     if constexpr (BLK >= 32) {
-                        oT = ld_tr_swz<D>(tO, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
-                        qT = ld_tr_swz<D>(tQ, qc * 32 + 4 * g, qc * 32 + 16 + 4 * g, db * 16, r);
+                        oT = rd.tr(tO, qc * 32, qc * 32 + 16, db);
+                        qT = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
                     } else {
-                        oT = ld_tr_swz_half<D>(tO, 4 * g, db * 16, r);
-                        qT = ld_tr_swz_half<D>(tQ, 4 * g, db * 16, r);
+                        oT = rd.tr_half(tO, 0, db);
+                        qT = rd.tr_half(tQ, 0, db);
                     }
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
@@ -552,12 +572,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                 }
             }
-        }
+        });
 
-        // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key0 + 16 kbw + r
+        // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key_of(kbw)
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
-            const int j = key0 + 16 * kbw + r;
+            const int j = key_of(kbw);
             uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
 #pragma unroll

@@ -98,9 +98,12 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     // load, off the vector-memory counter the ring waits on)
     int kb_next = e0 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e0]) : 0;
     if (e0 < e1) load_block(kb_next, 0);
-    for (int e = e0; e < e1; ++e) {
+    TileReader<D> rd;
+    rd.init(g, r);
+    two_stage_loop(e1 - e0, [&](auto stage, int idx) {
+        constexpr int st = decltype(stage)::value;  // ring stage of block e
+        const int e = e0 + idx;
         const int kb = kb_next;
-        const int st = (e - e0) & 1;  // ring stage of block e
         kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
         const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
@@ -116,7 +119,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         for (int kblk = 0; kblk < C::KB; ++kblk) {
             bf16x8 kf[C::KS];
 #pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = ld_row_swz<D>(tK, kblk * 16 + r, ks * 32 + 8 * g);
+            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = rd.row(tK, kblk * 16, ks);
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
                 s[u][kblk] = zero4();
@@ -126,14 +129,14 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         }
 
         // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
-        // which 32-key chunks hold an attended item anywhere in the wave
+        // the treatment of each 32-key chunk
         uint64_t bits[C::QBW];
-        bool live[C::QBW][C::KC];
+        int cls[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
             bits[u] = ~0ull;
 #pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = true;
+            for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
         }
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
@@ -142,7 +145,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             for (int u = 0; u < C::QBW; ++u) {
                 bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
 #pragma unroll
-                for (int kc = 0; kc < C::KC; ++kc) live[u][kc] = wave_any(chunk_bits(bits[u], kc, C::KB >= 2));
+                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
             }
         }
 
@@ -155,16 +158,19 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             float mloc = -INFINITY;
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
-                if (!live[u][kc]) continue;
+                if (cls[u][kc] == CHUNK_NONE) continue;
+                if (cls[u][kc] == CHUNK_PART) {
 #pragma unroll
-                for (int hk = 0; hk < HK; ++hk) {
-                    const int kblk = 2 * kc + hk;
-                    if (masked) {
+                    for (int hk = 0; hk < HK; ++hk)
 #pragma unroll
                         for (int t = 0; t < 4; ++t)
-                            s[u][kblk][t] = select_or_neg_inf(bit_lane_mask(bits[u], 16 * kblk + t), s[u][kblk][t]);
-                    }
-                    mloc = fmaxf(mloc, fmaxf(fmaxf(s[u][kblk][0], s[u][kblk][1]), fmaxf(s[u][kblk][2], s[u][kblk][3])));
+                            s[u][2 * kc + hk][t] =
+                                select_or_neg_inf(bit_lane_mask(bits[u], 16 * (2 * kc + hk) + t), s[u][2 * kc + hk][t]);
+                }
+#pragma unroll
+                for (int hk = 0; hk < HK; ++hk) {
+                    const f32x4 x = s[u][2 * kc + hk];
+                    mloc = fmaxf(mloc, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
                 }
             }
             mloc = max_over_g(mloc);
@@ -177,7 +183,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             float psum = 0.f;
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
-                if (live[u][kc]) {
+                if (cls[u][kc] != CHUNK_NONE) {
 #pragma unroll
                     for (int hk = 0; hk < HK; ++hk) {
 #pragma unroll
@@ -212,13 +218,13 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
                 bf16x8 vf;
-                if constexpr (BLK >= 32) vf = ld_tr_swz<D>(tV, kc * 32 + 4 * g, kc * 32 + 16 + 4 * g, db * 16, r);
-                else vf = ld_tr_swz_half<D>(tV, 4 * g, db * 16, r);
+                if constexpr (BLK >= 32) vf = rd.tr(tV, kc * 32, kc * 32 + 16, db);
+                else vf = rd.tr_half(tV, 0, db);
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vf, pf[u][kc], oacc[u][db]);
             }
         }
-    }
+    });
 
 #pragma unroll
     for (int u = 0; u < C::QBW; ++u) {

@@ -58,8 +58,17 @@ __device__ inline uint32_t chunk_bits(uint64_t bits, int qc, bool two_blocks) {
     return (uint32_t)(bits >> (32 * qc)) & (two_blocks ? 0x000F000Fu : 0x0000000Fu);
 }
 
-// Does any lane of the wave hold an attended item in these bits?
-__device__ inline bool wave_any(uint32_t lane_bits) { return __builtin_amdgcn_ballot_w64(lane_bits != 0u) != 0ull; }
+// How a chunk (32 queries or keys of one 16-wide block of the other side)
+// is treated, decided for the whole wave: nothing attended (no exponentials,
+// zero probabilities), everything attended (no masking), or per item.
+enum { CHUNK_NONE = 0, CHUNK_PART = 1, CHUNK_ALL = 2 };
+
+__device__ inline int chunk_class(uint32_t lane_bits, bool two_blocks) {
+    const uint32_t full = two_blocks ? 0x000F000Fu : 0x0000000Fu;
+    if (__builtin_amdgcn_ballot_w64(lane_bits != 0u) == 0ull) return CHUNK_NONE;
+    if (__builtin_amdgcn_ballot_w64(lane_bits != full) == 0ull) return CHUNK_ALL;
+    return CHUNK_PART;
+}
 
 // Row view (the lane owns query row i): constants of the lane.
 struct RowLane {

@@ -11,7 +11,7 @@
 // result straight back in as an operand: the D results of two consecutive
 // 16-row blocks give, per lane, rows {4g..4g+3} and {16+4g..16+4g+3}, which is
 // exactly what one operand needs if contraction index 8g+t stands for local
-// row 4g+t (t < 4) or 16+4g+(t-4) (t >= 4).  chunk_row() is that map.
+// row 4g+t (t < 4) or 16+4g+(t-4) (t >= 4): pack_bf16x8 of the two results.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -22,12 +22,10 @@ namespace sa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ inline f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -38,23 +36,6 @@ __device__ inline f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 // 16 bytes (8 bf16) from global or LDS memory, 16-byte aligned.
 __device__ inline bf16x8 ld_bf16x8(const uint16_t* p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
-}
-
-// Two 8-byte pieces (4 bf16 each) joined into one operand.
-__device__ inline bf16x8 ld_bf16x4x2(const uint16_t* lo, const uint16_t* hi) {
-    u32x2 a = *reinterpret_cast<const u32x2*>(lo);
-    u32x2 b = *reinterpret_cast<const u32x2*>(hi);
-    u32x4 w = {a.x, a.y, b.x, b.y};
-    return __builtin_bit_cast(bf16x8, w);
-}
-
-__device__ inline bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u}); }
-
-// x with every bit cleared unless keep is all ones (a data mask, not a branch).
-__device__ inline bf16x8 mask_bf16x8(bf16x8 x, uint32_t keep) {
-    u32x4 w = __builtin_bit_cast(u32x4, x);
-    w &= u32x4{keep, keep, keep, keep};
-    return __builtin_bit_cast(bf16x8, w);
 }
 
 // Round-to-nearest-even fp32 -> bf16 of two D results, as one operand.
@@ -68,17 +49,6 @@ __device__ inline uint2 pack_bf16x4_bits(f32x4 v) {
     bf16x4 a = __builtin_convertvector(v, bf16x4);
     return __builtin_bit_cast(uint2, a);
 }
-
-__device__ inline uint16_t bf16_bits(float x) {
-    return __builtin_bit_cast(uint16_t, (__bf16)x);
-}
-
-__device__ inline float bf16_to_f32(uint16_t b) {
-    return __uint_as_float((uint32_t)b << 16);
-}
-
-// Local row of contraction index 8g + t in a 32-row chunk (see top comment).
-__device__ inline int chunk_row(int g, int t) { return t < 4 ? 4 * g + t : 16 + 4 * g + (t - 4); }
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -109,17 +79,6 @@ __device__ inline u32x2 ld_tr16(const uint16_t* lds_ptr) {
     s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
         (__attribute__((address_space(3))) s16x4*)(lds_ptr));
     return __builtin_bit_cast(u32x2, v);
-}
-
-// B/A operand over 32 rows (k = 8g + t) of column c0 + (lane % 16) of a
-// row-major tile with pitch `pitch`: rows row0 + kmap(g, t) where the first
-// four t come from rows base_lo + u and the last four from base_hi + u.
-__device__ inline bf16x8 ld_tr_operand(const uint16_t* tile, int pitch, int base_lo, int base_hi,
-                                       int col0, int r) {
-    const int off = (r >> 2) * pitch + col0 + 4 * (r & 3);
-    u32x2 lo = ld_tr16(tile + base_lo * pitch + off);
-    u32x2 hi = ld_tr16(tile + base_hi * pitch + off);
-    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
 }
 
 }  // namespace sa

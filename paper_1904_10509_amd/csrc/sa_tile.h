@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sa_mfma.h"
 
 namespace sa {
@@ -114,28 +116,54 @@ __device__ inline void wait_loads_upto() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Transposed operand over 32 rows of column col0 + (lane % 16): the first
-// four contraction items from rows row_lo .. row_lo+3, the last four from
-// row_hi .. row_hi+3 (see ld_tr16).
+// Per-lane byte offsets of the operand reads of a swizzled [., D] tile.
+// Row block bases that are multiples of 16 leave the chunk permutation of
+// a lane unchanged, so an address is one per-lane offset (chosen by the
+// d-chunk) plus a constant: the tile's LDS address, its ring stage and the
+// row block, all of which fit the immediate offset of the LDS read when the
+// caller indexes the tile with compile-time constants.
 template <int D>
-__device__ inline bf16x8 ld_tr_swz(const uint16_t* tile, int row_lo, int row_hi, int col0, int r) {
-    const int dr = r >> 2, dc = col0 + 4 * (r & 3);
-    u32x2 lo = ld_tr16(tile + Swz<D>::off(row_lo + dr, dc));
-    u32x2 hi = ld_tr16(tile + Swz<D>::off(row_hi + dr, dc));
-    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-}
+struct TileReader {
+    static constexpr int KS = D / 32;  // 32-wide d chunks (row reads)
+    static constexpr int DB = D / 16;  // 16-wide d blocks (transposed reads)
+    uint32_t row_off[KS];  // row r, elements 32 ks + 8 g .. +7
+    uint32_t tr_off[DB];   // row 4 g + r / 4, elements 16 db + 4 (r % 4) .. +3
 
-// Same for a 16-row tile: rows row_lo .. row_lo+3 only, upper half zero.
-template <int D>
-__device__ inline bf16x8 ld_tr_swz_half(const uint16_t* tile, int row_lo, int col0, int r) {
-    u32x2 lo = ld_tr16(tile + Swz<D>::off(row_lo + (r >> 2), col0 + 4 * (r & 3)));
-    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, 0u, 0u});
-}
+    __device__ void init(int g, int r) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) row_off[ks] = 2u * (uint32_t)Swz<D>::off(r, 32 * ks + 8 * g);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) tr_off[db] = 2u * (uint32_t)Swz<D>::off(4 * g + r / 4, 16 * db + 4 * (r & 3));
+    }
+    // A / B operand: row row0 + r (row0 a multiple of 16), elements 32 ks + 8 g .. +7
+    __device__ bf16x8 row(const uint16_t* tile, int row0, int ks) const {
+        return ld_bf16x8(reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(tile) + row_off[ks]) +
+                         row0 * D);
+    }
+    // Transposed operand over the 32 rows lo .. lo+15 and hi .. hi+15
+    // (multiples of 16) of column 16 db + r (see ld_tr16)
+    __device__ bf16x8 tr(const uint16_t* tile, int lo, int hi, int db) const {
+        const uint16_t* t = reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(tile) + tr_off[db]);
+        const u32x2 a = ld_tr16(t + lo * D);
+        const u32x2 b = ld_tr16(t + hi * D);
+        return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
+    }
+    // Same over rows lo .. lo+15 only; the upper half of the operand is zero
+    __device__ bf16x8 tr_half(const uint16_t* tile, int lo, int db) const {
+        const uint16_t* t = reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(tile) + tr_off[db]);
+        const u32x2 a = ld_tr16(t + lo * D);
+        return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, 0u, 0u});
+    }
+};
 
-// Row read: 8 consecutive elements of one row.
-template <int D>
-__device__ inline bf16x8 ld_row_swz(const uint16_t* tile, int row, int col) {
-    return ld_bf16x8(tile + Swz<D>::off(row, col));
+// Runs body(stage, i) for i = 0 .. count-1, stage = i mod 2 passed as a
+// compile-time constant, so that ring-stage addresses are constants.
+template <typename F>
+__device__ inline void two_stage_loop(int count, F&& body) {
+    for (int i = 0; i < count; i += 2) {
+        body(std::integral_constant<int, 0>{}, i);
+        if (i + 1 < count) body(std::integral_constant<int, 1>{}, i + 1);
+    }
 }
 
 }  // namespace sa
