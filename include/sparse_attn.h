@@ -33,7 +33,9 @@
  *   - Tensors Q, K, V, O, dO, dQ, dK, dV are [batch, heads, n, d_head] with d
  *     contiguous and the same element strides (batch, head, sequence) for all;
  *     the sequence stride must be >= d_head and every base address 16-byte
- *     aligned, every stride a multiple of 8 elements.  LSE is [batch, heads, n]
+ *     aligned, every stride a multiple of 8 elements.  For bf16, block rows
+ *     at the sequence stride must span less than 4 GiB (2 * block * stride
+ *     < 2^32 bytes), else SA_ERR_UNSUPPORTED.  LSE is [batch, heads, n]
  *     contiguous fp32 (natural logarithm).
  */
 #ifndef SPARSE_ATTN_H

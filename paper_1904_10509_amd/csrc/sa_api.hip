@@ -59,6 +59,8 @@ int check_tensor_args(const PatternArgs& p, int32_t batch, int32_t heads, int32_
         if (strides[t] < 0 || strides[t] % unit != 0) return SA_ERR_INVALID;
     if (strides[2] < d) return SA_ERR_INVALID;
     if ((int64_t)batch * heads > INT32_MAX / 2) return SA_ERR_INVALID;
+    // the bf16 kernels stage a B x d tile with 32-bit byte offsets from its first row
+    if (dtype == SA_BF16 && strides[2] * 2 * p.block >= ((int64_t)1 << 32)) return SA_ERR_UNSUPPORTED;
     return SA_OK;
 }
 

@@ -1,7 +1,7 @@
 // Block layout builder (Sec. 5.5: the product is computed over B x B blocks and
 // blocks above the diagonal are never visited).
 //
-// Four launches on the caller's stream:
+// Three launches on the caller's stream:
 //   1. count:  one wave per (layout g, index x) counts the present blocks of
 //              query-block row x and of key-block column x (O(1) test each);
 //   2. scan:   one workgroup turns the counts into absolute CSR offsets for

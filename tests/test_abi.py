@@ -99,6 +99,8 @@ def _fwd(L, **over):
     (dict(strides=(ctypes.c_int64 * 3)(8192, 8192, 36)), sa.SA_ERR_INVALID),  # stride not 16-byte
     (dict(strides=(ctypes.c_int64 * 3)(8192, 8192, 16)), sa.SA_ERR_INVALID),  # rows overlap
     (dict(strides=None), sa.SA_ERR_INVALID),
+    # bf16 tiles are staged with 32-bit byte offsets: block rows of the sequence stride must span < 4 GiB
+    (dict(strides=(ctypes.c_int64 * 3)(1 << 40, 1 << 40, 1 << 27)), sa.SA_ERR_UNSUPPORTED),
     (dict(scale=float("nan")), sa.SA_ERR_INVALID),
 ])
 def test_fwd_rejects_invalid(L, over, expect):
