@@ -255,12 +255,17 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
             const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
+            if (far_block(a.pattern, a.dl, qb * BLK, j0, BLK)) {
 #pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+            } else {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+            }
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u)
 #pragma unroll
                 for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
-            }
         }
         // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
         bf16x8 dsf[C::QBW][C::KC];
@@ -503,13 +508,20 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             }
             if (masked) {
                 const int i0_mod = mod_l(a.dl, i0);
+                if (far_block(a.pattern, a.dl, i0, kb * BLK, BLK)) {
 #pragma unroll
-                for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
+                        bits[kbw] = (col_mask_far(mp, cl[kbw], i0_mod) & kTileBits) >> (4 * g);
+                } else {
+#pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
+                        bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
+                }
+#pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw)
 #pragma unroll
                     for (int qc = 0; qc < C::QC; ++qc)
                         cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
-                }
             }
 
             // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then

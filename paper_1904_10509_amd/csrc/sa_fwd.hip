@@ -141,12 +141,17 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
             const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
+            if (far_block(a.pattern, a.dl, qb * BLK, j0, BLK)) {
 #pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+            } else {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+            }
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u)
 #pragma unroll
                 for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
-            }
         }
 
         constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk

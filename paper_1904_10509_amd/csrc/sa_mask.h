@@ -101,6 +101,32 @@ __device__ inline uint64_t row_mask(const MaskParams& p, const RowLane& x, int j
     return m & causal;
 }
 
+// Blocks away from the diagonal.  When every key of a block lies before the
+// A1 part of every row of the block (the band of l + 1 keys for strided, the
+// row's own l-block for fixed), only A2 can hold there: a period of l along
+// the row (strided) or the summary columns (fixed), and causality holds
+// everywhere.  Such "far" blocks are most of a long sequence's blocks and get
+// these short forms; the general forms above handle the rest.
+//   row view, block rows from i0, keys from j0 (B wide):
+//     strided: j0 + B - 1 < i0 - l;  fixed: j0 + B - 1 < l floor(i0 / l)
+//   column view, block keys up to j1 = j0 + B - 1, rows from i0:
+//     strided: i0 > j1 + l;          fixed: i0 > l floor(j1 / l) + l - 1
+__device__ inline bool far_block(int pattern, const DivL& dl, int i0, int j0, int B) {
+    const int j1 = j0 + B - 1;
+    if (pattern == STRIDED) return j1 < i0 - dl.l;
+    return j1 < i0 - mod_l(dl, i0);
+}
+
+__device__ inline uint64_t row_mask_far(const MaskParams& p, const RowLane& x, int j0_mod, uint64_t sum) {
+    if (p.part == PART_A1) return 0ull;
+    if (p.pattern == STRIDED) {
+        int m = x.i_mod - j0_mod;  // (i - j0) mod l
+        m += m < 0 ? p.l : 0;
+        return periodic_from(p.period_bits, m);
+    }
+    return sum;
+}
+
 // Column view (the lane owns key column j): constants of the lane.
 struct ColLane {
     int j;         // key column
@@ -129,6 +155,19 @@ __device__ inline uint64_t col_mask(const MaskParams& p, const ColLane& y, int i
     }
     const uint64_t m = p.part == PART_A1 ? a1 : (p.part == PART_A2 ? a2 : (a1 | a2));
     return m & causal;
+}
+
+// Far block in the column view (see far_block; the same condition, read for
+// the keys): only A2 holds, periodic in the row (strided) or the whole
+// column when the key is a summary column (fixed).
+__device__ inline uint64_t col_mask_far(const MaskParams& p, const ColLane& y, int i0_mod) {
+    if (p.part == PART_A1) return 0ull;
+    if (p.pattern == STRIDED) {
+        int m = y.j_mod - i0_mod;  // (j - i0) mod l
+        m += m < 0 ? p.l : 0;
+        return periodic_from(p.period_bits, m);
+    }
+    return y.summary ? ~0ull : 0ull;
 }
 
 // All ones when bit pos (0..63, a constant after unrolling) of bits is set, else 0.
