@@ -146,7 +146,7 @@ struct DqCfg {
     static constexpr int NS = 2;  // K / V ring stages
 };
 
-template <int D, int BLK>
+template <int D, int BLK, int PAT, int MODE>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -162,8 +162,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
+    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
@@ -214,7 +214,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         const int kb = kb_next;
         kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
-        const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        const bool masked = !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // block e is in LDS everywhere; the other stage is free
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
@@ -254,8 +254,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         }
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
-            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
-            if (far_block(a.pattern, a.dl, qb * BLK, j0, BLK)) {
+            const uint64_t sum = PAT == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
+            if (far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
             } else {
@@ -339,7 +339,7 @@ struct DkvCfg {
     static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
 };
 
-template <int D, int BLK>
+template <int D, int BLK, int PAT, int MODE>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int32_t* __restrict__ row_idx,
                      const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -402,9 +402,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int rank = __builtin_amdgcn_readfirstlane((int)(t / (uint64_t)nx));  // position in the length order
         const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
         const int h = bh % a.heads, b = bh / a.heads;
-        const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+        const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
         const int kb = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * a.nq + rank]);
-        const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+        const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits};
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
@@ -461,7 +461,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
             const bool masked =
-                !block_full32(a.pattern, mp.part, a.dl, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+                !block_full32(PAT, mp.part, a.dl, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
             wait_loads_upto<0>();
             __syncthreads();  // block sidx is in LDS everywhere; the other stage is free
             if (sidx + 1 < len) load_block(qb_next, st ^ 1);
@@ -508,7 +508,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             }
             if (masked) {
                 const int i0_mod = mod_l(a.dl, i0);
-                if (far_block(a.pattern, a.dl, i0, kb * BLK, BLK)) {
+                if (far_block(PAT, a.dl, i0, kb * BLK, BLK)) {
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw)
                         bits[kbw] = (col_mask_far(mp, cl[kbw], i0_mod) & kTileBits) >> (4 * g);
@@ -767,16 +767,21 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                        dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2,
                        ws.queue, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
-    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
-                       a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
-    const int64_t slots = resident_workgroups(bwd_dkdv_bf16_kernel<D, BLK>, DkvCfg<D, BLK>::NT);
-    const unsigned qgrid = (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK>), dim3(qgrid), dim3(DkvCfg<D, BLK>::NT), 0, stream,
-                       a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                       (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv, ws.queue, ws.order);
-    return hipGetLastError();
+    return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
+        constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
+        hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
+                           a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                           (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
+        const int64_t slots = resident_workgroups(bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>, DkvCfg<D, BLK>::NT);
+        const unsigned qgrid =
+            (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK>::NT), 0,
+                           stream, a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
+                           (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,
+                           ws.queue, ws.order);
+        return hipGetLastError();
+    });
 }
 
 template <int D>

@@ -41,7 +41,7 @@ struct FwdCfg {
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
 // over the XCDs) share a query block index across heads, so with heads a
 // multiple of 8 each head stays on one XCD and its keys stay in that L2.
-template <int D, int BLK>
+template <int D, int BLK, int PAT, int MODE>
 __global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
 fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                 const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -58,8 +58,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{a.pattern, part_of_head(a.mode, h), a.l, a.c, a.period_bits};
+    const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
+    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int row0 = qb * BLK + w * C::RW;  // first query row of this wave
 
@@ -106,7 +106,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         const int kb = kb_next;
         kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
         const int j0 = kb * BLK;
-        const bool masked = !block_full32(a.pattern, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        const bool masked = !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // block e is in LDS everywhere; the other stage is free
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
@@ -140,8 +140,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         }
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
-            const uint64_t sum = a.pattern == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
-            if (far_block(a.pattern, a.dl, qb * BLK, j0, BLK)) {
+            const uint64_t sum = PAT == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
+            if (far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
             } else {
@@ -300,9 +300,12 @@ template <int D, int BLK>
 hipError_t launch_bf16(const AttnArgs& a, const void* q, const void* k, const void* v, void* o,
                        float* lse, hipStream_t stream) {
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK>), grid, dim3(FwdCfg<D, BLK>::NT), 0, stream, a,
-                       a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
-    return hipGetLastError();
+    return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
+        hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK, decltype(pat)::value, decltype(mode)::value>), grid,
+                           dim3(FwdCfg<D, BLK>::NT), 0, stream, a, a.row_ptr, a.col_idx, (const uint16_t*)q,
+                           (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
+        return hipGetLastError();
+    });
 }
 
 template <int D>

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sa_pattern.h"
 
 namespace sa {
@@ -18,6 +20,33 @@ hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode
                          int64_t c, int n_layouts, int32_t* row_ptr, int32_t* col_idx,
                          uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
                          hipStream_t stream);
+
+// Calls f(pattern, mode) with both as compile-time constants
+// (std::integral_constant), so that kernels are specialised per pattern and
+// head mode.
+template <typename F>
+inline hipError_t with_pattern_mode(int pattern, int mode, F&& f) {
+    using S = std::integral_constant<int, STRIDED>;
+    using X = std::integral_constant<int, FIXED>;
+    using M0 = std::integral_constant<int, MODE_A1>;
+    using M1 = std::integral_constant<int, MODE_A2>;
+    using M2 = std::integral_constant<int, MODE_MERGED>;
+    using M3 = std::integral_constant<int, MODE_INTERLEAVED>;
+    if (pattern == STRIDED) {
+        switch (mode) {
+        case MODE_A1: return f(S{}, M0{});
+        case MODE_A2: return f(S{}, M1{});
+        case MODE_MERGED: return f(S{}, M2{});
+        default: return f(S{}, M3{});
+        }
+    }
+    switch (mode) {
+    case MODE_A1: return f(X{}, M0{});
+    case MODE_A2: return f(X{}, M1{});
+    case MODE_MERGED: return f(X{}, M2{});
+    default: return f(X{}, M3{});
+    }
+}
 
 // Everything a kernel needs to know about one call.
 struct AttnArgs {
