@@ -85,6 +85,7 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.scale = scale;
     a.scale_log2 = scale * sa::kLog2eHost;
     a.period_bits = sa::host_period_bits(p.l);
+    sa::host_summary_pattern(p.l, p.c, &a.sum_lo, &a.sum_hi);
     a.dl = sa::make_divl(p.l);
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;

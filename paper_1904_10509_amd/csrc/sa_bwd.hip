@@ -163,7 +163,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits};
+    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
@@ -254,7 +254,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         }
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
-            const uint64_t sum = PAT == FIXED ? summary_bits(j0_mod, a.l, a.c) : 0ull;
+            const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
             if (far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
@@ -404,7 +404,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int h = bh % a.heads, b = bh / a.heads;
         const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
         const int kb = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * a.nq + rank]);
-        const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits};
+        const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so

@@ -58,6 +58,7 @@ struct AttnArgs {
     float scale;           // softmax scale (> 0)
     float scale_log2;      // scale * log2(e)
     uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
+    uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64)
     DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;

@@ -39,18 +39,22 @@ __device__ inline int mod_pos(int x, int l) {
     return r < 0 ? r + l : r;
 }
 
-// Summary columns (j mod l >= l - c) among j0 .. j0 + 63, as bits over j - j0;
-// r0 = j0 mod l.  Wave-uniform arguments: evaluated on the scalar unit.
-__device__ inline uint64_t summary_bits(int r0, int l, int c) {
-    uint64_t bits = 0ull;
-    for (int s = l - c - r0; s <= 63; s += l) bits |= bit_range(s, s + c - 1);
-    return bits;
-}
-
 struct MaskParams {
     int pattern, part, l, c;
-    uint64_t period_bits;  // bits at multiples of l below 64
+    uint64_t period_bits;  // strided: bits at multiples of l below 64
+    uint64_t sum_lo, sum_hi;  // fixed, l <= 64: summary positions p mod l >= l - c, p < 128
 };
+
+// Summary columns (j mod l >= l - c) among j0 .. j0 + 63, as bits over j - j0;
+// r0 = j0 mod l.  For l <= 64 it is the precomputed 128-position pattern
+// shifted by r0; for l > 64 at most two runs of the pattern reach the 64
+// positions (the third would start at 3l - c - r0 > 2l - c >= l > 64).
+// Wave-uniform arguments: evaluated on the scalar unit.
+__device__ inline uint64_t summary_bits(const MaskParams& p, int r0) {
+    if (p.l <= 64) return r0 == 0 ? p.sum_lo : (p.sum_lo >> r0) | (p.sum_hi << (64 - r0));
+    const int s = p.l - p.c - r0;
+    return bit_range(s, s + p.c - 1) | bit_range(s + p.l, s + p.l + p.c - 1);
+}
 
 // Bits of the 32-row (or 32-column) chunk qc of a lane's mask after the
 // lane's shift by 4 (lane / 16): items 16 q + t, q = 2 qc, 2 qc + 1, t < 4.
@@ -65,9 +69,9 @@ enum { CHUNK_NONE = 0, CHUNK_PART = 1, CHUNK_ALL = 2 };
 
 __device__ inline int chunk_class(uint32_t lane_bits, bool two_blocks) {
     const uint32_t full = two_blocks ? 0x000F000Fu : 0x0000000Fu;
-    if (__builtin_amdgcn_ballot_w64(lane_bits != 0u) == 0ull) return CHUNK_NONE;
-    if (__builtin_amdgcn_ballot_w64(lane_bits != full) == 0ull) return CHUNK_ALL;
-    return CHUNK_PART;
+    const uint64_t any = __builtin_amdgcn_ballot_w64(lane_bits != 0u);
+    const uint64_t short_of_full = __builtin_amdgcn_ballot_w64(lane_bits != full);
+    return any == 0ull ? CHUNK_NONE : (short_of_full == 0ull ? CHUNK_ALL : CHUNK_PART);
 }
 
 // Row view (the lane owns query row i): constants of the lane.
@@ -188,6 +192,14 @@ inline uint64_t host_period_bits(int64_t l) {
     uint64_t bits = 0ull;
     for (int64_t k = 0; k < 64; k += l) bits |= 1ull << k;
     return bits;
+}
+
+// Summary positions p < 128 with p mod l >= l - c, as two words (fixed, l <= 64).
+inline void host_summary_pattern(int64_t l, int64_t c, uint64_t* lo, uint64_t* hi) {
+    *lo = *hi = 0ull;
+    if (l > 64 || c < 1) return;
+    for (int64_t p = 0; p < 128; ++p)
+        if (p % l >= l - c) (p < 64 ? *lo : *hi) |= 1ull << (p % 64);
 }
 
 }  // namespace sa

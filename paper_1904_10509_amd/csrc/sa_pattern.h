@@ -122,27 +122,26 @@ __host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int
     return one_block || all_summary;
 }
 
-// Division by the stride l for 0 <= x < 2^31 with one multiply-high: with
-// s = ceil(log2 l) and m = ceil(2^(31+s) / l) < 2^32, floor(x / l) equals
-// floor(x m / 2^(31+s)), because m l - 2^(31+s) < l makes the error term
-// x (m l - 2^(31+s)) / (l 2^(31+s)) smaller than 2^-s <= 1/l.
+// Division by the stride l for 0 <= x < 2^31 with one 32 x 32 -> 64-bit
+// multiply: with s = ceil(log2 l) and m = ceil(2^(31+s) / l) <= 2^31 (< 2^32),
+// floor(x / l) equals floor(x m / 2^(31+s)), because m l - 2^(31+s) < l makes
+// the error term x (m l - 2^(31+s)) / (l 2^(31+s)) smaller than 2^-s <= 1/l.
+// (l = 1 gives m = 2^31 and the identity.)
 struct DivL {
     int32_t l;
-    int32_t s;   // ceil(log2 l); 0 for l = 1
-    uint32_t m;  // unused for l = 1
+    int32_t shift;  // 31 + ceil(log2 l)
+    uint32_t m;
 };
 
 inline DivL make_divl(int32_t l) {
-    DivL d{l, 0, 0u};
-    while ((1ll << d.s) < l) ++d.s;
-    if (d.s > 0) d.m = (uint32_t)(((1ull << (31 + d.s)) + (uint64_t)l - 1) / (uint64_t)l);
+    int s = 0;
+    while ((1ll << s) < l) ++s;
+    DivL d{l, 31 + s, (uint32_t)(((1ull << (31 + s)) + (uint64_t)l - 1) / (uint64_t)l)};
     return d;
 }
 
-__host__ __device__ inline uint32_t mulhi32(uint32_t a, uint32_t b) { return (uint32_t)(((uint64_t)a * b) >> 32); }
-
 __host__ __device__ inline int32_t div_l(const DivL& d, int32_t x) {
-    return d.s == 0 ? x : (int32_t)(mulhi32((uint32_t)x, d.m) >> (d.s - 1));
+    return (int32_t)(((uint64_t)(uint32_t)x * d.m) >> d.shift);
 }
 __host__ __device__ inline int32_t mod_l(const DivL& d, int32_t x) { return x - div_l(d, x) * d.l; }
 

@@ -1,0 +1,18 @@
+"""Host-side arithmetic of the library, compiled and run on the CPU."""
+import os
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
+def test_stride_division_is_exact(tmp_path):
+    exe = tmp_path / "check_divl"
+    subprocess.run([HIPCC, "-O2", "-std=c++17", "-I", os.path.join(ROOT, "paper_1904_10509_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "host", "check_divl.cpp"), "-o", str(exe)], check=True,
+                   capture_output=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0 and out.stdout.startswith("ok"), out.stdout + out.stderr
