@@ -255,17 +255,30 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
             const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-            if (far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+            const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+            if (PAT == FIXED && far && mp.part != PART_A1) {
+                // every row attends exactly the summary keys: one mask for the wave
+                const uint64_t sb = sum & kTileBits;
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                for (int u = 0; u < C::QBW; ++u) {
+                    bits[u] = sb >> (4 * g);
+#pragma unroll
+                    for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
+                }
             } else {
+                if (far) {
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                }
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u)
+#pragma unroll
+                    for (int kc = 0; kc < C::KC; ++kc)
+                        cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
             }
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u)
-#pragma unroll
-                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
         }
         // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
         bf16x8 dsf[C::QBW][C::KC];
@@ -425,6 +438,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             }
             cl[kbw] = col_lane(j, a.dl, a.c);
         }
+        // summary keys of this key block (fixed pattern), bit = key offset in the block
+        const uint64_t key_summary = PAT == FIXED ? summary_bits(mp, mod_l(a.dl, kb * BLK)) & kTileBits : 0ull;
         f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw)
@@ -508,7 +523,18 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             }
             if (masked) {
                 const int i0_mod = mod_l(a.dl, i0);
-                if (far_block(PAT, a.dl, i0, kb * BLK, BLK)) {
+                const bool far = far_block(PAT, a.dl, i0, kb * BLK, BLK);
+                if (PAT == FIXED && far && mp.part != PART_A1) {
+                    // a summary key is attended by every row, any other key by none
+#pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                        bits[kbw] = cl[kbw].summary ? (kTileBits >> (4 * g)) : 0ull;
+                        const uint32_t keys = (uint32_t)(key_summary >> (16 * (C::NW * kbw + w))) & 0xFFFFu;
+                        const int k_cls = keys == 0u ? CHUNK_NONE : (keys == 0xFFFFu ? CHUNK_ALL : CHUNK_PART);
+#pragma unroll
+                        for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = k_cls;
+                    }
+                } else if (far) {
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw)
                         bits[kbw] = (col_mask_far(mp, cl[kbw], i0_mod) & kTileBits) >> (4 * g);
@@ -517,11 +543,13 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     for (int kbw = 0; kbw < C::KBW; ++kbw)
                         bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
                 }
+                if (!(PAT == FIXED && far && mp.part != PART_A1)) {
 #pragma unroll
-                for (int kbw = 0; kbw < C::KBW; ++kbw)
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
 #pragma unroll
-                    for (int qc = 0; qc < C::QC; ++qc)
-                        cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
+                        for (int qc = 0; qc < C::QC; ++qc)
+                            cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
+                }
             }
 
             // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then

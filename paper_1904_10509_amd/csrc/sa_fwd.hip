@@ -141,17 +141,30 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (masked) {
             const int j0_mod = mod_l(a.dl, j0);
             const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-            if (far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+            const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+            if (PAT == FIXED && far && mp.part != PART_A1) {
+                // every row attends exactly the summary keys: one mask for the wave
+                const uint64_t sb = sum & kTileBits;
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                for (int u = 0; u < C::QBW; ++u) {
+                    bits[u] = sb >> (4 * g);
+#pragma unroll
+                    for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
+                }
             } else {
+                if (far) {
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                }
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u)
+#pragma unroll
+                    for (int kc = 0; kc < C::KC; ++kc)
+                        cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
             }
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u)
-#pragma unroll
-                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
         }
 
         constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
@@ -179,8 +192,10 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                 }
             }
             mloc = max_over_g(mloc);
-            const float m_new = fmaxf(m_run[u], mloc);
-            const bool grew = m_new > m_run[u];
+            // The reference is the exact running maximum, so the largest
+            // probability of a row is exactly 1 in bf16 as in fp32.
+            const bool grew = mloc > m_run[u];
+            const float m_new = grew ? mloc : m_run[u];
             // rows with nothing attended so far keep m = -inf; 0 as reference
             // gives p = 0 without a branch around the MFMAs
             const float m_ref = m_new == -INFINITY ? 0.f : m_new;

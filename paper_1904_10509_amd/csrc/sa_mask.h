@@ -74,6 +74,14 @@ __device__ inline int chunk_class(uint32_t lane_bits, bool two_blocks) {
     return any == 0ull ? CHUNK_NONE : (short_of_full == 0ull ? CHUNK_ALL : CHUNK_PART);
 }
 
+// Chunk class when every lane holds the same mask word `w` (before the lane
+// shift): the 32 keys (or 16 when one block) of chunk kc.
+__device__ inline int uniform_chunk_class(uint64_t w, int kc, bool two_blocks) {
+    const uint32_t x = two_blocks ? (uint32_t)(w >> (32 * kc)) : (uint32_t)w & 0xFFFFu;
+    const uint32_t full = two_blocks ? 0xFFFFFFFFu : 0xFFFFu;
+    return x == 0u ? CHUNK_NONE : (x == full ? CHUNK_ALL : CHUNK_PART);
+}
+
 // Row view (the lane owns query row i): constants of the lane.
 struct RowLane {
     int i;      // query row
