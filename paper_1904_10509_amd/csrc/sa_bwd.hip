@@ -220,6 +220,16 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
+        // K^T operands of this block, read now: their LDS latency then hides
+        // behind the S and dP products and the softmax
+        bf16x8 ktr[C::KC][C::DB];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc)
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                if constexpr (BLK >= 32) ktr[kc][db] = rd.tr(tK, kc * 32, kc * 32 + 16, db);
+                else ktr[kc][db] = rd.tr_half(tK, 0, db);
+            }
 
         // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
         f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
@@ -312,16 +322,13 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                 else dsf[u][kc] = pack_bf16x8(s[u][0], zero4());
             }
         }
-        // dQ^T += K^T dS^T, K^T read transposed from the row-major tile
+        // dQ^T += K^T dS^T
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                bf16x8 kt;
-                if constexpr (BLK >= 32) kt = rd.tr(tK, kc * 32, kc * 32 + 16, db);
-                else kt = rd.tr_half(tK, 0, db);
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(kt, dsf[u][kc], dqacc[u][db]);
+                for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
             }
         }
     });

@@ -112,6 +112,16 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
+        // V^T operands of this block, read now: their LDS latency then hides
+        // behind the S products and the softmax
+        bf16x8 vt[C::KC][C::DB];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc)
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                if constexpr (BLK >= 32) vt[kc][db] = rd.tr(tV, kc * 32, kc * 32 + 16, db);
+                else vt[kc][db] = rd.tr_half(tV, 0, db);
+            }
 
         // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
         f32x4 s[C::QBW][C::KB];
@@ -232,16 +242,13 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             }
         }
 
-        // O^T += V^T P^T, V^T read transposed from the row-major tile
+        // O^T += V^T P^T
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                bf16x8 vf;
-                if constexpr (BLK >= 32) vf = rd.tr(tV, kc * 32, kc * 32 + 16, db);
-                else vf = rd.tr_half(tV, 0, db);
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vf, pf[u][kc], oacc[u][db]);
+                for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vt[kc][db], pf[u][kc], oacc[u][db]);
             }
         }
     });
