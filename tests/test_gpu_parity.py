@@ -13,7 +13,7 @@ from oracle import oracle as orc_mod
 from paper_1904_10509_amd import sparse_attn as sa
 from paper_1904_10509_amd.inputs import WORKLOADS, make_inputs, workload_inputs
 
-from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, run_gpu
+from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, run_gpu, to64
 
 pytestmark = pytest.mark.gpu
 
@@ -205,3 +205,60 @@ def test_autograd_wrapper():
     assert max_err(q.grad.float().cpu().numpy(), ref["dq"]) <= 2e-2
     assert max_err(k.grad.float().cpu().numpy(), ref["dk"]) <= 2e-2
     assert max_err(v.grad.float().cpu().numpy(), ref["dv"]) <= 2e-2
+
+
+# ---------------------------------------------------------------------------
+# n = 1,048,576 (strided l = 1024, B = 64, 4 merged heads of 64): the layout
+# bitwise, and forward / backward on sampled rows and columns; outputs are
+# gathered on the device so that nothing of the full size is copied back in
+# float64.
+# ---------------------------------------------------------------------------
+def test_layout_n1048576_bitwise():
+    w = WORKLOADS["strided_n1048576_l1024_merged"]
+    dev = device()
+    lay = sa.build_layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode, device=dev)
+    got = layout_to_cpu(lay)
+    ref = orc_mod.layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode)
+    assert list(lay.nnz) == list(ref["nnz"])
+    total = int(sum(ref["nnz"]))
+    for key in ("row_ptr", "col_ptr"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    for key in ("col_idx", "kind", "row_idx", "kind_t"):
+        np.testing.assert_array_equal(got[key][:total], ref[key], err_msg=key)
+
+
+def test_workload_n1048576_sampled():
+    w = WORKLOADS["strided_n1048576_l1024_merged"]
+    dev = device()
+    x = workload_inputs(w)
+    lay = sa.build_layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode, device=dev)
+    q, k, v, dout = (x[name].to(dev) for name in ("q", "k", "v", "dout"))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record()
+    o, lse = sa.forward(q, k, v, lay, w.scale)
+    ev[1].record()
+    dq, dk, dv = sa.backward(q, k, v, o, dout, lse, lay, w.scale)
+    ev[2].record()
+    torch.cuda.synchronize()
+    print(f"n=1048576: forward {ev[0].elapsed_time(ev[1]):.1f} ms, backward {ev[1].elapsed_time(ev[2]):.1f} ms "
+          f"(first call)", flush=True)
+    for t in (o, dq, dk, dv):
+        assert bool(torch.isfinite(t).all())
+    rng = np.random.default_rng(w.seed)
+    rows = sample_index(w, rng, 32)
+    cols = sample_index(w, rng, 16)
+
+    def gather(t, idx):
+        ix = torch.as_tensor(idx, device=dev)
+        return to64(t[ix[:, 0], ix[:, 1], ix[:, 2]])
+
+    xi = oracle_inputs(x)
+    kw = dict(pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
+    o_ref, lse_ref = orc_mod.forward_rows(*xi[:3], rows, **kw)
+    dq_ref = orc_mod.backward_rows(*xi, rows, **kw)
+    dk_ref, dv_ref = orc_mod.backward_cols(*xi, cols, **kw)
+    assert max_err(gather(o, rows), o_ref) <= 2e-2
+    assert max_err(gather(lse, rows), lse_ref) <= 1e-3
+    assert max_err(gather(dq, rows), dq_ref) <= 2e-2
+    assert max_err(gather(dk, cols), dk_ref) <= 2e-2
+    assert max_err(gather(dv, cols), dv_ref) <= 2e-2
