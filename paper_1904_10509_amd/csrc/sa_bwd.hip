@@ -346,28 +346,36 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 // ---------------------------------------------------------------------------
 // bf16, matrix cores: dK and dV, column-parallel
 // ---------------------------------------------------------------------------
-template <int D, int BLK>
+// Keys per wave.  In the fixed pattern a block away from the diagonal is
+// uniform over each 16-key group (all of its keys are summary keys or none
+// is), so 16-key waves skip whole softmax passes and, holding half the
+// registers, run three to a SIMD instead of two.  In the strided pattern such
+// a block holds one diagonal, every group is partial, and 32-key waves read
+// each Q / dO operand from LDS for twice the keys.
+template <int D, int BLK, int PAT>
 struct DkvCfg {
-    static constexpr int KW = BLK < 32 ? BLK : 32;  // keys per wave
-    static constexpr int KBW = KW / 16;             // 16-key blocks per wave
-    static constexpr int NW = BLK / KW;             // waves
+    static constexpr int KW = BLK < 32 || PAT == FIXED ? 16 : 32;  // keys per wave
+    static constexpr int KBW = KW / 16;                            // 16-key blocks per wave
+    static constexpr int NW = BLK / KW;                            // waves
     static constexpr int NT = NW * 64;
-    static constexpr int KS = D / 32;               // 32-deep steps over d
-    static constexpr int QB = BLK / 16;             // 16-query blocks per tile
-    static constexpr int QC = (BLK + 31) / 32;      // 32-query chunks (contraction over queries)
+    static constexpr int KS = D / 32;           // 32-deep steps over d
+    static constexpr int QB = BLK / 16;         // 16-query blocks per tile
+    static constexpr int QC = (BLK + 31) / 32;  // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
+    static constexpr int WAVES_PER_EU = KW == 16 ? 3 : 2;
 };
 
 template <int D, int BLK, int PAT, int MODE>
-__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__((DkvCfg<D, BLK, PAT>::NT))
+    __attribute__((amdgpu_waves_per_eu(DkvCfg<D, BLK, PAT>::WAVES_PER_EU)))
 bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int32_t* __restrict__ row_idx,
                      const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                      const float* __restrict__ nlse2, const float* __restrict__ ndelta,
                      uint16_t* __restrict__ dk, uint16_t* __restrict__ dv,
                      unsigned long long* __restrict__ queue, const int32_t* __restrict__ order) {
-    using C = DkvCfg<D, BLK>;
+    using C = DkvCfg<D, BLK, PAT>;
     __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
@@ -754,11 +762,13 @@ BwdWorkspace bwd_workspace(void* ws, int64_t rows) {
     return w;
 }
 
-// Workgroups of `kernel` the current device holds at once (0 if unknown),
-// cached per device.
-template <typename K>
-int64_t resident_workgroups(K kernel, int threads) {
+// Workgroups of `Kernel` the current device holds at once (0 if unknown),
+// cached per kernel and device (every instantiation of this template has its
+// own cache: kernels differ in registers and LDS, hence in occupancy).
+template <auto Kernel>
+int64_t resident_workgroups(int threads) {
     static std::atomic<int64_t> cache[64];
+    const auto kernel = Kernel;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
     if (dev < 64) {
@@ -808,10 +818,10 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
                            a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
                            (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
-        const int64_t slots = resident_workgroups(bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>, DkvCfg<D, BLK>::NT);
+        const int64_t slots = resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>>(DkvCfg<D, BLK, PAT>::NT);
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
-        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK>::NT), 0,
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK, PAT>::NT), 0,
                            stream, a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
                            (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,
                            ws.queue, ws.order);
