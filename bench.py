@@ -35,10 +35,12 @@ def credited_flops(w, nnz):
     return 14.0 * w.block * w.block * w.d_head * blocks, 4.0 * w.block * w.block * w.d_head * blocks
 
 
-def executed_mfma_flops(w, nnz):
-    """MFMA work the kernels issue per present block and (batch, head): forward
-    2 products (QK^T, PV), dQ kernel 3 (QK^T, dO V^T, dS K), dK/dV kernel 4
-    (QK^T, dO V^T, P^T dO, dS^T Q).  Every block is computed whole."""
+def mfma_flops_upper_bound(w, nnz):
+    """MFMA work the kernels issue per present block and (batch, head) when no
+    part of a block is skipped: forward 2 products (QK^T, PV), dQ kernel 3
+    (QK^T, dO V^T, dS K), dK/dV kernel 4 (QK^T, dO V^T, P^T dO, dS^T Q).  The
+    kernels skip the products of 32-wide chunks in which no pair of a wave's
+    rows and columns is attended, so the work issued is at most this."""
     heads_per_layout = [w.heads] if len(nnz) == 1 else [(w.heads + 1) // 2, w.heads // 2]
     blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout))
     return 18.0 * w.block * w.block * w.d_head * blocks
@@ -209,7 +211,7 @@ def main():
         per[w.name] = {
             "n": w.n, "nnz_blocks": r["lay"].nnz, "credited_flop": cred,
             "element_level_flop": None if pairs is None else 14.0 * w.d_head * pairs * w.batch * w.heads,
-            "executed_mfma_flop": executed_mfma_flops(w, r["lay"].nnz),
+            "mfma_flop_upper_bound": mfma_flops_upper_bound(w, r["lay"].nnz),
             "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
             "fwd_tflops": cred_fwd / (fwd_ms * 1e-3) / 1e12,
             "bwd_tflops": (cred - cred_fwd) / (bwd_ms * 1e-3) / 1e12,

@@ -220,38 +220,6 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // K^T operands of this block, read now: their LDS latency then hides
-        // behind the S and dP products and the softmax
-        bf16x8 ktr[C::KC][C::DB];
-#pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc)
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                if constexpr (BLK >= 32) ktr[kc][db] = rd.tr(tK, kc * 32, kc * 32 + 16, db);
-                else ktr[kc][db] = rd.tr_half(tK, 0, db);
-            }
-
-        // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
-        f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
-#pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
-            bf16x8 kf[C::KS], vf[C::KS];
-#pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) {
-                kf[ks] = rd.row(tK, kblk * 16, ks);
-                vf[ks] = rd.row(tV, kblk * 16, ks);
-            }
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                s[u][kblk] = zero4();
-                dp[u][kblk] = nd4[u];
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) {
-                    s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
-                    dp[u][kblk] = mfma_16x16x32(vf[ks], of[u][ks], dp[u][kblk]);
-                }
-            }
-        }
         // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
         // the treatment of each 32-key chunk
         uint64_t bits[C::QBW];
@@ -290,13 +258,64 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                         cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
             }
         }
+        // A 32-key chunk enters the products only where some row of the wave
+        // attends one of its keys; elsewhere dS is zero and the chunk's
+        // operands are neither read nor multiplied (wave-uniform branches)
+        constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
+        bool kc_live[C::KC];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc) {
+            kc_live[kc] = false;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
+        }
+        // K^T operands of this block, read now: their LDS latency then hides
+        // behind the S and dP products and the softmax
+        bf16x8 ktr[C::KC][C::DB];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc) {
+            if (!kc_live[kc]) continue;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                if constexpr (BLK >= 32) ktr[kc][db] = rd.tr(tK, kc * 32, kc * 32 + 16, db);
+                else ktr[kc][db] = rd.tr_half(tK, 0, db);
+            }
+        }
+
+        // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
+        f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
+#pragma unroll
+        for (int kblk = 0; kblk < C::KB; ++kblk) {
+            const int kc = kblk / HK;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) {
+                s[u][kblk] = zero4();
+                dp[u][kblk] = nd4[u];
+            }
+            if (!kc_live[kc]) continue;
+            bf16x8 kf[C::KS], vf[C::KS];
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) {
+                kf[ks] = rd.row(tK, kblk * 16, ks);
+                vf[ks] = rd.row(tV, kblk * 16, ks);
+            }
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) {
+                if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+                    dp[u][kblk] = mfma_16x16x32(vf[ks], of[u][ks], dp[u][kblk]);
+                }
+            }
+        }
+
         // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
         bf16x8 dsf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
-                constexpr int HK = C::KB >= 2 ? 2 : 1;
                 auto chunk = [&](auto part) {
 #pragma unroll
                     for (int hk = 0; hk < HK; ++hk) {
@@ -326,9 +345,10 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
 #pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
+            for (int u = 0; u < C::QBW; ++u) {
+                if (cls[u][kc] == CHUNK_NONE) continue;
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
+                for (int db = 0; db < C::DB; ++db) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
             }
         }
     });
@@ -504,28 +524,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             auto row_stat = [&](const float* tile, int qblk) {
                 return *reinterpret_cast<const f32x4*>(&tile[qblk * 16 + 4 * g]);
             };
-            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
-            f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
-#pragma unroll
-            for (int qblk = 0; qblk < C::QB; ++qblk) {
-                bf16x8 qa[C::KS], oa[C::KS];
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) {
-                    qa[ks] = rd.row(tQ, qblk * 16, ks);
-                    oa[ks] = rd.row(tO, qblk * 16, ks);
-                }
-#pragma unroll
-                for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
-#pragma unroll
-                    for (int ks = 0; ks < C::KS; ++ks) {
-                        sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
-                        dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
-                    }
-                    p[kbw][qblk] = sacc;
-                    ds[kbw][qblk] = dpacc;
-                }
-            }
             // mask bits of this lane's column (bit 16 qblk + t after the shift),
             // and which 32-query chunks hold an attended item anywhere in the wave
             uint64_t bits[C::KBW];
@@ -567,12 +565,50 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 }
             }
 
+            // A 32-query chunk enters the products only where some key of the
+            // wave is attended by one of its queries; elsewhere P and dS are zero
+            // and its operands are neither read nor multiplied (wave-uniform
+            // branches)
+            constexpr int HQ = C::QB >= 2 ? 2 : 1;  // 16-query blocks per 32-query chunk
+            bool qc_live[C::QC];
+#pragma unroll
+            for (int qc = 0; qc < C::QC; ++qc) {
+                qc_live[qc] = false;
+#pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw) qc_live[qc] = qc_live[qc] || cls[kbw][qc] != CHUNK_NONE;
+            }
+            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
+            f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
+#pragma unroll
+            for (int qblk = 0; qblk < C::QB; ++qblk) {
+                const int qc = qblk / HQ;
+                if (!qc_live[qc]) continue;
+                bf16x8 qa[C::KS], oa[C::KS];
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    qa[ks] = rd.row(tQ, qblk * 16, ks);
+                    oa[ks] = rd.row(tO, qblk * 16, ks);
+                }
+#pragma unroll
+                for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                    if (cls[kbw][qc] == CHUNK_NONE) continue;
+                    f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
+#pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) {
+                        sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
+                        dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
+                    }
+                    p[kbw][qblk] = sacc;
+                    ds[kbw][qblk] = dpacc;
+                }
+            }
+
             // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then
             // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's
             // queries; dO^T and Q^T are read transposed from the row-major tiles
 #pragma unroll
             for (int qc = 0; qc < C::QC; ++qc) {
-                constexpr int HQ = C::QB >= 2 ? 2 : 1;
+                if (!qc_live[qc]) continue;
                 bf16x8 pb[C::KBW], sb[C::KBW];
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
@@ -590,25 +626,16 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                                 ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
                             }
                         }
-                    };
-                    if (cls[kbw][qc] == CHUNK_ALL) {
-                        chunk(std::false_type{});
-                    } else if (cls[kbw][qc] == CHUNK_PART) {
-                        chunk(std::true_type{});
-                    } else {
-#pragma unroll
-                        for (int hq = 0; hq < HQ; ++hq) {
-                            p[kbw][2 * qc + hq] = zero4();
-                            ds[kbw][2 * qc + hq] = zero4();
+                        if constexpr (BLK >= 32) {
+                            pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
+                            sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                        } else {
+                            pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
+                            sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
                         }
-                    }
-                    if constexpr (BLK >= 32) {
-                        pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
-                        sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
-                    } else {
-                        pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
-                        sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
-                    }
+                    };
+                    if (cls[kbw][qc] == CHUNK_ALL) chunk(std::false_type{});
+                    else if (cls[kbw][qc] == CHUNK_PART) chunk(std::true_type{});
                 }
 #pragma unroll
                 for (int db = 0; db < C::DB; ++db) {
@@ -622,6 +649,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                        if (cls[kbw][qc] == CHUNK_NONE) continue;
                         dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
                         dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
                     }

@@ -112,32 +112,6 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (e + 1 < e1) load_block(kb_next, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // V^T operands of this block, read now: their LDS latency then hides
-        // behind the S products and the softmax
-        bf16x8 vt[C::KC][C::DB];
-#pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc)
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                if constexpr (BLK >= 32) vt[kc][db] = rd.tr(tV, kc * 32, kc * 32 + 16, db);
-                else vt[kc][db] = rd.tr_half(tV, 0, db);
-            }
-
-        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
-        f32x4 s[C::QBW][C::KB];
-#pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
-            bf16x8 kf[C::KS];
-#pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = rd.row(tK, kblk * 16, ks);
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                s[u][kblk] = zero4();
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
-            }
-        }
-
         // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
         // the treatment of each 32-key chunk
         uint64_t bits[C::QBW];
@@ -177,7 +151,49 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             }
         }
 
+        // A 32-key chunk enters the products only where some row of the wave
+        // attends one of its keys; elsewhere its probabilities are zero and
+        // its operands are neither read nor multiplied (wave-uniform branches)
         constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
+        bool kc_live[C::KC];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc) {
+            kc_live[kc] = false;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
+        }
+        // V^T operands of this block, read now: their LDS latency then hides
+        // behind the S products and the softmax
+        bf16x8 vt[C::KC][C::DB];
+#pragma unroll
+        for (int kc = 0; kc < C::KC; ++kc) {
+            if (!kc_live[kc]) continue;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                if constexpr (BLK >= 32) vt[kc][db] = rd.tr(tV, kc * 32, kc * 32 + 16, db);
+                else vt[kc][db] = rd.tr_half(tV, 0, db);
+            }
+        }
+
+        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
+        f32x4 s[C::QBW][C::KB];
+#pragma unroll
+        for (int kblk = 0; kblk < C::KB; ++kblk) {
+            const int kc = kblk / HK;
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) s[u][kblk] = zero4();
+            if (!kc_live[kc]) continue;
+            bf16x8 kf[C::KS];
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = rd.row(tK, kblk * 16, ks);
+#pragma unroll
+            for (int u = 0; u < C::QBW; ++u) {
+                if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+            }
+        }
+
         bf16x8 pf[C::QBW][C::KC];
 #pragma unroll
         for (int u = 0; u < C::QBW; ++u) {
@@ -246,9 +262,10 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
 #pragma unroll
         for (int kc = 0; kc < C::KC; ++kc) {
 #pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
+            for (int u = 0; u < C::QBW; ++u) {
+                if (cls[u][kc] == CHUNK_NONE) continue;
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) oacc[u][db] = mfma_16x16x32(vt[kc][db], pf[u][kc], oacc[u][db]);
+                for (int db = 0; db < C::DB; ++db) oacc[u][db] = mfma_16x16x32(vt[kc][db], pf[u][kc], oacc[u][db]);
             }
         }
     });
