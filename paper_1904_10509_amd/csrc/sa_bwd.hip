@@ -197,27 +197,39 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
-    auto load_block = [&](int kb, int stage) {
-        const int64_t kbase = base + (int64_t)kb * BLK * a.ss;
-        ld.issue(k + kbase, sK_base + stage * kTileBytes);
-        ld.issue(v + kbase, sV_base + stage * kTileBytes);
+    // A step stages one block, or two upper halves (see RowStepper) as one tile
+    constexpr bool kPairs = PAT == FIXED && BLK == 64;
+    auto load_step = [&](RowStep s, int stage) {
+        const uint32_t kdst = sK_base + stage * kTileBytes, vdst = sV_base + stage * kTileBytes;
+        if (!kPairs || s.b < 0) {
+            const int64_t kbase = base + (int64_t)s.a * BLK * a.ss;
+            ld.issue(k + kbase, kdst);
+            ld.issue(v + kbase, vdst);
+        } else if constexpr (kPairs) {
+            const int64_t lo = base + ((int64_t)s.a * BLK + BLK / 2) * a.ss, hi = base + (int64_t)s.b * BLK * a.ss;
+            ld.issue_halves(k + lo, k + hi, kdst);
+            ld.issue_halves(v + lo, v + hi, vdst);
+        }
     };
     wait_loads_upto<0>();  // register loads done before the ring starts
-    // two-stage ring; the next block's index is read one step ahead
-    int kb_next = e0 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e0]) : 0;
-    if (e0 < e1) load_block(kb_next, 0);
+    // two-stage ring; the next step's blocks are read one step ahead
+    RowStepper<kPairs> steps{col_idx, e0, e1};
+    RowStep cur = steps.next(mp, a.dl, qb * BLK);
+    if (cur.a >= 0) load_step(cur, 0);
     TileReader<D> rd;
     rd.init(g, r);
-    two_stage_loop(e1 - e0, [&](auto stage, int idx) {
+    two_stage_while([&](auto stage) {
         constexpr int st = decltype(stage)::value;
-        const int e = e0 + idx;
-        const int kb = kb_next;
-        kb_next = e + 1 < e1 ? __builtin_amdgcn_readfirstlane(col_idx[e + 1]) : 0;
+        if (cur.a < 0) return false;
+        const RowStep nxt = steps.next(mp, a.dl, qb * BLK);
+        const int kb = cur.a;
         const int j0 = kb * BLK;
-        const bool masked = !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+        // a pair of upper halves is attended everywhere
+        const bool masked =
+            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
-        __syncthreads();  // block e is in LDS everywhere; the other stage is free
-        if (e + 1 < e1) load_block(kb_next, st ^ 1);
+        __syncthreads();  // this step is in LDS everywhere; the other stage is free
+        if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
         // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
@@ -351,6 +363,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                 for (int db = 0; db < C::DB; ++db) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
             }
         }
+        cur = nxt;
+        return true;
     });
 
     // this lane holds dQ^T at d = 16 db + 4g + t for query row0 + 16u + r

@@ -99,6 +99,20 @@ struct TileLoader {
 #pragma unroll
         for (int kk = 0; kk < PER; ++kk) dma_b128(s, off[kk], base + 1024 * (w + NW * kk));
     }
+    // One tile made of two half tiles: rows 0 .. BLK/2-1 from src_lo and rows
+    // BLK/2 .. BLK-1 from src_hi, each pointer being where tile row 0 would
+    // sit (so tile row R reads row R past its pointer).  A 1 KiB window never
+    // straddles the two halves.
+    __device__ void issue_halves(const uint16_t* src_lo, const uint16_t* src_hi, uint32_t base) const {
+        static_assert((NB / 2) * 512 == (BLK / 2) * D, "windows split at half the tile");
+        const void* lo = uniform_ptr(src_lo);
+        const void* hi = uniform_ptr(src_hi);
+#pragma unroll
+        for (int kk = 0; kk < PER; ++kk) {
+            const int win = w + NW * kk;
+            dma_b128(win < NB / 2 ? lo : hi, off[kk], base + 1024 * win);
+        }
+    }
 };
 
 // 64 consecutive fp32 values starting at src (one per lane, lanes past
@@ -163,6 +177,14 @@ __device__ inline void two_stage_loop(int count, F&& body) {
     for (int i = 0; i < count; i += 2) {
         body(std::integral_constant<int, 0>{}, i);
         if (i + 1 < count) body(std::integral_constant<int, 1>{}, i + 1);
+    }
+}
+
+// The same for a loop whose trip count is found on the way: body(stage)
+// returns false when there is no further step.
+template <typename F>
+__device__ inline void two_stage_while(F&& body) {
+    while (body(std::integral_constant<int, 0>{}) && body(std::integral_constant<int, 1>{})) {
     }
 }
 

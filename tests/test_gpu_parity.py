@@ -71,6 +71,10 @@ SMALL_CASES = [
     (F, A2, 256, 16, 64, 1, 32, torch.bfloat16, 1, 1),
     (F, MG, 256, 64, 64, 64, 64, torch.bfloat16, 1, 1),
     (F, IL, 512, 16, 48, 12, 64, torch.bfloat16, 1, 2),
+    # fixed, B = 64, c = 32: rows whose far blocks pair up (even and odd counts)
+    (F, A2, 1024, 64, 128, 32, 64, torch.bfloat16, 1, 2),
+    (F, MG, 512, 64, 64, 32, 64, torch.bfloat16, 1, 1),
+    (F, IL, 1024, 64, 128, 32, 128, torch.bfloat16, 2, 2),
     # more (batch, head) pairs than the dK / dV kernel has queues, not a multiple of them
     (S, MG, 256, 32, 32, 0, 32, torch.bfloat16, 3, 5),
     (F, IL, 256, 16, 64, 16, 32, torch.bfloat16, 3, 3),
