@@ -71,19 +71,46 @@ __device__ inline int64_t queue_heads(int64_t bh_count, int x) {
     return bh_count > x ? (bh_count - 1 - x) / kQueues + 1 : 0;
 }
 
-// Workgroup 0 of the pre kernel: empty queues, and per layout the key blocks
-// ordered by length class (order inside a class is arbitrary; it only
-// affects scheduling).
+// Items of the dK / dV schedule: key block kb whole (half 0), or one 32-key
+// half of a 64-wide block (half 1: keys 0..31, half 2: keys 32..63); -1 is
+// an empty slot.
+constexpr int kItemShift = 29;
+__device__ inline int32_t item_code(int kb, int half) { return kb | (half << kItemShift); }
+
+// In the fixed pattern with B = 64, a key block whose upper 32 keys are
+// summary keys and whose lower 32 are not is split into its two halves: the
+// lower keys meet only the blocks of their own l-block, the upper keys every
+// block of the column.  Each half is then shared by all four waves (its two
+// 16-key groups times the two 32-query halves of a block), where the whole
+// block would leave the two waves of the lower keys idle on every block away
+// from the diagonal.
+__device__ inline bool split_column(const AttnArgs& a, int g, int kb) {
+    if (a.pattern != FIXED || a.block != 64) return false;
+    const MaskParams mp{a.pattern, part_of_layout(a.mode, g), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
+    return mp.part != PART_A1 && summary_bits(mp, mod_l(a.dl, 64 * kb)) == 0xFFFFFFFF00000000ull;
+}
+
+// Workgroup 0 of the pre kernel: empty queues; per layout the items (2 nq
+// slots) ordered by length class, empty slots last (order inside a class is
+// arbitrary; it only affects scheduling); and in queue[kQueues] the largest
+// item count of a layout.
 __device__ void build_schedule(const AttnArgs& a, unsigned long long* queue, int32_t* order) {
     __shared__ int cls_pos[kLengthClasses];
+    __shared__ int items;
     const int tid = threadIdx.x;
     if (tid < kQueues) queue[tid] = 0ull;
     const int n_layouts = a.mode == MODE_INTERLEAVED ? 2 : 1;
+    const int lower_cls = length_class(2);  // a lower half meets at most a few blocks
+    int max_items = 0;
     for (int g = 0; g < n_layouts; ++g) {
         const int32_t* cp = a.col_ptr + (int64_t)g * (a.nq + 1);
+        int32_t* ord = order + (int64_t)g * 2 * a.nq;
         for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
         __syncthreads();
-        for (int kb = tid; kb < a.nq; kb += blockDim.x) atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+        for (int kb = tid; kb < a.nq; kb += blockDim.x) {
+            atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+            if (split_column(a, g, kb)) atomicAdd(&cls_pos[lower_cls], 1);
+        }
         __syncthreads();
         if (tid == 0) {
             int run = 0;
@@ -92,12 +119,19 @@ __device__ void build_schedule(const AttnArgs& a, unsigned long long* queue, int
                 cls_pos[i] = run;
                 run += c;
             }
+            items = run;
         }
         __syncthreads();
-        for (int kb = tid; kb < a.nq; kb += blockDim.x)
-            order[(int64_t)g * a.nq + atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = kb;
+        for (int kb = tid; kb < a.nq; kb += blockDim.x) {
+            const bool split = split_column(a, g, kb);
+            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, split ? 2 : 0);
+            if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 1);
+        }
+        for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
+        max_items = max_items > items ? max_items : items;
         __syncthreads();
     }
+    if (tid == 0) queue[kQueues] = (unsigned long long)max_items;
 }
 
 template <int D, typename T>
@@ -410,6 +444,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                      uint16_t* __restrict__ dk, uint16_t* __restrict__ dv,
                      unsigned long long* __restrict__ queue, const int32_t* __restrict__ order) {
     using C = DkvCfg<D, BLK, PAT>;
+    constexpr bool kHalves = PAT == FIXED && BLK == 64;  // items may be 32-key halves
+    static_assert(!kHalves || (C::NW == 4 && C::KBW == 1 && C::QC == 2), "half items: 4 waves of 16 keys");
     __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
@@ -432,7 +468,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     // on; a claim is (queue << 56 | index), kNoWork once all queues are dry.
     constexpr unsigned long long kNoWork = ~0ull;
     int qx = 0, q_left = kQueues;
+    uint64_t per_layout = 0;  // item slots taken per (batch, head)
     if (tid == 0) {
+        per_layout = queue[kQueues];
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
         qx = (int)(xcc % kQueues);
@@ -440,7 +478,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     auto claim = [&]() -> unsigned long long {
         while (q_left > 0) {
             const uint64_t t = atomicAdd(queue + qx, 1ull);
-            if (t < (uint64_t)a.nq * (uint64_t)queue_heads(bh_count, qx)) return ((uint64_t)qx << 56) | t;
+            if (t < per_layout * (uint64_t)queue_heads(bh_count, qx)) return ((uint64_t)qx << 56) | t;
             qx = qx + 1 == kQueues ? 0 : qx + 1;
             --q_left;
         }
@@ -465,14 +503,24 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
         const int h = bh % a.heads, b = bh / a.heads;
         const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
-        const int kb = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * a.nq + rank]);
+        const int32_t code = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
+        if (code < 0) {  // an empty slot (a layout with fewer items than the other)
+            if (tid == 0) sItem[(it + 1) & 1] = next;
+            __syncthreads();
+            continue;
+        }
+        const int kb = code & ((1 << kItemShift) - 1);
+        const int half = kHalves ? code >> kItemShift : 0;
         const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
         // that the waves share the summary columns of the fixed pattern (which
-        // sit at the end of a block) and with them the softmax work.
-        auto key_of = [&](int kbw) { return kb * BLK + 16 * (C::NW * kbw + w) + r; };
+        // sit at the end of a block) and with them the softmax work.  In a
+        // half item the wave takes key group w mod 2 of the half, for the
+        // queries of one 32-query half (w / 2) of every block.
+        auto kgrp = [&](int kbw) { return half == 0 ? C::NW * kbw + w : 2 * (half - 1) + (w & 1); };
+        auto key_of = [&](int kbw) { return kb * BLK + 16 * kgrp(kbw) + r; };
 
         // this lane's keys j = key_of(kbw) as B operands (d = 32 ks + 8g + t)
         bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
@@ -500,7 +548,16 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
 
         const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
         const int e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
-        const int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
+        int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
+        if (half == 1) {
+            // the lower keys are attended only inside their own l-block: the
+            // column's first entries (the query blocks ascend)
+            int near = 0;
+            while (near < len &&
+                   !far_block(FIXED, a.dl, BLK * __builtin_amdgcn_readfirstlane(row_idx[e0 + near]), kb * BLK, BLK))
+                ++near;
+            len = near;
+        }
         // The column is walked from its last query block down: the long
         // columns of a head, started together, then visit the same query
         // blocks at about the same time and share those Q / dO tiles in L2.
@@ -556,7 +613,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
                         bits[kbw] = cl[kbw].summary ? (kTileBits >> (4 * g)) : 0ull;
-                        const uint32_t keys = (uint32_t)(key_summary >> (16 * (C::NW * kbw + w))) & 0xFFFFu;
+                        const uint32_t keys = (uint32_t)(key_summary >> (16 * kgrp(kbw))) & 0xFFFFu;
                         const int k_cls = keys == 0u ? CHUNK_NONE : (keys == 0xFFFFu ? CHUNK_ALL : CHUNK_PART);
 #pragma unroll
                         for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = k_cls;
@@ -579,6 +636,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 }
             }
 
+            if (half != 0) {
+                // a half item: this wave takes one 32-query half of the block
+#pragma unroll
+                for (int qc = 0; qc < C::QC; ++qc)
+                    if (qc != (w >> 1)) cls[0][qc] = CHUNK_NONE;
+            }
             // A 32-query chunk enters the products only where some key of the
             // wave is attended by one of its queries; elsewhere P and dS are zero
             // and its operands are neither read nor multiplied (wave-uniform
@@ -671,9 +734,35 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             }
         });
 
+        if constexpr (kHalves) {
+            if (half != 0) {
+                // the two query halves of each key group are summed through LDS
+                // (the ring is idle once every wave has passed the last step)
+                static_assert(sizeof(sQ) >= 2 * 2 * C::DB * 64 * sizeof(f32x4), "reduction fits the Q ring");
+                __syncthreads();
+                f32x4* red = reinterpret_cast<f32x4*>(&sQ[0][0]);
+                const int slot = (w & 1) * 2 * C::DB;
+                if (w >= 2) {
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        red[(slot + db) * 64 + lane] = dvacc[0][db];
+                        red[(slot + C::DB + db) * 64 + lane] = dkacc[0][db];
+                    }
+                }
+                __syncthreads();
+                if (w < 2) {
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        dvacc[0][db] += red[(slot + db) * 64 + lane];
+                        dkacc[0][db] += red[(slot + C::DB + db) * 64 + lane];
+                    }
+                }
+            }
+        }
         // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key_of(kbw)
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
+            if (half != 0 && w >= 2) break;  // written by the wave of the other query half
             const int j = key_of(kbw);
             uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
@@ -780,7 +869,8 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
 }
 
 // Workspace: -D [rows] and -LSE log2 e [rows] (fp32), then (16-byte aligned)
-// the kQueues queue counters and the key-block order of each layout.
+// the kQueues queue counters, the item count per layout, and the item order
+// of each layout (2 nq slots).
 struct BwdWorkspace {
     float* ndelta;  // -D
     float* nlse2;   // -LSE log2 e
@@ -791,7 +881,7 @@ struct BwdWorkspace {
 constexpr int64_t align16(int64_t x) { return (x + 15) / 16 * 16; }
 
 int64_t bwd_workspace_size(int64_t rows, int64_t nq, int n_layouts) {
-    return align16(2 * rows * (int64_t)sizeof(float)) + kQueues * 8 + n_layouts * nq * 4;
+    return align16(2 * rows * (int64_t)sizeof(float)) + (kQueues + 1) * 8 + n_layouts * 2 * nq * 4;
 }
 
 BwdWorkspace bwd_workspace(void* ws, int64_t rows) {
@@ -800,7 +890,7 @@ BwdWorkspace bwd_workspace(void* ws, int64_t rows) {
     w.ndelta = reinterpret_cast<float*>(p);
     w.nlse2 = w.ndelta + rows;
     w.queue = reinterpret_cast<unsigned long long*>(p + align16(2 * rows * (int64_t)sizeof(float)));
-    w.order = reinterpret_cast<int32_t*>(w.queue + kQueues);
+    w.order = reinterpret_cast<int32_t*>(w.queue + kQueues + 1);
     return w;
 }
 

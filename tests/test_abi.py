@@ -110,17 +110,18 @@ def test_fwd_rejects_invalid(L, over, expect):
 def test_bwd_workspace_and_errors(L):
     out = ctypes.c_size_t(0)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
-    # D_i and the base-2 LSE per row, 8 queue counters, the column order of the one layout
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 4 * (256 // 16)
+    # D_i and the base-2 LSE per row, 8 queue counters and the item count, the
+    # item order of the one layout (two slots per key block)
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_F32, ctypes.byref(out)) == 0
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 4 * (256 // 16)
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 8, 1, 3, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 2 * 4 * (256 // 16)  # interleaved: two layouts
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 2 * 4 * (256 // 16)  # interleaved: two layouts
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 40, sa.SA_F32, ctypes.byref(out)) == \
         sa.SA_ERR_UNSUPPORTED
     strides = (ctypes.c_int64 * 3)(256 * 64, 256 * 64, 64)
     common = [256, 16, 16, 0, 0, 2] + [FAKE] * 6 + [1, 1, 64, sa.SA_BF16] + [FAKE] * 6 + [strides, 0.125] + [FAKE] * 3
-    need = 2 * 256 * 4 + 8 * 8 + 4 * (256 // 16)
+    need = 2 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd(*common, FAKE, need - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
     assert L.sparse_attn_bwd(*common, None, need, None) == sa.SA_ERR_INVALID
     bad = list(common)
