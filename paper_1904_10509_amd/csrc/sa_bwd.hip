@@ -266,137 +266,145 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
-        // the treatment of each 32-key chunk
-        uint64_t bits[C::QBW];
-        int cls[C::QBW][C::KC];
+        // In the fixed pattern the step body exists twice: for blocks attended
+        // everywhere (every chunk class a compile-time ALL, no mask and no
+        // branch on classes) and for the others.  The strided pattern has few
+        // such blocks per row (l / B - 1), not worth a second copy of the code.
+        auto compute = [&](auto full) {
+            // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
+            // the treatment of each 32-key chunk
+            uint64_t bits[C::QBW];
+            int cls[C::QBW][C::KC];
 #pragma unroll
-        for (int u = 0; u < C::QBW; ++u) {
-            bits[u] = ~0ull;
+            for (int u = 0; u < C::QBW; ++u) {
+                bits[u] = ~0ull;
 #pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
-        }
-        if (masked) {
-            const int j0_mod = mod_l(a.dl, j0);
-            const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-            const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
-            if (PAT == FIXED && far && mp.part != PART_A1) {
-                // every row attends exactly the summary keys: one mask for the wave
-                const uint64_t sb = sum & kTileBits;
+                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
+            }
+            if constexpr (!decltype(full)::value) {
+                const int j0_mod = mod_l(a.dl, j0);
+                const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
+                const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+                if (PAT == FIXED && far && mp.part != PART_A1) {
+                    // every row attends exactly the summary keys: one mask for the wave
+                    const uint64_t sb = sum & kTileBits;
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u) {
-                    bits[u] = sb >> (4 * g);
+                    for (int u = 0; u < C::QBW; ++u) {
+                        bits[u] = sb >> (4 * g);
 #pragma unroll
-                    for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
-                }
-            } else {
-                if (far) {
-#pragma unroll
-                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                        for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
+                    }
                 } else {
+                    if (far) {
 #pragma unroll
-                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
-                }
+                        for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                    } else {
 #pragma unroll
-                for (int u = 0; u < C::QBW; ++u)
+                        for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                    }
 #pragma unroll
-                    for (int kc = 0; kc < C::KC; ++kc)
-                        cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
-            }
-        }
-        // A 32-key chunk enters the products only where some row of the wave
-        // attends one of its keys; elsewhere dS is zero and the chunk's
-        // operands are neither read nor multiplied (wave-uniform branches)
-        constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
-        bool kc_live[C::KC];
+                    for (int u = 0; u < C::QBW; ++u)
 #pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
-            kc_live[kc] = false;
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
-        }
-        // K^T operands of this block, read now: their LDS latency then hides
-        // behind the S and dP products and the softmax
-        bf16x8 ktr[C::KC][C::DB];
-#pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
-            if (!kc_live[kc]) continue;
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                if constexpr (BLK >= 32) ktr[kc][db] = rd.tr(tK, kc * 32, kc * 32 + 16, db);
-                else ktr[kc][db] = rd.tr_half(tK, 0, db);
-            }
-        }
-
-        // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
-        f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
-#pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
-            const int kc = kblk / HK;
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                s[u][kblk] = zero4();
-                dp[u][kblk] = nd4[u];
-            }
-            if (!kc_live[kc]) continue;
-            bf16x8 kf[C::KS], vf[C::KS];
-#pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) {
-                kf[ks] = rd.row(tK, kblk * 16, ks);
-                vf[ks] = rd.row(tV, kblk * 16, ks);
-            }
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) {
-                if (cls[u][kc] == CHUNK_NONE) continue;
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) {
-                    s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
-                    dp[u][kblk] = mfma_16x16x32(vf[ks], of[u][ks], dp[u][kblk]);
+                        for (int kc = 0; kc < C::KC; ++kc)
+                            cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
                 }
             }
-        }
-
-        // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
-        bf16x8 dsf[C::QBW][C::KC];
-#pragma unroll
-        for (int u = 0; u < C::QBW; ++u) {
+            // A 32-key chunk enters the products only where some row of the wave
+            // attends one of its keys; elsewhere dS is zero and the chunk's
+            // operands are neither read nor multiplied (wave-uniform branches)
+            constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
+            bool kc_live[C::KC];
 #pragma unroll
             for (int kc = 0; kc < C::KC; ++kc) {
-                auto chunk = [&](auto part) {
+                kc_live[kc] = false;
 #pragma unroll
-                    for (int hk = 0; hk < HK; ++hk) {
-                        const int kblk = 2 * kc + hk;
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            float pv = exp2_fast(fmaf(s[u][kblk][t], c2, nl2[u]));
-                            if constexpr (decltype(part)::value)
-                                pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
-                            s[u][kblk][t] = pv * dp[u][kblk][t];
-                        }
-                    }
-                };
-                if (cls[u][kc] == CHUNK_ALL) {
-                    chunk(std::false_type{});
-                } else if (cls[u][kc] == CHUNK_PART) {
-                    chunk(std::true_type{});
-                } else {
-#pragma unroll
-                    for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
-                }
-                if constexpr (BLK >= 32) dsf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
-                else dsf[u][kc] = pack_bf16x8(s[u][0], zero4());
+                for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
             }
-        }
-        // dQ^T += K^T dS^T
+            // K^T operands of this block, read now: their LDS latency then hides
+            // behind the S and dP products and the softmax
+            bf16x8 ktr[C::KC][C::DB];
 #pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if (!kc_live[kc]) continue;
+#pragma unroll
+                for (int db = 0; db < C::DB; ++db) {
+                    if constexpr (BLK >= 32) ktr[kc][db] = rd.tr(tK, kc * 32, kc * 32 + 16, db);
+                    else ktr[kc][db] = rd.tr_half(tK, 0, db);
+                }
+            }
+
+            // S^T and dP^T - D: x[u][kb16][t] for key j0 + 16 kb16 + 4g + t, query row0 + 16u + r
+            f32x4 s[C::QBW][C::KB], dp[C::QBW][C::KB];
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                const int kc = kblk / HK;
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    s[u][kblk] = zero4();
+                    dp[u][kblk] = nd4[u];
+                }
+                if (!kc_live[kc]) continue;
+                bf16x8 kf[C::KS], vf[C::KS];
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) {
+                    kf[ks] = rd.row(tK, kblk * 16, ks);
+                    vf[ks] = rd.row(tV, kblk * 16, ks);
+                }
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) {
+                        s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+                        dp[u][kblk] = mfma_16x16x32(vf[ks], of[u][ks], dp[u][kblk]);
+                    }
+                }
+            }
+
+            // dS^T = P^T (dP^T - D), P^T = exp2(S^T c2 - LSE log2 e)
+            bf16x8 dsf[C::QBW][C::KC];
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
-                if (cls[u][kc] == CHUNK_NONE) continue;
 #pragma unroll
-                for (int db = 0; db < C::DB; ++db) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
+                for (int kc = 0; kc < C::KC; ++kc) {
+                    auto chunk = [&](auto part) {
+#pragma unroll
+                        for (int hk = 0; hk < HK; ++hk) {
+                            const int kblk = 2 * kc + hk;
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) {
+                                float pv = exp2_fast(fmaf(s[u][kblk][t], c2, nl2[u]));
+                                if constexpr (decltype(part)::value)
+                                    pv = select_or_zero(bit_lane_mask(bits[u], 16 * kblk + t), pv);
+                                s[u][kblk][t] = pv * dp[u][kblk][t];
+                            }
+                        }
+                    };
+                    if (cls[u][kc] == CHUNK_ALL) {
+                        chunk(std::false_type{});
+                    } else if (cls[u][kc] == CHUNK_PART) {
+                        chunk(std::true_type{});
+                    } else {
+#pragma unroll
+                        for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
+                    }
+                    if constexpr (BLK >= 32) dsf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
+                    else dsf[u][kc] = pack_bf16x8(s[u][0], zero4());
+                }
             }
-        }
+            // dQ^T += K^T dS^T
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) dqacc[u][db] = mfma_16x16x32(ktr[kc][db], dsf[u][kc], dqacc[u][db]);
+                }
+            }
+        };
+        if (masked || PAT != FIXED) compute(std::false_type{});
+        else compute(std::true_type{});
         cur = nxt;
         return true;
     });
@@ -590,148 +598,156 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint16_t* tO = sdO[st];
             const float* tL = sL[st];
             const float* tD = sDl[st];
+            // The step body exists twice: for blocks attended everywhere (every
+            // chunk class a compile-time ALL unless a half item leaves a query
+            // half to the other waves, no mask) and for the others.
+            auto compute = [&](auto full) {
 
-            // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
-            auto row_stat = [&](const float* tile, int qblk) {
-                return *reinterpret_cast<const f32x4*>(&tile[qblk * 16 + 4 * g]);
-            };
-            // mask bits of this lane's column (bit 16 qblk + t after the shift),
-            // and which 32-query chunks hold an attended item anywhere in the wave
-            uint64_t bits[C::KBW];
-            int cls[C::KBW][C::QC];
-#pragma unroll
-            for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                bits[kbw] = ~0ull;
-#pragma unroll
-                for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = CHUNK_ALL;
-            }
-            if (masked) {
-                const int i0_mod = mod_l(a.dl, i0);
-                const bool far = far_block(PAT, a.dl, i0, kb * BLK, BLK);
-                if (PAT == FIXED && far && mp.part != PART_A1) {
-                    // a summary key is attended by every row, any other key by none
-#pragma unroll
-                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                        bits[kbw] = cl[kbw].summary ? (kTileBits >> (4 * g)) : 0ull;
-                        const uint32_t keys = (uint32_t)(key_summary >> (16 * kgrp(kbw))) & 0xFFFFu;
-                        const int k_cls = keys == 0u ? CHUNK_NONE : (keys == 0xFFFFu ? CHUNK_ALL : CHUNK_PART);
-#pragma unroll
-                        for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = k_cls;
-                    }
-                } else if (far) {
-#pragma unroll
-                    for (int kbw = 0; kbw < C::KBW; ++kbw)
-                        bits[kbw] = (col_mask_far(mp, cl[kbw], i0_mod) & kTileBits) >> (4 * g);
-                } else {
-#pragma unroll
-                    for (int kbw = 0; kbw < C::KBW; ++kbw)
-                        bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
-                }
-                if (!(PAT == FIXED && far && mp.part != PART_A1)) {
-#pragma unroll
-                    for (int kbw = 0; kbw < C::KBW; ++kbw)
-#pragma unroll
-                        for (int qc = 0; qc < C::QC; ++qc)
-                            cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
-                }
-            }
-
-            if (half != 0) {
-                // a half item: this wave takes one 32-query half of the block
-#pragma unroll
-                for (int qc = 0; qc < C::QC; ++qc)
-                    if (qc != (w >> 1)) cls[0][qc] = CHUNK_NONE;
-            }
-            // A 32-query chunk enters the products only where some key of the
-            // wave is attended by one of its queries; elsewhere P and dS are zero
-            // and its operands are neither read nor multiplied (wave-uniform
-            // branches)
-            constexpr int HQ = C::QB >= 2 ? 2 : 1;  // 16-query blocks per 32-query chunk
-            bool qc_live[C::QC];
-#pragma unroll
-            for (int qc = 0; qc < C::QC; ++qc) {
-                qc_live[qc] = false;
-#pragma unroll
-                for (int kbw = 0; kbw < C::KBW; ++kbw) qc_live[qc] = qc_live[qc] || cls[kbw][qc] != CHUNK_NONE;
-            }
-            // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
-            f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
-#pragma unroll
-            for (int qblk = 0; qblk < C::QB; ++qblk) {
-                const int qc = qblk / HQ;
-                if (!qc_live[qc]) continue;
-                bf16x8 qa[C::KS], oa[C::KS];
-#pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) {
-                    qa[ks] = rd.row(tQ, qblk * 16, ks);
-                    oa[ks] = rd.row(tO, qblk * 16, ks);
-                }
+                // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
+                auto row_stat = [&](const float* tile, int qblk) {
+                    return *reinterpret_cast<const f32x4*>(&tile[qblk * 16 + 4 * g]);
+                };
+                // mask bits of this lane's column (bit 16 qblk + t after the shift),
+                // and which 32-query chunks hold an attended item anywhere in the wave
+                uint64_t bits[C::KBW];
+                int cls[C::KBW][C::QC];
 #pragma unroll
                 for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    if (cls[kbw][qc] == CHUNK_NONE) continue;
-                    f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
+                    bits[kbw] = ~0ull;
+#pragma unroll
+                    for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = CHUNK_ALL;
+                }
+                if constexpr (!decltype(full)::value) {
+                    const int i0_mod = mod_l(a.dl, i0);
+                    const bool far = far_block(PAT, a.dl, i0, kb * BLK, BLK);
+                    if (PAT == FIXED && far && mp.part != PART_A1) {
+                        // a summary key is attended by every row, any other key by none
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                            bits[kbw] = cl[kbw].summary ? (kTileBits >> (4 * g)) : 0ull;
+                            const uint32_t keys = (uint32_t)(key_summary >> (16 * kgrp(kbw))) & 0xFFFFu;
+                            const int k_cls = keys == 0u ? CHUNK_NONE : (keys == 0xFFFFu ? CHUNK_ALL : CHUNK_PART);
+#pragma unroll
+                            for (int qc = 0; qc < C::QC; ++qc) cls[kbw][qc] = k_cls;
+                        }
+                    } else if (far) {
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw)
+                            bits[kbw] = (col_mask_far(mp, cl[kbw], i0_mod) & kTileBits) >> (4 * g);
+                    } else {
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw)
+                            bits[kbw] = (col_mask(mp, cl[kbw], i0, i0_mod) & kTileBits) >> (4 * g);
+                    }
+                    if (!(PAT == FIXED && far && mp.part != PART_A1)) {
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw)
+#pragma unroll
+                            for (int qc = 0; qc < C::QC; ++qc)
+                                cls[kbw][qc] = chunk_class(chunk_bits(bits[kbw], qc, C::QB >= 2), C::QB >= 2);
+                    }
+                }
+
+                if (half != 0) {
+                    // a half item: this wave takes one 32-query half of the block
+#pragma unroll
+                    for (int qc = 0; qc < C::QC; ++qc)
+                        if (qc != (w >> 1)) cls[0][qc] = CHUNK_NONE;
+                }
+                // A 32-query chunk enters the products only where some key of the
+                // wave is attended by one of its queries; elsewhere P and dS are zero
+                // and its operands are neither read nor multiplied (wave-uniform
+                // branches)
+                constexpr int HQ = C::QB >= 2 ? 2 : 1;  // 16-query blocks per 32-query chunk
+                bool qc_live[C::QC];
+#pragma unroll
+                for (int qc = 0; qc < C::QC; ++qc) {
+                    qc_live[qc] = false;
+#pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw) qc_live[qc] = qc_live[qc] || cls[kbw][qc] != CHUNK_NONE;
+                }
+                // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
+                f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
+#pragma unroll
+                for (int qblk = 0; qblk < C::QB; ++qblk) {
+                    const int qc = qblk / HQ;
+                    if (!qc_live[qc]) continue;
+                    bf16x8 qa[C::KS], oa[C::KS];
 #pragma unroll
                     for (int ks = 0; ks < C::KS; ++ks) {
-                        sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
-                        dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
-                    }
-                    p[kbw][qblk] = sacc;
-                    ds[kbw][qblk] = dpacc;
-                }
-            }
-
-            // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then
-            // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's
-            // queries; dO^T and Q^T are read transposed from the row-major tiles
-#pragma unroll
-            for (int qc = 0; qc < C::QC; ++qc) {
-                if (!qc_live[qc]) continue;
-                bf16x8 pb[C::KBW], sb[C::KBW];
-#pragma unroll
-                for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                    auto chunk = [&](auto part) {
-#pragma unroll
-                        for (int hq = 0; hq < HQ; ++hq) {
-                            const int qblk = 2 * qc + hq;
-                            const f32x4 nl = row_stat(tL, qblk);
-#pragma unroll
-                            for (int t = 0; t < 4; ++t) {
-                                float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[t]));
-                                if constexpr (decltype(part)::value)
-                                    pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
-                                p[kbw][qblk][t] = pv;
-                                ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
-                            }
-                        }
-                        if constexpr (BLK >= 32) {
-                            pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
-                            sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
-                        } else {
-                            pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
-                            sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
-                        }
-                    };
-                    if (cls[kbw][qc] == CHUNK_ALL) chunk(std::false_type{});
-                    else if (cls[kbw][qc] == CHUNK_PART) chunk(std::true_type{});
-                }
-#pragma unroll
-                for (int db = 0; db < C::DB; ++db) {
-                    bf16x8 oT, qT;
-                    if constexpr (BLK >= 32) {
-                        oT = rd.tr(tO, qc * 32, qc * 32 + 16, db);
-                        qT = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
-                    } else {
-                        oT = rd.tr_half(tO, 0, db);
-                        qT = rd.tr_half(tQ, 0, db);
+                        qa[ks] = rd.row(tQ, qblk * 16, ks);
+                        oa[ks] = rd.row(tO, qblk * 16, ks);
                     }
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
                         if (cls[kbw][qc] == CHUNK_NONE) continue;
-                        dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
-                        dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
+                        f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
+#pragma unroll
+                        for (int ks = 0; ks < C::KS; ++ks) {
+                            sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
+                            dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
+                        }
+                        p[kbw][qblk] = sacc;
+                        ds[kbw][qblk] = dpacc;
                     }
                 }
-            }
+
+                // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then
+                // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's
+                // queries; dO^T and Q^T are read transposed from the row-major tiles
+#pragma unroll
+                for (int qc = 0; qc < C::QC; ++qc) {
+                    if (!qc_live[qc]) continue;
+                    bf16x8 pb[C::KBW], sb[C::KBW];
+#pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                        auto chunk = [&](auto part) {
+#pragma unroll
+                            for (int hq = 0; hq < HQ; ++hq) {
+                                const int qblk = 2 * qc + hq;
+                                const f32x4 nl = row_stat(tL, qblk);
+#pragma unroll
+                                for (int t = 0; t < 4; ++t) {
+                                    float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[t]));
+                                    if constexpr (decltype(part)::value)
+                                        pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
+                                    p[kbw][qblk][t] = pv;
+                                    ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
+                                }
+                            }
+                            if constexpr (BLK >= 32) {
+                                pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
+                                sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                            } else {
+                                pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
+                                sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
+                            }
+                        };
+                        if (cls[kbw][qc] == CHUNK_ALL) chunk(std::false_type{});
+                        else if (cls[kbw][qc] == CHUNK_PART) chunk(std::true_type{});
+                    }
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        bf16x8 oT, qT;
+                        if constexpr (BLK >= 32) {
+                            oT = rd.tr(tO, qc * 32, qc * 32 + 16, db);
+                            qT = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
+                        } else {
+                            oT = rd.tr_half(tO, 0, db);
+                            qT = rd.tr_half(tQ, 0, db);
+                        }
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                            if (cls[kbw][qc] == CHUNK_NONE) continue;
+                            dvacc[kbw][db] = mfma_16x16x32(oT, pb[kbw], dvacc[kbw][db]);
+                            dkacc[kbw][db] = mfma_16x16x32(qT, sb[kbw], dkacc[kbw][db]);
+                        }
+                    }
+                }
+            };
+            // (32-key waves: one body only; the second would not fit the registers)
+            if (masked || C::KBW > 1) compute(std::false_type{});
+            else compute(std::true_type{});
         });
 
         if constexpr (kHalves) {

@@ -124,162 +124,170 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
-        // the treatment of each 32-key chunk
-        uint64_t bits[C::QBW];
-        int cls[C::QBW][C::KC];
-#pragma unroll
-        for (int u = 0; u < C::QBW; ++u) {
-            bits[u] = ~0ull;
-#pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
-        }
-        if (masked) {
-            const int j0_mod = mod_l(a.dl, j0);
-            const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-            const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
-            if (PAT == FIXED && far && mp.part != PART_A1) {
-                // every row attends exactly the summary keys: one mask for the wave
-                const uint64_t sb = sum & kTileBits;
-#pragma unroll
-                for (int u = 0; u < C::QBW; ++u) {
-                    bits[u] = sb >> (4 * g);
-#pragma unroll
-                    for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
-                }
-            } else {
-                if (far) {
-#pragma unroll
-                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
-                } else {
-#pragma unroll
-                    for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
-                }
-#pragma unroll
-                for (int u = 0; u < C::QBW; ++u)
-#pragma unroll
-                    for (int kc = 0; kc < C::KC; ++kc)
-                        cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
-            }
-        }
-
-        // A 32-key chunk enters the products only where some row of the wave
-        // attends one of its keys; elsewhere its probabilities are zero and
-        // its operands are neither read nor multiplied (wave-uniform branches)
-        constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
-        bool kc_live[C::KC];
-#pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
-            kc_live[kc] = false;
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
-        }
-        // V^T operands of this block, read now: their LDS latency then hides
-        // behind the S products and the softmax
-        bf16x8 vt[C::KC][C::DB];
-#pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
-            if (!kc_live[kc]) continue;
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                if constexpr (BLK >= 32) vt[kc][db] = rd.tr(tV, kc * 32, kc * 32 + 16, db);
-                else vt[kc][db] = rd.tr_half(tV, 0, db);
-            }
-        }
-
-        // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
-        f32x4 s[C::QBW][C::KB];
-#pragma unroll
-        for (int kblk = 0; kblk < C::KB; ++kblk) {
-            const int kc = kblk / HK;
-#pragma unroll
-            for (int u = 0; u < C::QBW; ++u) s[u][kblk] = zero4();
-            if (!kc_live[kc]) continue;
-            bf16x8 kf[C::KS];
-#pragma unroll
-            for (int ks = 0; ks < C::KS; ++ks) kf[ks] = rd.row(tK, kblk * 16, ks);
+        // In the fixed pattern the step body exists twice: for blocks attended
+        // everywhere (every chunk class a compile-time ALL, no mask and no
+        // branch on classes) and for the others.  The strided pattern has few
+        // such blocks per row (l / B - 1), not worth a second copy of the code.
+        auto compute = [&](auto full) {
+            // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
+            // the treatment of each 32-key chunk
+            uint64_t bits[C::QBW];
+            int cls[C::QBW][C::KC];
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
-                if (cls[u][kc] == CHUNK_NONE) continue;
+                bits[u] = ~0ull;
 #pragma unroll
-                for (int ks = 0; ks < C::KS; ++ks) s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+                for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = CHUNK_ALL;
             }
-        }
-
-        bf16x8 pf[C::QBW][C::KC];
+            if constexpr (!decltype(full)::value) {
+                const int j0_mod = mod_l(a.dl, j0);
+                const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
+                const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+                if (PAT == FIXED && far && mp.part != PART_A1) {
+                    // every row attends exactly the summary keys: one mask for the wave
+                    const uint64_t sb = sum & kTileBits;
 #pragma unroll
-        for (int u = 0; u < C::QBW; ++u) {
-            // running max in raw score units (the scale is positive) over the
-            // chunks that hold attended keys; masked items become -inf
-            float mloc = -INFINITY;
+                    for (int u = 0; u < C::QBW; ++u) {
+                        bits[u] = sb >> (4 * g);
 #pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) {
-                if (cls[u][kc] == CHUNK_NONE) continue;
-                if (cls[u][kc] == CHUNK_PART) {
-#pragma unroll
-                    for (int hk = 0; hk < HK; ++hk)
-#pragma unroll
-                        for (int t = 0; t < 4; ++t)
-                            s[u][2 * kc + hk][t] =
-                                select_or_neg_inf(bit_lane_mask(bits[u], 16 * (2 * kc + hk) + t), s[u][2 * kc + hk][t]);
-                }
-#pragma unroll
-                for (int hk = 0; hk < HK; ++hk) {
-                    const f32x4 x = s[u][2 * kc + hk];
-                    mloc = fmaxf(mloc, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-                }
-            }
-            mloc = max_over_g(mloc);
-            // The reference is the exact running maximum, so the largest
-            // probability of a row is exactly 1 in bf16 as in fp32.
-            const bool grew = mloc > m_run[u];
-            const float m_new = grew ? mloc : m_run[u];
-            // rows with nothing attended so far keep m = -inf; 0 as reference
-            // gives p = 0 without a branch around the MFMAs
-            const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-            const float neg = -m_ref * c2;
-            float psum = 0.f;
-#pragma unroll
-            for (int kc = 0; kc < C::KC; ++kc) {
-                if (cls[u][kc] != CHUNK_NONE) {
-#pragma unroll
-                    for (int hk = 0; hk < HK; ++hk) {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            const float pv = exp2_fast(fmaf(s[u][2 * kc + hk][t], c2, neg));
-                            s[u][2 * kc + hk][t] = pv;
-                            psum += pv;
-                        }
+                        for (int kc = 0; kc < C::KC; ++kc) cls[u][kc] = uniform_chunk_class(sb, kc, C::KB >= 2);
                     }
                 } else {
+                    if (far) {
 #pragma unroll
-                    for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
+                        for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask_far(mp, rl[u], j0_mod, sum) & kTileBits) >> (4 * g);
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < C::QBW; ++u) bits[u] = (row_mask(mp, rl[u], j0, j0_mod, sum) & kTileBits) >> (4 * g);
+                    }
+#pragma unroll
+                    for (int u = 0; u < C::QBW; ++u)
+#pragma unroll
+                        for (int kc = 0; kc < C::KC; ++kc)
+                            cls[u][kc] = chunk_class(chunk_bits(bits[u], kc, C::KB >= 2), C::KB >= 2);
                 }
-                if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
-                else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
             }
-            // alpha rescales the state kept for the old maximum (0 when it was -inf)
-            const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
-            l_run[u] = fmaf(l_run[u], alpha, psum);
-            m_run[u] = m_new;
-            // O is rescaled only in the blocks where some row's maximum grew
-            // (a wave-uniform branch); everywhere else alpha is exactly 1.
-            if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {
-#pragma unroll
-                for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
-            }
-        }
 
-        // O^T += V^T P^T
+            // A 32-key chunk enters the products only where some row of the wave
+            // attends one of its keys; elsewhere its probabilities are zero and
+            // its operands are neither read nor multiplied (wave-uniform branches)
+            constexpr int HK = C::KB >= 2 ? 2 : 1;  // 16-key blocks per 32-key chunk
+            bool kc_live[C::KC];
 #pragma unroll
-        for (int kc = 0; kc < C::KC; ++kc) {
+            for (int kc = 0; kc < C::KC; ++kc) {
+                kc_live[kc] = false;
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) kc_live[kc] = kc_live[kc] || cls[u][kc] != CHUNK_NONE;
+            }
+            // V^T operands of this block, read now: their LDS latency then hides
+            // behind the S products and the softmax
+            bf16x8 vt[C::KC][C::DB];
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) {
+                if (!kc_live[kc]) continue;
+#pragma unroll
+                for (int db = 0; db < C::DB; ++db) {
+                    if constexpr (BLK >= 32) vt[kc][db] = rd.tr(tV, kc * 32, kc * 32 + 16, db);
+                    else vt[kc][db] = rd.tr_half(tV, 0, db);
+                }
+            }
+
+            // S^T blocks: s[u][kb16][t] = q_(row0+16u+r) . k_(j0 + 16 kb16 + 4g + t)
+            f32x4 s[C::QBW][C::KB];
+#pragma unroll
+            for (int kblk = 0; kblk < C::KB; ++kblk) {
+                const int kc = kblk / HK;
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) s[u][kblk] = zero4();
+                if (!kc_live[kc]) continue;
+                bf16x8 kf[C::KS];
+#pragma unroll
+                for (int ks = 0; ks < C::KS; ++ks) kf[ks] = rd.row(tK, kblk * 16, ks);
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) s[u][kblk] = mfma_16x16x32(kf[ks], qf[u][ks], s[u][kblk]);
+                }
+            }
+
+            bf16x8 pf[C::QBW][C::KC];
 #pragma unroll
             for (int u = 0; u < C::QBW; ++u) {
-                if (cls[u][kc] == CHUNK_NONE) continue;
+                // running max in raw score units (the scale is positive) over the
+                // chunks that hold attended keys; masked items become -inf
+                float mloc = -INFINITY;
 #pragma unroll
-                for (int db = 0; db < C::DB; ++db) oacc[u][db] = mfma_16x16x32(vt[kc][db], pf[u][kc], oacc[u][db]);
+                for (int kc = 0; kc < C::KC; ++kc) {
+                    if (cls[u][kc] == CHUNK_NONE) continue;
+                    if (cls[u][kc] == CHUNK_PART) {
+#pragma unroll
+                        for (int hk = 0; hk < HK; ++hk)
+#pragma unroll
+                            for (int t = 0; t < 4; ++t)
+                                s[u][2 * kc + hk][t] =
+                                    select_or_neg_inf(bit_lane_mask(bits[u], 16 * (2 * kc + hk) + t), s[u][2 * kc + hk][t]);
+                    }
+#pragma unroll
+                    for (int hk = 0; hk < HK; ++hk) {
+                        const f32x4 x = s[u][2 * kc + hk];
+                        mloc = fmaxf(mloc, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+                    }
+                }
+                mloc = max_over_g(mloc);
+                // The reference is the exact running maximum, so the largest
+                // probability of a row is exactly 1 in bf16 as in fp32.
+                const bool grew = mloc > m_run[u];
+                const float m_new = grew ? mloc : m_run[u];
+                // rows with nothing attended so far keep m = -inf; 0 as reference
+                // gives p = 0 without a branch around the MFMAs
+                const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+                const float neg = -m_ref * c2;
+                float psum = 0.f;
+#pragma unroll
+                for (int kc = 0; kc < C::KC; ++kc) {
+                    if (cls[u][kc] != CHUNK_NONE) {
+#pragma unroll
+                        for (int hk = 0; hk < HK; ++hk) {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) {
+                                const float pv = exp2_fast(fmaf(s[u][2 * kc + hk][t], c2, neg));
+                                s[u][2 * kc + hk][t] = pv;
+                                psum += pv;
+                            }
+                        }
+                    } else {
+#pragma unroll
+                        for (int hk = 0; hk < HK; ++hk) s[u][2 * kc + hk] = zero4();
+                    }
+                    if constexpr (BLK >= 32) pf[u][kc] = pack_bf16x8(s[u][2 * kc], s[u][2 * kc + 1]);
+                    else pf[u][kc] = pack_bf16x8(s[u][0], zero4());
+                }
+                // alpha rescales the state kept for the old maximum (0 when it was -inf)
+                const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
+                l_run[u] = fmaf(l_run[u], alpha, psum);
+                m_run[u] = m_new;
+                // O is rescaled only in the blocks where some row's maximum grew
+                // (a wave-uniform branch); everywhere else alpha is exactly 1.
+                if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
+                }
             }
-        }
+
+            // O^T += V^T P^T
+#pragma unroll
+            for (int kc = 0; kc < C::KC; ++kc) {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    if (cls[u][kc] == CHUNK_NONE) continue;
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) oacc[u][db] = mfma_16x16x32(vt[kc][db], pf[u][kc], oacc[u][db]);
+                }
+            }
+        };
+        if (masked || PAT != FIXED) compute(std::false_type{});
+        else compute(std::true_type{});
         cur = nxt;
         return true;
     });
