@@ -167,9 +167,13 @@ bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, 
 // ---------------------------------------------------------------------------
 // bf16, matrix cores: dQ, row-parallel
 // ---------------------------------------------------------------------------
-template <int D, int BLK>
+// Query rows per wave.  Strided: 16, so that in a block holding one diagonal
+// each wave has a single live 32-key chunk and four waves share the block.
+// Fixed: 32, where most steps are fully attended blocks (the summary pairs)
+// and each K / V operand read from LDS then serves 32 rows.
+template <int D, int BLK, int PAT>
 struct DqCfg {
-    static constexpr int RW = BLK < 32 ? BLK : 32;  // query rows per wave
+    static constexpr int RW = BLK < 32 || PAT == STRIDED ? 16 : 32;  // query rows per wave
     static constexpr int QBW = RW / 16;
     static constexpr int NW = BLK / RW;
     static constexpr int NT = NW * 64;
@@ -178,16 +182,18 @@ struct DqCfg {
     static constexpr int KC = (BLK + 31) / 32;
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // K / V ring stages
+    static constexpr int WAVES_PER_EU = RW == 16 ? 3 : 2;
 };
 
 template <int D, int BLK, int PAT, int MODE>
-__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__((DqCfg<D, BLK, PAT>::NT))
+    __attribute__((amdgpu_waves_per_eu(DqCfg<D, BLK, PAT>::WAVES_PER_EU)))
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                    const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                    const float* __restrict__ nlse2, const float* __restrict__ ndelta,
                    uint16_t* __restrict__ dq) {
-    using C = DqCfg<D, BLK>;
+    using C = DqCfg<D, BLK, PAT>;
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
     constexpr uint32_t kTileBytes = BLK * D * 2;
@@ -963,7 +969,7 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
-        hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE>), grid, dim3(DqCfg<D, BLK>::NT), 0, stream, a,
+        hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE>), grid, dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a,
                            a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
                            (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
         const int64_t slots = resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>>(DkvCfg<D, BLK, PAT>::NT);

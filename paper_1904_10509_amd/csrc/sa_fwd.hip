@@ -25,9 +25,12 @@ namespace {
 // ---------------------------------------------------------------------------
 // bf16, matrix cores
 // ---------------------------------------------------------------------------
+// Waves of 16 query rows: with four waves per 64-wide block the workgroup holds
+// more waves per SIMD (fewer registers each), and in the strided pattern a
+// block that holds one diagonal leaves each 16-row wave a single live chunk.
 template <int D, int BLK>
 struct FwdCfg {
-    static constexpr int RW = BLK < 32 ? BLK : 32;  // query rows per wave
+    static constexpr int RW = 16;                   // query rows per wave
     static constexpr int QBW = RW / 16;             // 16-row blocks per wave
     static constexpr int NW = BLK / RW;             // waves per workgroup
     static constexpr int NT = NW * 64;              // threads
@@ -42,7 +45,7 @@ struct FwdCfg {
 // over the XCDs) share a query block index across heads, so with heads a
 // multiple of 8 each head stays on one XCD and its keys stay in that L2.
 template <int D, int BLK, int PAT, int MODE>
-__global__ void __launch_bounds__(BLK < 32 ? 64 : 2 * BLK)
+__global__ void __launch_bounds__((FwdCfg<D, BLK>::NT)) __attribute__((amdgpu_waves_per_eu(3)))
 fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                 const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
