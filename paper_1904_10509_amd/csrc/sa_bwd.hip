@@ -428,24 +428,23 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 // ---------------------------------------------------------------------------
 // bf16, matrix cores: dK and dV, column-parallel
 // ---------------------------------------------------------------------------
-// Keys per wave.  In the fixed pattern a block away from the diagonal is
-// uniform over each 16-key group (all of its keys are summary keys or none
-// is), so 16-key waves skip whole softmax passes and, holding half the
-// registers, run three to a SIMD instead of two.  In the strided pattern such
-// a block holds one diagonal, every group is partial, and 32-key waves read
-// each Q / dO operand from LDS for twice the keys.
+// Waves of 16 keys, four per 64-wide block, three waves per SIMD.  In the
+// fixed pattern a block away from the diagonal is uniform over each 16-key
+// group (all of its keys are summary keys or none is), so whole waves skip
+// their products; in the strided pattern a block holding one diagonal leaves
+// each 16-key wave a single live 32-query chunk.
 template <int D, int BLK, int PAT>
 struct DkvCfg {
-    static constexpr int KW = BLK < 32 || PAT == FIXED ? 16 : 32;  // keys per wave
-    static constexpr int KBW = KW / 16;                            // 16-key blocks per wave
-    static constexpr int NW = BLK / KW;                            // waves
+    static constexpr int KW = 16;               // keys per wave
+    static constexpr int KBW = KW / 16;         // 16-key blocks per wave
+    static constexpr int NW = BLK / KW;         // waves
     static constexpr int NT = NW * 64;
     static constexpr int KS = D / 32;           // 32-deep steps over d
     static constexpr int QB = BLK / 16;         // 16-query blocks per tile
     static constexpr int QC = (BLK + 31) / 32;  // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
-    static constexpr int WAVES_PER_EU = KW == 16 ? 3 : 2;
+    static constexpr int WAVES_PER_EU = 3;
 };
 
 template <int D, int BLK, int PAT, int MODE>
@@ -606,7 +605,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const float* tD = sDl[st];
             // The step body exists twice: for blocks attended everywhere (every
             // chunk class a compile-time ALL unless a half item leaves a query
-            // half to the other waves, no mask) and for the others.
+            // half to the other waves, no mask) and for the others, in both
+            // patterns.
             auto compute = [&](auto full) {
 
                 // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
@@ -751,8 +751,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                 }
             };
-            // (32-key waves: one body only; the second would not fit the registers)
-            if (masked || C::KBW > 1) compute(std::false_type{});
+            if (masked) compute(std::false_type{});
             else compute(std::true_type{});
         });
 
