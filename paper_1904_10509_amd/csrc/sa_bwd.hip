@@ -253,15 +253,15 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     };
     wait_loads_upto<0>();  // register loads done before the ring starts
     // two-stage ring; the next step's blocks are read one step ahead
-    RowStepper<kPairs> steps{col_idx, e0, e1};
-    RowStep cur = steps.next(mp, a.dl, qb * BLK);
+    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    RowStep cur = steps.next();
     if (cur.a >= 0) load_step(cur, 0);
     TileReader<D> rd;
     rd.init(g, r);
     two_stage_while([&](auto stage) {
         constexpr int st = decltype(stage)::value;
         if (cur.a < 0) return false;
-        const RowStep nxt = steps.next(mp, a.dl, qb * BLK);
+        const RowStep nxt = steps.next();
         const int kb = cur.a;
         const int j0 = kb * BLK;
         // a pair of upper halves is attended everywhere

@@ -108,15 +108,15 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const float c2 = a.scale_log2;
     // two-stage ring; the next step's blocks are read one step ahead (scalar
     // loads, off the vector-memory counter the ring waits on)
-    RowStepper<kPairs> steps{col_idx, e0, e1};
-    RowStep cur = steps.next(mp, a.dl, qb * BLK);
+    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    RowStep cur = steps.next();
     if (cur.a >= 0) load_step(cur, 0);
     TileReader<D> rd;
     rd.init(g, r);
     two_stage_while([&](auto stage) {
         constexpr int st = decltype(stage)::value;  // ring stage of the current step
         if (cur.a < 0) return false;
-        const RowStep nxt = steps.next(mp, a.dl, qb * BLK);
+        const RowStep nxt = steps.next();
         const int kb = cur.a;
         const int j0 = kb * BLK;
         // a pair of upper halves is attended everywhere

@@ -129,35 +129,37 @@ __device__ inline bool far_block(int pattern, const DivL& dl, int i0, int j0, in
     return j1 < i0 - mod_l(dl, i0);
 }
 
-// A 64-wide block of the fixed pattern away from the diagonal whose attended
-// keys, the same for every row, are exactly its upper 32 (summary) keys.  Two
-// such blocks of one block row can be computed as one unmasked block made of
-// their upper halves.  Wave-uniform arguments: evaluated on the scalar unit.
-__device__ inline bool upper_half_summary_block(const MaskParams& p, const DivL& dl, int i0, int j0) {
-    if (p.pattern != FIXED || p.part == PART_A1 || !far_block(FIXED, dl, i0, j0, 64)) return false;
-    return summary_bits(p, mod_l(dl, j0)) == 0xFFFFFFFF00000000ull;
-}
-
-// The steps of a walk along one block row (query block at row i0): a step is
-// one present block, or, with PAIRS (fixed pattern, B = 64), two consecutive
-// upper_half_summary_block blocks computed together.  RowStep::a < 0: the row
-// is done; RowStep::b < 0: block a alone.  Entries are read with scalar loads.
+// The steps of a walk along one block row: a step is one present block, or,
+// with PAIRS (fixed pattern, B = 64), two consecutive blocks whose attended
+// keys, the same for every row, are exactly their upper 32, computed together
+// as one unmasked block made of the two upper halves.  When c = 32 and l is a
+// multiple of 64, every present block away from the diagonal is such a block
+// (only the last block of an l-block holds summary keys, exactly its upper
+// 32), and the blocks away from the diagonal are those below far_end, the
+// first block of the row's l-block: so one compare per entry decides.
+// RowStep::a < 0: the row is done; RowStep::b < 0: block a alone.  Entries are
+// read with scalar loads.
 struct RowStep {
     int a, b;
 };
 template <bool PAIRS>
 struct RowStepper {
     const int32_t* col_idx;
-    int e, e1;  // next entry, end of the row
-    __device__ RowStep next(const MaskParams& p, const DivL& dl, int i0) {
+    int e, e1;    // next entry, end of the row
+    int far_end;  // pairs are formed below this key block; 0: no pairs
+    __device__ static int pair_bound(const MaskParams& p, const DivL& dl, int i0) {
+        if (p.pattern != FIXED || p.part == PART_A1 || p.c != 32 || p.l % 64 != 0) return 0;
+        return (i0 - mod_l(dl, i0)) / 64;
+    }
+    __device__ RowStep next() {
         RowStep s{-1, -1};
         if (e >= e1) return s;
         s.a = __builtin_amdgcn_readfirstlane(col_idx[e]);
         ++e;
         if constexpr (PAIRS) {
             if (e < e1) {
-                const int kb = __builtin_amdgcn_readfirstlane(col_idx[e]);
-                if (upper_half_summary_block(p, dl, i0, 64 * s.a) && upper_half_summary_block(p, dl, i0, 64 * kb)) {
+                const int kb = __builtin_amdgcn_readfirstlane(col_idx[e]);  // entries ascend: kb > s.a
+                if (kb < far_end) {
                     s.b = kb;
                     ++e;
                 }
