@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--workloads", default=",".join(BENCH_WORKLOADS),
+                    help="comma-separated workload names (default: the two measured workloads of the metric); "
+                         "other workloads give side measurements, not the metric's line")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -159,7 +162,8 @@ def main():
         copy_calibration(torch, dev)
 
     runs = []
-    for name in BENCH_WORKLOADS:
+    names = [x for x in args.workloads.split(",") if x]
+    for name in names:
         w = WORKLOADS[name]
         x = workload_inputs(w)
         lay = sa.build_layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode, device=dev)
@@ -237,7 +241,7 @@ def main():
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": " + ".join(BENCH_WORKLOADS),
+        "config": {"workload": " + ".join(names),
                    "workloads": {r["w"].name: r["w"].describe() for r in runs}},
         "pct_bf16_peak": 100 * value / PEAK_BF16_TFLOPS,
         "per_workload": per,
