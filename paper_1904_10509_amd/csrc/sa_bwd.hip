@@ -672,58 +672,58 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) qc_live[qc] = qc_live[qc] || cls[kbw][qc] != CHUNK_NONE;
                 }
-                // S and dP - D: x[kbw][qblk][t] is query i0 + 16 qblk + 4g + t against key key_of(kbw)
-                f32x4 p[C::KBW][C::QB], ds[C::KBW][C::QB];
-#pragma unroll
-                for (int qblk = 0; qblk < C::QB; ++qblk) {
-                    const int qc = qblk / HQ;
-                    if (!qc_live[qc]) continue;
-                    bf16x8 qa[C::KS], oa[C::KS];
-#pragma unroll
-                    for (int ks = 0; ks < C::KS; ++ks) {
-                        qa[ks] = rd.row(tQ, qblk * 16, ks);
-                        oa[ks] = rd.row(tO, qblk * 16, ks);
-                    }
-#pragma unroll
-                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
-                        if (cls[kbw][qc] == CHUNK_NONE) continue;
-                        f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
-#pragma unroll
-                        for (int ks = 0; ks < C::KS; ++ks) {
-                            sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
-                            dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
-                        }
-                        p[kbw][qblk] = sacc;
-                        ds[kbw][qblk] = dpacc;
-                    }
-                }
-
-                // P = exp2(S c2 - LSE log2 e), dS = P (dP - D), then
-                // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's
-                // queries; dO^T and Q^T are read transposed from the row-major tiles
+                // Per 32-query chunk: S and dP - D, then P = exp2(S c2 - LSE log2 e)
+                // and dS = P (dP - D), then dV^T += dO^T P and dK^T += Q^T dS,
+                // contracting over the chunk's queries (dO^T and Q^T read
+                // transposed from the row-major tiles).  A chunk is finished before
+                // the next starts, so only its P and dS are live.
 #pragma unroll
                 for (int qc = 0; qc < C::QC; ++qc) {
                     if (!qc_live[qc]) continue;
+                    // x[kbw][hq][t]: query i0 + 16 (2 qc + hq) + 4g + t against key key_of(kbw)
+                    f32x4 p[C::KBW][HQ], ds[C::KBW][HQ];
+#pragma unroll
+                    for (int hq = 0; hq < HQ; ++hq) {
+                        const int qblk = HQ * qc + hq;
+                        bf16x8 qa[C::KS], oa[C::KS];
+#pragma unroll
+                        for (int ks = 0; ks < C::KS; ++ks) {
+                            qa[ks] = rd.row(tQ, qblk * 16, ks);
+                            oa[ks] = rd.row(tO, qblk * 16, ks);
+                        }
+#pragma unroll
+                        for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                            if (cls[kbw][qc] == CHUNK_NONE) continue;
+                            f32x4 sacc = zero4(), dpacc = row_stat(tD, qblk);
+#pragma unroll
+                            for (int ks = 0; ks < C::KS; ++ks) {
+                                sacc = mfma_16x16x32(qa[ks], kf[kbw][ks], sacc);
+                                dpacc = mfma_16x16x32(oa[ks], vf[kbw][ks], dpacc);
+                            }
+                            p[kbw][hq] = sacc;
+                            ds[kbw][hq] = dpacc;
+                        }
+                    }
                     bf16x8 pb[C::KBW], sb[C::KBW];
 #pragma unroll
                     for (int kbw = 0; kbw < C::KBW; ++kbw) {
                         auto chunk = [&](auto part) {
 #pragma unroll
                             for (int hq = 0; hq < HQ; ++hq) {
-                                const int qblk = 2 * qc + hq;
+                                const int qblk = HQ * qc + hq;
                                 const f32x4 nl = row_stat(tL, qblk);
 #pragma unroll
                                 for (int t = 0; t < 4; ++t) {
-                                    float pv = exp2_fast(fmaf(p[kbw][qblk][t], c2, nl[t]));
+                                    float pv = exp2_fast(fmaf(p[kbw][hq][t], c2, nl[t]));
                                     if constexpr (decltype(part)::value)
                                         pv = select_or_zero(bit_lane_mask(bits[kbw], 16 * qblk + t), pv);
-                                    p[kbw][qblk][t] = pv;
-                                    ds[kbw][qblk][t] = pv * ds[kbw][qblk][t];
+                                    p[kbw][hq][t] = pv;
+                                    ds[kbw][hq][t] = pv * ds[kbw][hq][t];
                                 }
                             }
-                            if constexpr (BLK >= 32) {
-                                pb[kbw] = pack_bf16x8(p[kbw][2 * qc], p[kbw][2 * qc + 1]);
-                                sb[kbw] = pack_bf16x8(ds[kbw][2 * qc], ds[kbw][2 * qc + 1]);
+                            if constexpr (HQ == 2) {
+                                pb[kbw] = pack_bf16x8(p[kbw][0], p[kbw][1]);
+                                sb[kbw] = pack_bf16x8(ds[kbw][0], ds[kbw][1]);
                             } else {
                                 pb[kbw] = pack_bf16x8(p[kbw][0], zero4());
                                 sb[kbw] = pack_bf16x8(ds[kbw][0], zero4());
