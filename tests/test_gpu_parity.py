@@ -77,6 +77,10 @@ SMALL_CASES = [
     (F, IL, 1024, 64, 128, 32, 128, torch.bfloat16, 2, 2),
     # an odd number of summary key blocks: one upper half left without a partner
     (F, MG, 768, 64, 256, 32, 64, torch.bfloat16, 1, 2),
+    # d = 32 with pairs and half items; l = 96 (blocks straddle l-blocks): half
+    # items without pairs
+    (F, MG, 512, 64, 128, 32, 32, torch.bfloat16, 1, 2),
+    (F, MG, 768, 64, 96, 32, 64, torch.bfloat16, 1, 1),
     # more (batch, head) pairs than the dK / dV kernel has queues, not a multiple of them
     (S, MG, 256, 32, 32, 0, 32, torch.bfloat16, 3, 5),
     (F, IL, 256, 16, 64, 16, 32, torch.bfloat16, 3, 3),
