@@ -133,6 +133,70 @@ def cpu_baseline(workloads, inputs):
     }
 
 
+# The paper's Table 2: time per training iteration of whole models (dense
+# attention against the two sparse patterns), on its own hardware.  Quoted only
+# as the ratios next to which the attention-only ratios here are set.
+TABLE2 = {
+    "text, n=12,288": {"dense": "dense_n12288_merged", "fixed": "fixed_n12288_l128_c32_merged",
+                       "strided": "strided_n12288_l128_merged",
+                       "paper_time_per_iter": {"dense": 1.31, "fixed": 0.55, "strided": 0.35}},
+    "image, n=3,072": {"dense": "dense_n3072_merged", "fixed": "fixed_n3072_l128_c32_merged",
+                       "strided": "strided_n3072_l128_merged",
+                       "paper_time_per_iter": {"dense": 0.54, "fixed": 0.47, "strided": 0.38}},
+}
+
+
+def table2(args):
+    """Attention forward + backward time, dense causal against fixed and strided,
+    at the two contexts of Table 2 (same kernels; dense is the stride-n limit)."""
+    import torch
+
+    from paper_1904_10509_amd import sparse_attn as sa
+    from paper_1904_10509_amd.inputs import WORKLOADS, workload_inputs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    out = {"metric": "attention fwd+bwd time, dense causal vs sparse (kernel analogue of Table 2)",
+           "unit": "ms", "higher_is_better": False, "steps": args.steps, "warmup": args.warmup,
+           "dtype": "bf16", "data": "synthetic", "contexts": {}}
+    for ctx, spec in TABLE2.items():
+        res = {}
+        for kind in ("dense", "fixed", "strided"):
+            w = WORKLOADS[spec[kind]]
+            x = workload_inputs(w)
+            lay = sa.build_layout(w.n, w.block, w.stride, w.summary, w.pattern, w.mode, device=dev)
+            q, k, v, dout = (x[n_].to(dev) for n_ in ("q", "k", "v", "dout"))
+            o = torch.empty_like(q)
+            lse = torch.empty(q.shape[:3], dtype=torch.float32, device=dev)
+            grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+            need = sa.sparse_attn_bwd_workspace_size(*lay.pattern_args, w.batch, w.heads, w.d_head, sa.SA_BF16)
+            ws = torch.empty(need, dtype=torch.uint8, device=dev)
+
+            def step():
+                sa.forward(q, k, v, lay, w.scale, out=o, lse=lse)
+                sa.backward(q, k, v, o, dout, lse, lay, w.scale, grads=grads, workspace=ws)
+
+            for _ in range(args.warmup):
+                step()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                step()
+            e1.record()
+            torch.cuda.synchronize()
+            cred, _ = credited_flops(w, lay.nnz)
+            ms = e0.elapsed_time(e1) / args.steps
+            res[kind] = {"workload": w.name, "ms": ms, "nnz_blocks": lay.nnz,
+                         "credited_tflops": cred / (ms * 1e-3) / 1e12}
+        paper = spec["paper_time_per_iter"]
+        for kind in ("fixed", "strided"):
+            res[kind]["speedup_vs_dense"] = res["dense"]["ms"] / res[kind]["ms"]
+            res[kind]["paper_speedup_vs_dense"] = paper["dense"] / paper[kind]
+        out["contexts"][ctx] = res
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,7 +208,13 @@ def main():
     ap.add_argument("--workloads", default=",".join(BENCH_WORKLOADS),
                     help="comma-separated workload names (default: the two measured workloads of the metric); "
                          "other workloads give side measurements, not the metric's line")
+    ap.add_argument("--table2", action="store_true",
+                    help="instead of the metric's line, time dense causal against fixed and strided attention at "
+                         "the two contexts of the paper's Table 2")
     args = ap.parse_args()
+    if args.table2:
+        table2(args)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(see the sharding design note); run with --gpus 1", file=sys.stderr)

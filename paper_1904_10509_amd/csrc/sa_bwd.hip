@@ -185,7 +185,7 @@ struct DqCfg {
     static constexpr int WAVES_PER_EU = RW == 16 ? 3 : 2;
 };
 
-template <int D, int BLK, int PAT, int MODE>
+template <int D, int BLK, int PAT, int MODE, bool FULL_BODY>
 __global__ void __launch_bounds__((DqCfg<D, BLK, PAT>::NT))
     __attribute__((amdgpu_waves_per_eu(DqCfg<D, BLK, PAT>::WAVES_PER_EU)))
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
@@ -272,10 +272,9 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // In the fixed pattern the step body exists twice: for blocks attended
+        // With FULL_BODY the step body exists twice: for blocks attended
         // everywhere (every chunk class a compile-time ALL, no mask and no
-        // branch on classes) and for the others.  The strided pattern has few
-        // such blocks per row (l / B - 1), not worth a second copy of the code.
+        // branch on classes) and for the others (see with_full_body).
         auto compute = [&](auto full) {
             // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
             // the treatment of each 32-key chunk
@@ -409,7 +408,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                 }
             }
         };
-        if (masked || PAT != FIXED) compute(std::false_type{});
+        if (masked || !FULL_BODY) compute(std::false_type{});
         else compute(std::true_type{});
         cur = nxt;
         return true;
@@ -968,9 +967,13 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
-        hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE>), grid, dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a,
-                           a.row_ptr, a.col_idx, (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                           (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dq);
+        with_full_body<PAT>(a, [&](auto fb) {
+            hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value>), grid,
+                               dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx,
+                               (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)dout,
+                               nlse2, ndelta, (uint16_t*)dq);
+            return hipSuccess;
+        });
         const int64_t slots = resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>>(DkvCfg<D, BLK, PAT>::NT);
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));

@@ -44,7 +44,7 @@ struct FwdCfg {
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
 // over the XCDs) share a query block index across heads, so with heads a
 // multiple of 8 each head stays on one XCD and its keys stay in that L2.
-template <int D, int BLK, int PAT, int MODE>
+template <int D, int BLK, int PAT, int MODE, bool FULL_BODY>
 __global__ void __launch_bounds__((FwdCfg<D, BLK>::NT)) __attribute__((amdgpu_waves_per_eu(3)))
 fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                 const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -127,10 +127,9 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
-        // In the fixed pattern the step body exists twice: for blocks attended
+        // With FULL_BODY the step body exists twice: for blocks attended
         // everywhere (every chunk class a compile-time ALL, no mask and no
-        // branch on classes) and for the others.  The strided pattern has few
-        // such blocks per row (l / B - 1), not worth a second copy of the code.
+        // branch on classes) and for the others (see with_full_body).
         auto compute = [&](auto full) {
             // mask bits of this lane's rows (bit 16 kb16 + t after the shift), and
             // the treatment of each 32-key chunk
@@ -289,7 +288,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                 }
             }
         };
-        if (masked || PAT != FIXED) compute(std::false_type{});
+        if (masked || !FULL_BODY) compute(std::false_type{});
         else compute(std::true_type{});
         cur = nxt;
         return true;
@@ -365,10 +364,13 @@ hipError_t launch_bf16(const AttnArgs& a, const void* q, const void* k, const vo
                        float* lse, hipStream_t stream) {
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
-        hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK, decltype(pat)::value, decltype(mode)::value>), grid,
-                           dim3(FwdCfg<D, BLK>::NT), 0, stream, a, a.row_ptr, a.col_idx, (const uint16_t*)q,
-                           (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
-        return hipGetLastError();
+        constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
+        return with_full_body<PAT>(a, [&](auto fb) {
+            hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value>), grid,
+                               dim3(FwdCfg<D, BLK>::NT), 0, stream, a, a.row_ptr, a.col_idx, (const uint16_t*)q,
+                               (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
+            return hipGetLastError();
+        });
     });
 }
 

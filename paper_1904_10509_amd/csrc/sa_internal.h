@@ -74,6 +74,21 @@ hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k
 
 // Backward workspace: D and the base-2 LSE per row [b, h, n] (fp32), then
 // the work queues and the column order of the dK / dV kernel.
+// Whether the row-view kernels (forward, dQ) carry a second step body for
+// fully attended blocks: always in the fixed pattern; in the strided pattern
+// when those blocks (l / B - 1 per row) outnumber the diagonal-only blocks of
+// a middle row (about n / 2l), i.e. 2 l^2 > n B, as in the dense limit l >= n.
+// Otherwise the second copy of the code costs more than it saves.
+template <int PAT, typename F>
+inline hipError_t with_full_body(const AttnArgs& a, F&& f) {
+    if constexpr (PAT == FIXED) {
+        return f(std::true_type{});
+    } else {
+        if (2.0 * (double)a.l * (double)a.l > (double)a.n * (double)a.block) return f(std::true_type{});
+        return f(std::false_type{});
+    }
+}
+
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, int n_layouts);
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,

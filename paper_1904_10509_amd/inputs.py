@@ -68,6 +68,19 @@ WORKLOADS = {
                  BF16, 4, "audio sequence of 65,536"),
         Workload("strided_n1048576_l1024_merged", STRIDED, MODE_MERGED, 1048576, 1024, 0, 64, 1, 4,
                  64, BF16, 5, "audio sequence of 1,048,576"),
+        # dense against sparse at the two contexts of the paper's Table 2 (text of
+        # 12,288: 8 heads of 64; image of 3,072: 2 heads of 128); dense causal
+        # attention is the strided pattern with a stride of n (A1 then covers j <= i)
+        Workload("dense_n12288_merged", STRIDED, MODE_MERGED, 12288, 12288, 0, 64, 2, 8, 64, BF16, 6,
+                 "dense causal limit at the text context of 12,288"),
+        Workload("fixed_n12288_l128_c32_merged", FIXED, MODE_MERGED, 12288, 128, 32, 64, 2, 8, 64, BF16, 7,
+                 "text context of 12,288, fixed pattern with the paper's text settings"),
+        Workload("dense_n3072_merged", STRIDED, MODE_MERGED, 3072, 3072, 0, 64, 4, 2, 128, BF16, 8,
+                 "dense causal limit at the image context of 3,072"),
+        Workload("fixed_n3072_l128_c32_merged", FIXED, MODE_MERGED, 3072, 128, 32, 64, 4, 2, 128, BF16, 9,
+                 "image context of 3,072, fixed pattern"),
+        Workload("strided_n3072_l128_merged", STRIDED, MODE_MERGED, 3072, 128, 0, 64, 4, 2, 128, BF16, 10,
+                 "image context of 3,072, strided pattern"),
     ]
 }
 

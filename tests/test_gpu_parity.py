@@ -126,13 +126,16 @@ def test_workload_interleaved_full():
 def sample_index(w, rng, count):
     """(b, h, i) triples: first and last rows, tile and l-block edges, random."""
     idx = [0, 1, w.block - 1, w.block, w.stride - 1, w.stride, w.stride + 1, w.n // 2, w.n - w.block, w.n - 1]
+    idx = [min(i, w.n - 1) for i in idx]  # a dense-limit stride equals n
     idx += list(rng.integers(0, w.n, count - len(idx)))
     b = rng.integers(0, w.batch, len(idx))
     h = rng.integers(0, w.heads, len(idx))
     return np.stack([b, h, np.array(idx)], axis=1)
 
 
-@pytest.mark.parametrize("name", ["strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged"])
+@pytest.mark.parametrize("name", ["strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged",
+                                  "dense_n12288_merged", "fixed_n12288_l128_c32_merged", "dense_n3072_merged",
+                                  "fixed_n3072_l128_c32_merged", "strided_n3072_l128_merged"])
 def test_workload_sampled(name):
     w = WORKLOADS[name]
     x = workload_inputs(w)
