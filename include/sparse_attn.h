@@ -172,6 +172,46 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static English description of a status code. */
+/*
+ * Bytes of device workspace that sparse_attn_decode needs (host only): the
+ * partial softmax states of the key ranges a decoding step is split into,
+ * (d_head + 2) fp32 values per range and (batch, head).  Pattern arguments
+ * as in sparse_attn_decode.
+ */
+int sparse_attn_decode_workspace_size(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                                      int32_t head_mode, int32_t batch, int32_t heads, int32_t d_head,
+                                      int32_t dtype, size_t* bytes);
+
+/*
+ * One step of autoregressive generation (the samples of Fig. 1 are drawn one
+ * position at a time, Sec. 5.6): for every (batch, head), the output of the
+ * single query at position pos attending S_pos (Sec. 4.3, heads combined as
+ * in Sec. 5.1) over a key / value cache that holds positions 0 .. pos:
+ *     o = softmax_j( scale * q . k_j )  v_j     over j in S_pos.
+ * The same result as row pos of sparse_attn_fwd on a sequence of pos + 1
+ * positions, without a layout: S_pos is enumerated directly (no block size),
+ * and q . k and the softmax are computed in fp32 (the paper casts queries and
+ * keys to single precision for sampling).
+ *   q        [batch, heads, d_head], element strides q_strides[0..1] (batch,
+ *            head), d contiguous.  o has the same shape and strides.
+ *   k_cache, v_cache  [batch, heads, >= pos + 1, d_head], element strides
+ *            kv_strides[0..2] (batch, head, sequence), d contiguous, sequence
+ *            stride >= d_head.
+ *   lse      [batch, heads] contiguous fp32, natural log; -inf (and o = 0)
+ *            when S_pos is empty.
+ * Every base address 16-byte aligned and every stride a multiple of 16 bytes.
+ * workspace: at least sparse_attn_decode_workspace_size bytes of device memory,
+ * 16-byte aligned (SA_ERR_BUFFER_TOO_SMALL otherwise); its contents on entry
+ * are ignored and calls sharing one workspace must not overlap.
+ * pos in [0, 2^31 - 1]; pattern, head_mode, stride_l, summary_c, d_head and
+ * dtype as in sparse_attn_fwd.
+ */
+int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t pattern, int32_t head_mode,
+                       int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, const void* q,
+                       const int64_t* q_strides, const void* k_cache, const void* v_cache,
+                       const int64_t* kv_strides, float softmax_scale, void* o, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 const char* sparse_attn_status_string(int status);
 
 #ifdef __cplusplus

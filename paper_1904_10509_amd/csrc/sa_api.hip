@@ -96,6 +96,22 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     return a;
 }
 
+// Pattern arguments of a decoding step (no block size: S_pos is enumerated).
+int check_decode_pattern(int64_t pos, int32_t l, int32_t c, int32_t pattern, int32_t mode) {
+    if (pos < 0 || pos > INT32_MAX || l < 1) return SA_ERR_INVALID;
+    if (pattern != SA_STRIDED && pattern != SA_FIXED) return SA_ERR_INVALID;
+    if (mode < SA_MODE_A1 || mode > SA_MODE_INTERLEAVED) return SA_ERR_INVALID;
+    if (pattern == SA_FIXED && (c < 1 || c > l)) return SA_ERR_INVALID;
+    if (pattern == SA_STRIDED && c != 0) return SA_ERR_INVALID;
+    return SA_OK;
+}
+int check_decode_shape(int32_t batch, int32_t heads, int32_t d, int32_t dtype) {
+    if (batch < 1 || heads < 1 || (int64_t)batch * heads > INT32_MAX / 2) return SA_ERR_INVALID;
+    if (dtype != SA_F32 && dtype != SA_BF16) return SA_ERR_INVALID;
+    if (d != 32 && d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
+    return SA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -193,6 +209,47 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                                kind, col_ptr, row_idx, kind_t);
     hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
                                   static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+
+int sparse_attn_decode_workspace_size(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                                      int32_t head_mode, int32_t batch, int32_t heads, int32_t d_head,
+                                      int32_t dtype, size_t* bytes) {
+    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode);
+    if (st != SA_OK) return st;
+    st = check_decode_shape(batch, heads, d_head, dtype);
+    if (st != SA_OK) return st;
+    if (!bytes) return SA_ERR_INVALID;
+    *bytes = sa::decode_workspace_bytes(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head);
+    return SA_OK;
+}
+
+int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t pattern, int32_t head_mode,
+                       int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, const void* q,
+                       const int64_t* q_strides, const void* k_cache, const void* v_cache,
+                       const int64_t* kv_strides, float softmax_scale, void* o, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode);
+    if (st != SA_OK) return st;
+    st = check_decode_shape(batch, heads, d_head, dtype);
+    if (st != SA_OK) return st;
+    if (!q || !q_strides || !k_cache || !v_cache || !kv_strides || !o || !lse) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o)) return SA_ERR_INVALID;
+    const int64_t unit = dtype == SA_BF16 ? 8 : 4;  // elements per 16 bytes
+    for (int t = 0; t < 2; ++t)
+        if (q_strides[t] < 0 || q_strides[t] % unit != 0) return SA_ERR_INVALID;
+    for (int t = 0; t < 3; ++t)
+        if (kv_strides[t] < 0 || kv_strides[t] % unit != 0) return SA_ERR_INVALID;
+    if (kv_strides[2] < d_head) return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
+    const size_t need =
+        sa::decode_workspace_bytes(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head);
+    if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
+    if (!workspace || !aligned16(workspace)) return SA_ERR_INVALID;
+    hipError_t e = sa::decode_launch(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head,
+                                     dtype, q, q_strides, k_cache, v_cache, kv_strides, softmax_scale, o, lse,
+                                     workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

@@ -89,6 +89,13 @@ inline hipError_t with_full_body(const AttnArgs& a, F&& f) {
     }
 }
 
+size_t decode_workspace_bytes(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int64_t batch,
+                              int64_t heads, int d);
+hipError_t decode_launch(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int batch, int heads, int d,
+                         int dtype, const void* q, const int64_t* q_strides, const void* k, const void* v,
+                         const int64_t* kv_strides, float scale, void* o, float* lse, void* workspace,
+                         hipStream_t stream);
+
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, int n_layouts);
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,

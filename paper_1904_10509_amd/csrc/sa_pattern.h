@@ -162,6 +162,53 @@ __host__ __device__ inline bool block_full32(int pattern, int part, const DivL& 
     return one_block || all_summary;
 }
 
+// The set S_pos of one query position (Sec. 4.3) as an index space for
+// decoding: key t (0 <= t < count) is position at(t), each position of the set
+// exactly once.  Order: the A1 interval ascending, then the A2 positions
+// outside it (strided: pos - 2l, pos - 3l, ...; fixed: the summary columns of
+// the earlier l-blocks, ascending).  A2 alone: strided pos, pos - l, ...;
+// fixed the summary columns up to pos, ascending.  dc divides by c (fixed).
+struct DecodeSet {
+    int pattern, part;
+    int32_t pos, l, c;
+    int32_t a1_lo;      // A1 is [a1_lo, a1_lo + n1)
+    int64_t n1;         // up to 2^31 (pos = 2^31 - 1 with A1 from 0)
+    int64_t count;
+    DivL dc;
+    __host__ __device__ DecodeSet(int pattern_, int part_, int32_t pos_, int32_t l_, int32_t c_, const DivL& dc_)
+        : pattern(pattern_), part(part_), pos(pos_), l(l_), c(c_), dc(dc_) {
+        const int32_t lblk = pos / l;
+        if (pattern == STRIDED) {
+            a1_lo = pos - l > 0 ? pos - l : 0;
+            n1 = (int64_t)pos - a1_lo + 1;
+            if (part == PART_A1) count = n1;
+            else if (part == PART_A2) count = (int64_t)lblk + 1;
+            else count = n1 + (lblk > 1 ? lblk - 1 : 0);
+        } else {
+            a1_lo = lblk * l;
+            n1 = (int64_t)pos - a1_lo + 1;
+            const int32_t first_sum = a1_lo + l - c;  // first summary column of pos's l-block
+            if (part == PART_A1) count = n1;
+            else if (part == PART_A2) count = (int64_t)lblk * c + (pos >= first_sum ? pos - first_sum + 1 : 0);
+            else count = n1 + (int64_t)lblk * c;
+        }
+    }
+    __host__ __device__ int32_t summary(int32_t u) const {  // u-th summary column from position 0
+        const int32_t blk = div_l(dc, u);
+        return blk * l + l - c + (u - blk * c);
+    }
+    __host__ __device__ int32_t at(int64_t t) const {
+        if (pattern == STRIDED) {
+            if (part == PART_A2) return pos - (int32_t)t * l;
+            if (t < n1) return a1_lo + (int32_t)t;
+            return pos - ((int32_t)(t - n1) + 2) * l;
+        }
+        if (part == PART_A2) return summary((int32_t)t);
+        if (t < n1) return a1_lo + (int32_t)t;
+        return summary((int32_t)(t - n1));
+    }
+};
+
 // Element predicate in 32-bit arithmetic (0 <= i, j < 2^31).
 __host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32_t c, int32_t i,
                                          int32_t j) {

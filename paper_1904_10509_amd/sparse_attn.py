@@ -30,6 +30,8 @@ EXPORTED = (
     "sparse_attn_fwd",
     "sparse_attn_bwd_workspace_size",
     "sparse_attn_bwd",
+    "sparse_attn_decode_workspace_size",
+    "sparse_attn_decode",
     "sparse_attn_status_string",
 )
 
@@ -57,6 +59,9 @@ def lib():
         L.sparse_attn_bwd_workspace_size.argtypes = _PAT + [_i32] * 4 + [_vp]
         L.sparse_attn_bwd.argtypes = (_PAT + [_vp] * 6 + [_i32] * 4 + [_vp] * 7 + [_f32]
                                       + [_vp] * 4 + [_sz, _vp])
+        _DEC = [_i64, _i32, _i32, _i32, _i32]  # pos, stride_l, summary_c, pattern, head_mode
+        L.sparse_attn_decode_workspace_size.argtypes = _DEC + [_i32] * 4 + [_vp]
+        L.sparse_attn_decode.argtypes = _DEC + [_i32] * 4 + [_vp] * 5 + [_f32] + [_vp] * 3 + [_sz, _vp]
         L.sparse_attn_status_string.argtypes = [ctypes.c_int]
         L.sparse_attn_status_string.restype = ctypes.c_char_p
         for name in EXPORTED[:-1]:
@@ -153,6 +158,23 @@ def sparse_attn_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, 
     _check("sparse_attn_bwd", st)
 
 
+def sparse_attn_decode_workspace_size(pos, stride_l, summary_c, pattern, head_mode, batch, heads, d_head, dtype):
+    out = ctypes.c_size_t(0)
+    st = lib().sparse_attn_decode_workspace_size(pos, stride_l, summary_c, pattern, head_mode, batch, heads,
+                                                 d_head, dtype, ctypes.byref(out))
+    _check("sparse_attn_decode_workspace_size", st)
+    return out.value
+
+
+def sparse_attn_decode(pos, stride_l, summary_c, pattern, head_mode, batch, heads, d_head, dtype, q, q_strides,
+                       k_cache, v_cache, kv_strides, softmax_scale, o, lse, workspace, workspace_bytes,
+                       stream=None):
+    st = lib().sparse_attn_decode(pos, stride_l, summary_c, pattern, head_mode, batch, heads, d_head, dtype,
+                                  _ptr(q), q_strides, _ptr(k_cache), _ptr(v_cache), kv_strides, softmax_scale,
+                                  _ptr(o), _ptr(lse), _ptr(workspace), workspace_bytes, _stream(stream, q.device))
+    _check("sparse_attn_decode", st)
+
+
 # ---------------------------------------------------------------------------
 # Convenience layer: torch allocates, the entry points above compute
 # ---------------------------------------------------------------------------
@@ -236,6 +258,32 @@ def backward(q, k, v, o, dout, lse, layout: Layout, softmax_scale=None, grads=No
                     dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
                     workspace.numel() * workspace.element_size(), stream)
     return dq, dk, dv
+
+
+def decode(q, k_cache, v_cache, pos, stride_l, summary_c, pattern, head_mode, softmax_scale=None, out=None,
+           lse=None, workspace=None, stream=None):
+    """Output of query position ``pos`` (q: [b, h, d]) over the cache ([b, h, >= pos + 1, d]) and S_pos."""
+    b, h, d = q.shape
+    if k_cache.dim() != 4 or k_cache.shape[:2] != (b, h) or k_cache.shape[3] != d or k_cache.shape[2] <= pos:
+        raise ValueError("cache must be [batch, heads, >= pos + 1, d] matching q")
+    if v_cache.shape != k_cache.shape or v_cache.stride() != k_cache.stride() or k_cache.stride(3) != 1:
+        raise ValueError("k_cache and v_cache must share shape and strides, d contiguous")
+    if q.stride(2) != 1:
+        raise ValueError("q must have d contiguous")
+    o = torch.empty_like(q) if out is None else out
+    if o.shape != q.shape or o.stride() != q.stride():
+        raise ValueError("out must match q in shape and strides")
+    lse = torch.empty((b, h), dtype=torch.float32, device=q.device) if lse is None else lse
+    dtype = _dtype_code(q)
+    need = sparse_attn_decode_workspace_size(pos, stride_l, summary_c, pattern, head_mode, b, h, d, dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    qs = (ctypes.c_int64 * 2)(q.stride(0), q.stride(1))
+    ks = (ctypes.c_int64 * 3)(k_cache.stride(0), k_cache.stride(1), k_cache.stride(2))
+    sparse_attn_decode(pos, stride_l, summary_c, pattern, head_mode, b, h, d, dtype, q, qs, k_cache, v_cache, ks,
+                       _scale(softmax_scale, d), o, lse, workspace, workspace.numel() * workspace.element_size(),
+                       stream)
+    return o, lse
 
 
 class SparseAttention(torch.autograd.Function):

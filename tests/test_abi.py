@@ -140,3 +140,52 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(sa, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError, match="not built"):
         sa.lib()
+
+
+
+def test_decode_workspace_and_errors(L):
+    out = ctypes.c_size_t(0)
+    # fixed, pos 65,535, l 256, c 32: |S_pos| = 256 + 255 * 32 = 8,416 keys, 33 ranges of up to 256 keys,
+    # (64 + 2) fp32 per range and (batch, head)
+    assert L.sparse_attn_decode_workspace_size(65535, 256, 32, sa.SA_FIXED, sa.SA_MODE_MERGED, 1, 8, 64, sa.SA_BF16,
+                                               ctypes.byref(out)) == 0
+    assert out.value == 8 * 33 * 66 * 4
+    # a single range when the set is small; ranges capped at 4,096 workgroups in all
+    assert L.sparse_attn_decode_workspace_size(5, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 2, 3, 32, sa.SA_F32,
+                                               ctypes.byref(out)) == 0
+    assert out.value == 6 * 1 * 34 * 4
+    assert L.sparse_attn_decode_workspace_size(2**31 - 1, 2**31 - 1, 0, sa.SA_STRIDED, sa.SA_MODE_A1, 64, 8, 128,
+                                               sa.SA_BF16, ctypes.byref(out)) == 0
+    assert out.value == 64 * 8 * 8 * 130 * 4
+    bad = [
+        (-1, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (2**31, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 0, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 0, sa.SA_FIXED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 17, sa.SA_FIXED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 4, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 0, sa.SA_STRIDED, 4, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 0, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
+        (10, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 48, sa.SA_BF16, sa.SA_ERR_UNSUPPORTED),
+        (10, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, 7, sa.SA_ERR_INVALID),
+    ]
+    for *args, expect in bad:
+        assert L.sparse_attn_decode_workspace_size(*args, ctypes.byref(out)) == expect, args
+    assert L.sparse_attn_decode_workspace_size(10, 16, 0, 0, 2, 1, 1, 64, 1, None) == sa.SA_ERR_INVALID
+    # validation before any launch: bad strides, alignment, workspace, scale (fake device pointers)
+    qs = (ctypes.c_int64 * 2)(64, 64)
+    ks = (ctypes.c_int64 * 3)(64 * 64, 64 * 64, 64)
+    need = 1 * 1 * 1 * 66 * 4
+    base = [10, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16]
+
+    def call(q=FAKE, qst=qs, k=FAKE, v=FAKE, kst=ks, scale=0.125, o=FAKE, lse=FAKE, ws=FAKE, wsb=need):
+        return L.sparse_attn_decode(*base, q, qst, k, v, kst, scale, o, lse, ws, wsb, None)
+
+    assert call(q=None) == sa.SA_ERR_INVALID
+    assert call(q=FAKE + 2) == sa.SA_ERR_INVALID
+    assert call(qst=(ctypes.c_int64 * 2)(60, 64)) == sa.SA_ERR_INVALID
+    assert call(kst=(ctypes.c_int64 * 3)(64 * 64, 64 * 64, 32)) == sa.SA_ERR_INVALID
+    assert call(scale=float("nan")) == sa.SA_ERR_INVALID
+    assert call(scale=-1.0) == sa.SA_ERR_INVALID
+    assert call(wsb=need - 1) == sa.SA_ERR_BUFFER_TOO_SMALL
+    assert call(ws=None) == sa.SA_ERR_INVALID

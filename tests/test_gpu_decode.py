@@ -1,0 +1,97 @@
+"""GPU parity of the decoding entry point (sparse_attn_decode) against the fp64
+oracle: the output and LSE of query position pos over S_pos equal row pos of
+the oracle's forward on the same inputs (Sec. 4.2, 4.3, 5.1)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc_mod
+from paper_1904_10509_amd import sparse_attn as sa
+from paper_1904_10509_amd.inputs import make_inputs
+
+from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, to64
+
+pytestmark = pytest.mark.gpu
+
+S, F = sa.SA_STRIDED, sa.SA_FIXED
+A1, A2, MG, IL = sa.SA_MODE_A1, sa.SA_MODE_A2, sa.SA_MODE_MERGED, sa.SA_MODE_INTERLEAVED
+
+# (pattern, mode, n of the cache, l, c, d, dtype, batch, heads)
+CASES = [
+    (S, MG, 600, 16, 0, 32, torch.float32, 1, 2),
+    (S, A2, 600, 16, 0, 64, torch.float32, 2, 1),
+    (F, IL, 600, 32, 8, 128, torch.float32, 1, 3),
+    (S, MG, 2048, 128, 0, 64, torch.bfloat16, 2, 3),
+    (S, A1, 1000, 100, 0, 64, torch.bfloat16, 1, 2),
+    (S, MG, 700, 1000, 0, 128, torch.bfloat16, 1, 2),  # dense limit
+    (F, MG, 4096, 256, 32, 64, torch.bfloat16, 1, 4),
+    (F, A2, 1500, 128, 32, 32, torch.bfloat16, 2, 2),
+    (F, IL, 3072, 128, 32, 128, torch.bfloat16, 2, 2),
+    (F, A1, 900, 96, 40, 64, torch.bfloat16, 1, 1),
+]
+
+
+def positions(n, l):
+    """First and last positions, l-block and stride edges, a few inside."""
+    ps = {0, 1, l - 1, l, l + 1, 2 * l, 3 * l - 1, n // 2, n - 2, n - 1}
+    return sorted(p for p in ps if 0 <= p < n)
+
+
+@pytest.mark.parametrize("pattern,mode,n,l,c,d,dtype,batch,heads", CASES)
+def test_decode_matches_oracle_rows(pattern, mode, n, l, c, d, dtype, batch, heads):
+    dev = device()
+    x = make_inputs(batch, heads, n, d, dtype, seed=n + l + c + d + 7)
+    scale = d ** -0.5
+    kc, vc = x["k"].to(dev), x["v"].to(dev)
+    xi = oracle_inputs(x)
+    for pos in positions(n, l):
+        q = x["q"][:, :, pos, :].contiguous().to(dev)
+        o, lse = sa.decode(q, kc, vc, pos, l, c, pattern, mode, scale)
+        torch.cuda.synchronize()
+        rows = np.array([(b, h, pos) for b in range(batch) for h in range(heads)])
+        o_ref, lse_ref = orc_mod.forward_rows(*xi[:3], rows, pattern=pattern, mode=mode, l=l, c=c, scale=scale)
+        got_o = to64(o).reshape(-1, d)
+        got_lse = to64(lse).reshape(-1)
+        assert max_err(got_o, o_ref) <= TOL[dtype], (pos, max_err(got_o, o_ref))
+        assert max_err(got_lse, lse_ref) <= LSE_TOL[dtype], (pos, max_err(got_lse, lse_ref))
+
+
+def test_decode_empty_set_and_views():
+    """Fixed A2 before the first summary column: empty S_pos gives o = 0 and
+    LSE = -inf.  A cache that is a view into a longer buffer (larger sequence
+    stride than d) gives the same result as a contiguous copy."""
+    dev = device()
+    n, l, c, d = 512, 64, 16, 64
+    x = make_inputs(1, 2, n, d, torch.bfloat16, seed=3)
+    kc, vc = x["k"].to(dev), x["v"].to(dev)
+    q = x["q"][:, :, 10, :].contiguous().to(dev)
+    o, lse = sa.decode(q, kc, vc, 10, l, c, F, A2, d ** -0.5)
+    torch.cuda.synchronize()
+    assert torch.all(o == 0) and torch.all(torch.isneginf(lse))
+    wide_k = torch.zeros(1, 2, n, 2 * d, dtype=torch.bfloat16, device=dev)
+    wide_v = torch.zeros_like(wide_k)
+    wide_k[..., :d] = kc
+    wide_v[..., :d] = vc
+    q = x["q"][:, :, 300, :].contiguous().to(dev)
+    o1, lse1 = sa.decode(q, kc, vc, 300, l, c, F, MG, d ** -0.5)
+    o2, lse2 = sa.decode(q, wide_k[..., :d], wide_v[..., :d], 300, l, c, F, MG, d ** -0.5)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(lse1, lse2)
+
+
+def test_decode_large_position():
+    """pos = 65,535 of the fixed n = 65,536 workload shape (8 heads of 64):
+    sampled against the oracle."""
+    dev = device()
+    n, l, c, d = 65536, 256, 32, 64
+    x = make_inputs(1, 8, n, d, torch.bfloat16, seed=4)
+    kc, vc = x["k"].to(dev), x["v"].to(dev)
+    xi = oracle_inputs(x)
+    for pos in (n - 1, 40000, 257):
+        q = x["q"][:, :, pos, :].contiguous().to(dev)
+        o, lse = sa.decode(q, kc, vc, pos, l, c, F, MG, d ** -0.5)
+        torch.cuda.synchronize()
+        rows = np.array([(0, h, pos) for h in range(8)])
+        o_ref, lse_ref = orc_mod.forward_rows(*xi[:3], rows, pattern=F, mode=MG, l=l, c=c, scale=d ** -0.5)
+        assert max_err(to64(o).reshape(-1, d), o_ref) <= 2e-2
+        assert max_err(to64(lse).reshape(-1), lse_ref) <= 1e-3
