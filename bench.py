@@ -197,6 +197,77 @@ def table2(args):
     print(json.dumps(out), flush=True)
 
 
+# Decoding steps at the two long-sequence shapes: one new position per
+# sequence, a batch of sequences, the K / V cache resident in HBM.
+DECODE = {
+    "fixed n=65,536 (l 256, c 32, 8 heads of 64)":
+        dict(n=65536, l=256, c=32, pattern=1, heads=8, d=64, batch=32, seed=21),
+    "strided n=1,048,576 (l 1,024, 4 heads of 64)":
+        dict(n=1048576, l=1024, c=0, pattern=0, heads=4, d=64, batch=16, seed=22),
+}
+
+
+def decode_bench(args):
+    """Time per decoding step (sparse_attn_decode at positions n - steps .. n - 1,
+    one per step, as in generation) and the bandwidth of the K / V rows it
+    reads (|S_pos| rows of K and of V per (sequence, head)) against HBM."""
+    import torch
+
+    from paper_1904_10509_amd import sparse_attn as sa
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    out = {"metric": "decoding step time and K/V bandwidth (sparse_attn_decode)", "unit": "us", "dtype": "bf16",
+           "data": "synthetic", "steps": args.steps, "warmup": args.warmup, "shapes": {}}
+    for name, c in DECODE.items():
+        g = torch.Generator(device=dev).manual_seed(c["seed"])
+        shape = (c["batch"], c["heads"], c["n"], c["d"])
+        kc = torch.randn(shape, generator=g, device=dev, dtype=torch.bfloat16)
+        vc = torch.randn(shape, generator=g, device=dev, dtype=torch.bfloat16)
+        qs = torch.randn((args.steps + args.warmup, c["batch"], c["heads"], c["d"]), generator=g, device=dev,
+                         dtype=torch.bfloat16)
+        o = torch.empty_like(qs[0])
+        lse = torch.empty((c["batch"], c["heads"]), dtype=torch.float32, device=dev)
+        ws_bytes = sa.sparse_attn_decode_workspace_size(c["n"] - 1, c["l"], c["c"], c["pattern"], sa.SA_MODE_MERGED,
+                                                        c["batch"], c["heads"], c["d"], sa.SA_BF16)
+        ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+        total = args.steps + args.warmup
+        positions = [c["n"] - total + s for s in range(total)]
+
+        def step(s):
+            sa.decode(qs[s], kc, vc, positions[s], c["l"], c["c"], c["pattern"], sa.SA_MODE_MERGED,
+                      out=o, lse=lse, workspace=ws)
+
+        for s in range(args.warmup):
+            step(s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for s in range(args.warmup, total):
+            step(s)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        # |S_pos| of the merged sets (closed forms of Sec. 4.3), averaged over the timed positions
+        rows = 0
+        for pos in positions[args.warmup:]:
+            if c["pattern"] == 0:
+                rows += min(pos, c["l"]) + 1 + max(0, pos // c["l"] - 1)
+            else:
+                rows += pos % c["l"] + 1 + (pos // c["l"]) * c["c"]
+        rows /= args.steps
+        kv_bytes = 2.0 * rows * c["d"] * 2 * c["batch"] * c["heads"]
+        gbs = kv_bytes / (us * 1e-6) / 1e9
+        out["shapes"][name] = {"batch": c["batch"], "heads": c["heads"], "d": c["d"], "cache_len": c["n"],
+                               "keys_per_step": rows, "us_per_step": us, "kv_bytes_per_step": kv_bytes,
+                               "tokens_per_s": c["batch"] / (us * 1e-6),
+                               "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                            "frac": gbs / HBM_PEAK_GBS}}
+        del kc, vc
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,7 +282,13 @@ def main():
     ap.add_argument("--table2", action="store_true",
                     help="instead of the metric's line, time dense causal against fixed and strided attention at "
                          "the two contexts of the paper's Table 2")
+    ap.add_argument("--decode", action="store_true",
+                    help="instead of the metric's line, time decoding steps (sparse_attn_decode) at the two "
+                         "long-sequence shapes")
     args = ap.parse_args()
+    if args.decode:
+        decode_bench(args)
+        return
     if args.table2:
         table2(args)
         return
