@@ -268,6 +268,79 @@ def decode_bench(args):
     print(json.dumps(out), flush=True)
 
 
+# Strided A2 heads two ways: the block-sparse kernels over the A2 layout, and
+# the transposed form (dense causal attention per residue class, Sec. 5.5).
+TRANSPOSED = {
+    "text, n=12,288 (l 128, 2 x 8 heads of 64)": dict(n=12288, l=128, batch=2, heads=8, d=64, block=64,
+                                                        class_block=32, seed=31),
+    "audio, n=1,048,576 (l 1,024, 4 heads of 64)": dict(n=1048576, l=1024, batch=1, heads=4, d=64, block=64,
+                                                          class_block=64, seed=32),
+}
+
+
+def transposed_bench(args):
+    """Forward + backward time of strided A2 attention, block-sparse against
+    transposed, with FLOPs counted per attended pair (14 d per pair and head:
+    4 d forward, 10 d backward), the honest count for both."""
+    import torch
+
+    from paper_1904_10509_amd import sparse_attn as sa
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    out = {"metric": "strided A2 fwd+bwd: block-sparse vs transposed (Sec. 5.5)", "unit": "ms", "dtype": "bf16",
+           "data": "synthetic", "steps": args.steps, "warmup": args.warmup, "shapes": {}}
+    for name, c in TRANSPOSED.items():
+        g = torch.Generator(device=dev).manual_seed(c["seed"])
+        shape = (c["batch"], c["heads"], c["n"], c["d"])
+        q, k, v, dout = (torch.randn(shape, generator=g, device=dev, dtype=torch.bfloat16) for _ in range(4))
+        m = c["n"] // c["l"]
+        pairs = c["l"] * m * (m + 1) // 2 * c["batch"] * c["heads"]
+        flop = 14.0 * c["d"] * pairs
+        res = {}
+        lay_b = sa.build_layout(c["n"], c["block"], c["l"], 0, sa.SA_STRIDED, sa.SA_MODE_A2, device=dev)
+        lay_t = sa.transposed_a2_layout(c["n"], c["l"], c["class_block"], device=dev)
+        o = torch.empty_like(q)
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+        lse_b = torch.empty(shape[:3], dtype=torch.float32, device=dev)
+        lse_t = torch.empty((c["batch"] * c["heads"], c["l"], m), dtype=torch.float32, device=dev)
+        ws_b = torch.empty(max(16, sa.sparse_attn_bwd_workspace_size(*lay_b.pattern_args, c["batch"], c["heads"],
+                                                                     c["d"], sa.SA_BF16)), dtype=torch.uint8,
+                           device=dev)
+        ws_t = torch.empty(max(16, sa.sparse_attn_bwd_workspace_size(*lay_t.pattern_args,
+                                                                     c["batch"] * c["heads"], c["l"], c["d"],
+                                                                     sa.SA_BF16)), dtype=torch.uint8, device=dev)
+
+        def block_step():
+            sa.forward(q, k, v, lay_b, out=o, lse=lse_b)
+            sa.backward(q, k, v, o, dout, lse_b, lay_b, grads=grads, workspace=ws_b)
+
+        def transposed_step():
+            sa.forward_a2_transposed(q, k, v, c["l"], lay_t, out=o, lse=lse_t)
+            sa.backward_a2_transposed(q, k, v, o, dout, lse_t, c["l"], lay_t, grads=grads, workspace=ws_t)
+
+        for kind, fn in (("block", block_step), ("transposed", transposed_step)):
+            for _ in range(args.warmup):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            res[kind] = {"ms": ms, "pair_tflops": flop / (ms * 1e-3) / 1e12}
+        res["block"]["layout_blocks"] = lay_b.nnz
+        res["transposed"]["class_layout_blocks"] = lay_t.nnz
+        res["speedup"] = res["block"]["ms"] / res["transposed"]["ms"]
+        res["attended_pairs"] = pairs
+        out["shapes"][name] = res
+        del q, k, v, dout, o, grads
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -285,7 +358,13 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="instead of the metric's line, time decoding steps (sparse_attn_decode) at the two "
                          "long-sequence shapes")
+    ap.add_argument("--transposed", action="store_true",
+                    help="instead of the metric's line, time strided A2 attention block-sparse against the "
+                         "transposed form (dense causal per residue class)")
     args = ap.parse_args()
+    if args.transposed:
+        transposed_bench(args)
+        return
     if args.decode:
         decode_bench(args)
         return

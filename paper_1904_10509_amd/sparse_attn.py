@@ -286,6 +286,71 @@ def decode(q, k_cache, v_cache, pos, stride_l, summary_c, pattern, head_mode, so
     return o, lse
 
 
+# ---------------------------------------------------------------------------
+# Strided A2 by transposition (Sec. 5.5).  With l dividing n, write positions
+# as i = m l + r (class r = i mod l, index m = i div l): j is in A2 of i iff
+# j has the same class and m_j <= m_i.  In class order A2 is therefore dense
+# causal attention inside each of the l classes of n / l positions.  A class is
+# a strided view of a [b, h, n, d] tensor (first row r, a step of l rows), so
+# the entry points above compute it unchanged: "batch" = the b * h heads (the
+# stride of one head), "heads" = the l classes (a stride of d elements),
+# sequence stride l rows, and the dense causal layout of n / l positions (the
+# strided pattern with a stride of n / l).  O and the gradients land in place
+# in the original layout; LSE comes out in class order, [b * h, l, n / l].
+# ---------------------------------------------------------------------------
+def transposed_a2_layout(n, stride_l, block, device="cuda", stream=None):
+    """Dense causal layout of one class: n / l positions in blocks of ``block``."""
+    if n % stride_l != 0 or (n // stride_l) % block != 0:
+        raise ValueError("needs l | n and block | n / l")
+    m = n // stride_l
+    return build_layout(m, block, m, 0, SA_STRIDED, SA_MODE_A1, device=device, stream=stream)
+
+
+def _class_view_strides(t, stride_l):
+    b, h, n, d = t.shape
+    if not t.is_contiguous():
+        raise ValueError("the transposed path takes contiguous [b, h, n, d] tensors")
+    return (ctypes.c_int64 * 3)(n * d, d, stride_l * d)  # a head, a class, a step within a class
+
+
+def forward_a2_transposed(q, k, v, stride_l, class_layout: Layout, softmax_scale=None, out=None, lse=None,
+                          stream=None):
+    """O (original layout) and LSE (class order) of strided A2 attention, computed per class."""
+    b, h, n, d = q.shape
+    strides = _class_view_strides(q, stride_l)
+    for t in (k, v):
+        if t.shape != q.shape:
+            raise ValueError("q, k, v must have one shape")
+        _class_view_strides(t, stride_l)
+    m = n // stride_l
+    if class_layout.n != m:
+        raise ValueError("class layout is for another n / l")
+    o = torch.empty_like(q) if out is None else out
+    _class_view_strides(o, stride_l)
+    lse = torch.empty((b * h, stride_l, m), dtype=torch.float32, device=q.device) if lse is None else lse
+    sparse_attn_fwd(*class_layout.pattern_args, *class_layout.row_args, b * h, stride_l, d, _dtype_code(q), q, k,
+                    v, strides, _scale(softmax_scale, d), o, lse, stream)
+    return o, lse
+
+
+def backward_a2_transposed(q, k, v, o, dout, lse, stride_l, class_layout: Layout, softmax_scale=None, grads=None,
+                           workspace=None, stream=None):
+    """dq, dk, dv (original layout) of strided A2 attention, given the class-order LSE."""
+    b, h, n, d = q.shape
+    strides = _class_view_strides(q, stride_l)
+    for t in (k, v, o, dout):
+        _class_view_strides(t, stride_l)
+    dq, dk, dv = grads if grads is not None else (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    dtype = _dtype_code(q)
+    need = sparse_attn_bwd_workspace_size(*class_layout.pattern_args, b * h, stride_l, d, dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    sparse_attn_bwd(*class_layout.pattern_args, *class_layout.row_args, *class_layout.col_args, b * h, stride_l,
+                    d, dtype, q, k, v, o, dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
+                    workspace.numel() * workspace.element_size(), stream)
+    return dq, dk, dv
+
+
 class SparseAttention(torch.autograd.Function):
     """Autograd wrapper: saves O and LSE, recomputes attention weights in backward."""
 
