@@ -7,11 +7,13 @@ It has nothing in common with the interval enumeration of the C oracle.
 """
 import numpy as np
 
-STRIDED, FIXED = 0, 1
+STRIDED, FIXED, FIXED_PER_HEAD = 0, 1, 2
 
 
-def part_mask(pattern, part, n, l, c):
-    """Boolean [n, n] mask, mask[i, j] = j in S_i, for part 0=A1, 1=A2, 2=merged."""
+def part_mask(pattern, part, n, l, c, s=0):
+    """Boolean [n, n] mask, mask[i, j] = j in S_i, for part 0=A1, 1=A2, 2=merged.
+    Fixed pattern: s picks the summary subblock, positions l-(s+1)c .. l-sc-1
+    of each block (s = 0: the last c positions)."""
     i = np.arange(n)[:, None]
     j = np.arange(n)[None, :]
     causal = j <= i
@@ -20,7 +22,7 @@ def part_mask(pattern, part, n, l, c):
         a2 = ((i - j) % l) == 0
     else:
         a1 = (j // l) == (i // l)
-        a2 = (j % l) >= (l - c)
+        a2 = ((j % l) >= (l - (s + 1) * c)) & ((j % l) < (l - s * c))
     if part == 0:
         m = a1
     elif part == 1:
@@ -32,7 +34,8 @@ def part_mask(pattern, part, n, l, c):
 
 def head_mask(pattern, mode, h, n, l, c):
     part = mode if mode < 3 else (0 if h % 2 == 0 else 1)
-    return part_mask(pattern, part, n, l, c)
+    s = h % (l // c) if pattern == FIXED_PER_HEAD else 0
+    return part_mask(pattern, part, n, l, c, s)
 
 
 def attention(q, k, v, mask, scale):

@@ -5,7 +5,9 @@ float64, float32, or bfloat16 stored as raw uint16 bit patterns; the C side
 converts each element exactly to fp64.  Outputs are float64.
 
 Pattern / mode codes follow the paper's vocabulary (Sec. 4.3 and Sec. 5.1):
-pattern 0 = strided, 1 = fixed; mode 0 = A1 only, 1 = A2 only, 2 = merged
+pattern 0 = strided, 1 = fixed, 2 = fixed with a distinct summary subblock
+per head (head h attends positions l-(s+1)c .. l-sc-1 of every l-block, with
+s = h mod floor(l/c)); mode 0 = A1 only, 1 = A2 only, 2 = merged
 (union of A1 and A2), 3 = interleaved over heads (even heads A1, odd heads A2).
 """
 import ctypes
@@ -13,7 +15,7 @@ import numpy as np
 
 from .build import ensure_built
 
-STRIDED, FIXED = 0, 1
+STRIDED, FIXED, FIXED_PER_HEAD = 0, 1, 2
 MODE_A1, MODE_A2, MODE_MERGED, MODE_INTERLEAVED = 0, 1, 2, 3
 PART_A1, PART_A2, PART_MERGED = 0, 1, 2
 
@@ -33,6 +35,12 @@ def lib():
         L.oracle_row_set.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _vp]
         L.oracle_col_set.restype = _i64
         L.oracle_col_set.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _vp]
+        L.oracle_head_row_set.restype = _i64
+        L.oracle_head_row_set.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _i64, _vp]
+        L.oracle_head_col_set.restype = _i64
+        L.oracle_head_col_set.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _i64, _vp]
+        L.oracle_num_layouts.restype = _int
+        L.oracle_num_layouts.argtypes = [_i64, _i64, _int, _int]
         L.oracle_forward.restype = _int
         L.oracle_forward.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _i64, _i64, _int,
                                      _vp, _vp, _vp, _dbl, _vp, _vp]
@@ -97,6 +105,26 @@ def col_set(pattern, part, n, l, c, j):
     out = np.empty(max(m, 1), dtype=np.int64)
     lib().oracle_col_set(pattern, part, n, l, c, j, _ptr(out))
     return out[:m]
+
+
+def head_row_set(pattern, mode, n, l, c, h, i):
+    """S_i of head h of a multi-head call (its factor and summary window)."""
+    m = lib().oracle_head_row_set(pattern, mode, n, l, c, h, i, None)
+    out = np.empty(max(m, 1), dtype=np.int64)
+    lib().oracle_head_row_set(pattern, mode, n, l, c, h, i, _ptr(out))
+    return out[:m]
+
+
+def head_col_set(pattern, mode, n, l, c, h, j):
+    """T_j of head h, ascending."""
+    m = lib().oracle_head_col_set(pattern, mode, n, l, c, h, j, None)
+    out = np.empty(max(m, 1), dtype=np.int64)
+    lib().oracle_head_col_set(pattern, mode, n, l, c, h, j, _ptr(out))
+    return out[:m]
+
+
+def num_layouts(l, c, pattern, mode):
+    return int(lib().oracle_num_layouts(l, c, pattern, mode))
 
 
 def forward(q, k, v, *, pattern, mode, l, c, scale):
@@ -179,7 +207,7 @@ def backward_cols(q, k, v, dout, cols, *, pattern, mode, l, c, scale):
 def layout(n, block, l, c, pattern, mode):
     """Brute-force block layout: dict of numpy arrays (CSR rows + transpose)."""
     ng = np.zeros(1, dtype=np.int64)
-    nnz = np.zeros(2, dtype=np.int64)
+    nnz = np.zeros(max(2, num_layouts(l, c, pattern, mode)), dtype=np.int64)
     rc = lib().oracle_layout_count(n, block, l, c, pattern, mode, _ptr(ng), _ptr(nnz))
     if rc:
         raise ValueError(f"oracle_layout_count failed ({rc})")

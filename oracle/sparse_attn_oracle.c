@@ -33,7 +33,13 @@
  *   - fixed A2 keeps the summary columns of the query's own block when j <= i;
  *   - a row whose set is empty (fixed A2 alone, first block) has O = 0,
  *     LSE = -inf, and contributes no gradient;
- *   - a merged set is a set union: each j is counted once.
+ *   - a merged set is a set union: each j is counted once;
+ *   - distinct summary subblocks per head (Sec. 4.3, the remark closing the
+ *     fixed pattern: heads may look at different c-wide subblocks of each
+ *     l-block): pattern code 2.  The floor(l/c) subblocks are numbered from
+ *     the end of the block, subblock s holding the positions l-(s+1)c ..
+ *     l-sc-1 of every block, and head h takes s = h mod floor(l/c).  s = 0 is
+ *     the shared window of the plain fixed pattern.
  *
  * Inputs are read as fp64, fp32 or bf16 (raw 16-bit patterns), each converted
  * exactly to fp64.  Outputs are fp64.  Layout of every tensor: [b, h, n, d],
@@ -47,7 +53,7 @@
 #include <omp.h>
 #endif
 
-enum { O_STRIDED = 0, O_FIXED = 1 };
+enum { O_STRIDED = 0, O_FIXED = 1, O_FIXED_PER_HEAD = 2 };
 enum { O_MODE_A1 = 0, O_MODE_A2 = 1, O_MODE_MERGED = 2, O_MODE_INTERLEAVED = 3 };
 enum { O_PART_A1 = 0, O_PART_A2 = 1, O_PART_MERGED = 2 };
 enum { O_F64 = 0, O_F32 = 1, O_BF16 = 2 };
@@ -74,6 +80,14 @@ static int head_part(int mode, int64_t h) {
     }
 }
 
+/* First position, inside each l-block, of the c summary columns head h
+ * attends (Sec. 4.3): the last c positions, or with distinct subblocks per
+ * head subblock s = h mod floor(l/c), counted from the end of the block. */
+static int64_t summary_start(int pattern, int64_t l, int64_t c, int64_t h) {
+    if (pattern != O_FIXED_PER_HEAD) return l - c;
+    return l - (h % (l / c) + 1) * c;
+}
+
 static int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
 static int64_t imin(int64_t a, int64_t b) { return a < b ? a : b; }
 
@@ -86,12 +100,12 @@ static int64_t put_range(int64_t* out, int64_t cnt, int64_t lo, int64_t hi) {
     return cnt;
 }
 
-/* S_i for one part, ascending j, all within [0, i] (Sec. 4.3).  Returns |S_i|;
+/* S_i for one part, ascending j, all within [0, i] (Sec. 4.3); w is the
+ * first summary position inside a block (fixed pattern).  Returns |S_i|;
  * writes the members to out when out is not NULL. */
-int64_t oracle_row_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
-                       int64_t i, int64_t* out) {
+static int64_t row_set_w(int pattern, int part, int64_t l, int64_t c, int64_t w, int64_t i,
+                         int64_t* out) {
     int64_t cnt = 0;
-    (void)n;
     if (pattern == O_STRIDED) {
         int64_t t = imax(0, i - l); /* A1 = {t, ..., i} */
         if (part == O_PART_A1) return put_range(out, 0, t, i);
@@ -110,23 +124,25 @@ int64_t oracle_row_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
         }
         return put_range(out, cnt, t, i);
     }
-    /* fixed */
+    /* fixed: A1 is the query's own l-block up to i, A2 the columns at
+     * positions w .. w+c-1 of every block */
     int64_t blk = i / l;
     if (part == O_PART_A1) return put_range(out, 0, blk * l, i);
     if (part == O_PART_A2) {
-        /* columns whose position within their block is in {l-c, ..., l-1} */
         for (int64_t L = 0; L <= blk; ++L)
-            cnt = put_range(out, cnt, L * l + l - c, imin(L * l + l - 1, i));
+            cnt = put_range(out, cnt, L * l + w, imin(L * l + w + c - 1, i));
         return cnt;
     }
+    /* union: the summary columns of the earlier blocks, then all of A1 (the
+     * own block's summary columns up to i lie inside A1) */
     for (int64_t L = 0; L < blk; ++L)
-        cnt = put_range(out, cnt, L * l + l - c, L * l + l - 1);
+        cnt = put_range(out, cnt, L * l + w, L * l + w + c - 1);
     return put_range(out, cnt, blk * l, i);
 }
 
-/* T_j = {i : j in S_i}, ascending i, within [j, n-1].  Returns |T_j|. */
-int64_t oracle_col_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
-                       int64_t j, int64_t* out) {
+/* T_j = {i : j in S_i}, ascending i, within [j, n-1]. */
+static int64_t col_set_w(int pattern, int part, int64_t n, int64_t l, int64_t c, int64_t w,
+                         int64_t j, int64_t* out) {
     int64_t cnt = 0;
     if (pattern == O_STRIDED) {
         int64_t a1_hi = imin(n - 1, j + l); /* i - l <= j <= i */
@@ -145,11 +161,37 @@ int64_t oracle_col_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
         }
         return cnt;
     }
-    int summary = (j % l) >= (l - c);
+    int summary = (j % l) >= w && (j % l) < w + c;
     int64_t blk_hi = imin(n - 1, (j / l) * l + l - 1);
     if (part == O_PART_A1) return put_range(out, 0, j, blk_hi);
     if (part == O_PART_A2) return summary ? put_range(out, 0, j, n - 1) : 0;
     return put_range(out, 0, j, summary ? n - 1 : blk_hi);
+}
+
+/* S_i of one factor with the shared summary window (patterns 0 and 1; any
+ * other code is read as the fixed pattern). */
+int64_t oracle_row_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
+                       int64_t i, int64_t* out) {
+    (void)n;
+    return row_set_w(pattern, part, l, c, summary_start(O_FIXED, l, c, 0), i, out);
+}
+
+int64_t oracle_col_set(int pattern, int part, int64_t n, int64_t l, int64_t c,
+                       int64_t j, int64_t* out) {
+    return col_set_w(pattern, part, n, l, c, summary_start(O_FIXED, l, c, 0), j, out);
+}
+
+/* S_i and T_j of head h of a multi-head call: its factor (Sec. 5.1) and, for
+ * pattern 2, its own summary subblock. */
+int64_t oracle_head_row_set(int pattern, int mode, int64_t n, int64_t l, int64_t c, int64_t h,
+                            int64_t i, int64_t* out) {
+    (void)n;
+    return row_set_w(pattern, head_part(mode, h), l, c, summary_start(pattern, l, c, h), i, out);
+}
+
+int64_t oracle_head_col_set(int pattern, int mode, int64_t n, int64_t l, int64_t c, int64_t h,
+                            int64_t j, int64_t* out) {
+    return col_set_w(pattern, head_part(mode, h), n, l, c, summary_start(pattern, l, c, h), j, out);
 }
 
 /* ---------------------------------------------------------------------------
@@ -196,8 +238,7 @@ static double dot_dov(const problem* P, int64_t bh, int64_t i, int64_t j) {
  * jbuf and sbuf hold at least n entries.  Writes o[0..d) and *lse. */
 static void row_forward(const problem* P, int64_t bh, int64_t i, int64_t* jbuf,
                         double* sbuf, double* o, double* lse) {
-    int part = head_part(P->mode, bh % P->heads);
-    int64_t cnt = oracle_row_set(P->pattern, part, P->n, P->l, P->c, i, jbuf);
+    int64_t cnt = oracle_head_row_set(P->pattern, P->mode, P->n, P->l, P->c, bh % P->heads, i, jbuf);
     for (int64_t t = 0; t < P->d; ++t) o[t] = 0.0;
     if (cnt == 0) {
         *lse = -INFINITY;
@@ -230,8 +271,7 @@ static double row_delta(const problem* P, int64_t bh, int64_t i, const double* o
  * the saved LSE (Sec. 5.4). */
 static void row_dq(const problem* P, int64_t bh, int64_t i, int64_t* jbuf,
                    double lse, double delta, double* dq) {
-    int part = head_part(P->mode, bh % P->heads);
-    int64_t cnt = oracle_row_set(P->pattern, part, P->n, P->l, P->c, i, jbuf);
+    int64_t cnt = oracle_head_row_set(P->pattern, P->mode, P->n, P->l, P->c, bh % P->heads, i, jbuf);
     for (int64_t t = 0; t < P->d; ++t) dq[t] = 0.0;
     for (int64_t a = 0; a < cnt; ++a) {
         int64_t j = jbuf[a];
@@ -246,8 +286,7 @@ static void row_dq(const problem* P, int64_t bh, int64_t i, int64_t* jbuf,
 /* dk_j, dv_j by the column pass over T_j; lse[] and delta[] indexed by row. */
 static void col_dkdv(const problem* P, int64_t bh, int64_t j, int64_t* ibuf,
                      const double* lse, const double* delta, double* dk, double* dv) {
-    int part = head_part(P->mode, bh % P->heads);
-    int64_t cnt = oracle_col_set(P->pattern, part, P->n, P->l, P->c, j, ibuf);
+    int64_t cnt = oracle_head_col_set(P->pattern, P->mode, P->n, P->l, P->c, bh % P->heads, j, ibuf);
     for (int64_t t = 0; t < P->d; ++t) dk[t] = dv[t] = 0.0;
     for (int64_t a = 0; a < cnt; ++a) {
         int64_t i = ibuf[a];
@@ -263,9 +302,9 @@ static void col_dkdv(const problem* P, int64_t bh, int64_t j, int64_t* ibuf,
 
 static int check_problem(const problem* P) {
     if (P->n < 1 || P->l < 1 || P->d < 1 || P->heads < 1) return -1;
-    if (P->pattern != O_STRIDED && P->pattern != O_FIXED) return -1;
+    if (P->pattern < O_STRIDED || P->pattern > O_FIXED_PER_HEAD) return -1;
     if (P->mode < O_MODE_A1 || P->mode > O_MODE_INTERLEAVED) return -1;
-    if (P->pattern == O_FIXED && (P->c < 1 || P->c > P->l)) return -1;
+    if (P->pattern != O_STRIDED && (P->c < 1 || P->c > P->l)) return -1;
     if (P->dtype < O_F64 || P->dtype > O_BF16) return -1;
     return 0;
 }
@@ -442,14 +481,13 @@ int oracle_backward_cols(int pattern, int mode, int64_t n, int64_t l, int64_t c,
     int err = 0;
     for (int64_t r = 0; r < ncols && !err; ++r) {
         int64_t bh = cols[r] / n, j = cols[r] % n;
-        int part = head_part(P.mode, bh % P.heads);
         int64_t* ibuf = malloc(sizeof(int64_t) * n);
         double* lse = calloc((size_t)n, sizeof(double));
         double* delta = calloc((size_t)n, sizeof(double));
         if (!ibuf || !lse || !delta) {
             err = -2;
         } else {
-            int64_t cnt = oracle_col_set(P.pattern, part, n, l, c, j, ibuf);
+            int64_t cnt = oracle_head_col_set(P.pattern, P.mode, n, l, c, bh % P.heads, j, ibuf);
 #pragma omp parallel
             {
                 int64_t* jbuf = malloc(sizeof(int64_t) * n);
@@ -486,49 +524,69 @@ int oracle_backward_cols(int pattern, int mode, int64_t n, int64_t l, int64_t c,
  * for key tile j / B.  A tile is present iff its counter is positive, and is
  * FULL (kind 0) iff all B*B of its pairs are attended, else MASKED (kind 1).
  *
- * Layouts: one per call, except when heads alternate the two factors, where
- * layout 0 is A1 and layout 1 is A2.  Rows of all layouts are concatenated;
- * row_ptr[g*(nq+1) + qb] is an absolute offset into col_idx.  col_ptr /
- * row_idx / kind_t are the same tiles in column order.
+ * Layouts, one per distinct set of the heads of a call:
+ *   - shared summary window (patterns 0 and 1): one layout, except when heads
+ *     alternate the two factors, where layout 0 is A1 and layout 1 is A2;
+ *   - distinct subblocks (pattern 2), S = floor(l/c): A1 alone has one
+ *     layout (A1 has no summary columns); A2 or merged has S layouts, layout
+ *     s for subblock s (head h uses layout h mod S); alternating heads have
+ *     1 + S, layout 0 for A1 and layout 1 + s for A2 with subblock s (odd
+ *     head h uses layout 1 + h mod S).
+ * Rows of all layouts are concatenated; row_ptr[g*(nq+1) + qb] is an
+ * absolute offset into col_idx.  col_ptr / row_idx / kind_t are the same
+ * tiles in column order.
  * ------------------------------------------------------------------------- */
-static int layout_parts(int mode, int* parts) {
+int oracle_num_layouts(int64_t l, int64_t c, int pattern, int mode) {
+    if (pattern != O_FIXED_PER_HEAD || mode == O_MODE_A1)
+        return mode == O_MODE_INTERLEAVED ? 2 : 1;
+    int64_t S = l / c;
+    return (int)(mode == O_MODE_INTERLEAVED ? 1 + S : S);
+}
+
+/* Factor and summary window start of layout g. */
+static void layout_set(int64_t l, int64_t c, int pattern, int mode, int g, int* part, int64_t* w) {
+    int s = 0;
     if (mode == O_MODE_INTERLEAVED) {
-        parts[0] = O_PART_A1;
-        parts[1] = O_PART_A2;
-        return 2;
+        *part = g == 0 ? O_PART_A1 : O_PART_A2;
+        s = g == 0 ? 0 : g - 1;
+    } else {
+        *part = head_part(mode, 0);
+        s = g;
     }
-    parts[0] = head_part(mode, 0);
-    return 1;
+    *w = pattern == O_FIXED_PER_HEAD ? l - (s + 1) * c : l - c;
 }
 
 static int check_layout_args(int64_t n, int64_t B, int64_t l, int64_t c, int pattern, int mode) {
     if (n < 1 || B < 1 || n % B != 0 || l < 1) return -1;
-    if (pattern != O_STRIDED && pattern != O_FIXED) return -1;
+    if (pattern < O_STRIDED || pattern > O_FIXED_PER_HEAD) return -1;
     if (mode < O_MODE_A1 || mode > O_MODE_INTERLEAVED) return -1;
-    if (pattern == O_FIXED && (c < 1 || c > l)) return -1;
+    if (pattern != O_STRIDED && (c < 1 || c > l)) return -1;
     return 0;
 }
 
 /* Count attended pairs of query tile qb per key tile into cnt[0..nq). */
-static void tile_row_counts(int pattern, int part, int64_t n, int64_t B, int64_t l, int64_t c,
-                            int64_t qb, int64_t* cnt, int64_t* jbuf) {
+static void tile_row_counts(int pattern, int part, int64_t w, int64_t n, int64_t B, int64_t l,
+                            int64_t c, int64_t qb, int64_t* cnt, int64_t* jbuf) {
     int64_t nq = n / B;
     for (int64_t kb = 0; kb < nq; ++kb) cnt[kb] = 0;
     for (int64_t i = qb * B; i < qb * B + B; ++i) {
-        int64_t m = oracle_row_set(pattern, part, n, l, c, i, jbuf);
+        int64_t m = row_set_w(pattern, part, l, c, w, i, jbuf);
         for (int64_t a = 0; a < m; ++a) cnt[jbuf[a] / B] += 1;
     }
 }
 
-/* n_layouts and nnz per layout (nnz[1] = 0 when there is one layout). */
+/* n_layouts and nnz per layout; nnz holds max(2, oracle_num_layouts(...))
+ * entries (unused ones are set to 0). */
 int oracle_layout_count(int64_t n, int64_t B, int64_t l, int64_t c, int pattern, int mode,
                         int64_t* n_layouts, int64_t* nnz) {
     if (check_layout_args(n, B, l, c, pattern, mode)) return -1;
-    int parts[2];
-    int ng = layout_parts(mode, parts);
+    int ng = oracle_num_layouts(l, c, pattern, mode);
     int64_t nq = n / B;
     nnz[0] = nnz[1] = 0;
     for (int g = 0; g < ng; ++g) {
+        int part;
+        int64_t w;
+        layout_set(l, c, pattern, mode, g, &part, &w);
         int64_t total = 0;
 #pragma omp parallel
         {
@@ -536,7 +594,7 @@ int oracle_layout_count(int64_t n, int64_t B, int64_t l, int64_t c, int pattern,
             int64_t* jbuf = malloc(sizeof(int64_t) * n);
 #pragma omp for schedule(dynamic, 1) reduction(+ : total)
             for (int64_t qb = 0; qb < nq; ++qb) {
-                tile_row_counts(pattern, parts[g], n, B, l, c, qb, cnt, jbuf);
+                tile_row_counts(pattern, part, w, n, B, l, c, qb, cnt, jbuf);
                 for (int64_t kb = 0; kb < nq; ++kb) total += cnt[kb] > 0;
             }
             free(cnt);
@@ -552,11 +610,13 @@ int oracle_layout_fill(int64_t n, int64_t B, int64_t l, int64_t c, int pattern, 
                        int32_t* row_ptr, int32_t* col_idx, uint8_t* kind, int32_t* col_ptr,
                        int32_t* row_idx, uint8_t* kind_t) {
     if (check_layout_args(n, B, l, c, pattern, mode)) return -1;
-    int parts[2];
-    int ng = layout_parts(mode, parts);
+    int ng = oracle_num_layouts(l, c, pattern, mode);
     int64_t nq = n / B;
     int64_t base = 0;
     for (int g = 0; g < ng; ++g) {
+        int part;
+        int64_t w;
+        layout_set(l, c, pattern, mode, g, &part, &w);
         int32_t* rp = row_ptr + g * (nq + 1);
         int32_t* cp = col_ptr + g * (nq + 1);
         /* pass 1: tiles per query tile */
@@ -567,7 +627,7 @@ int oracle_layout_fill(int64_t n, int64_t B, int64_t l, int64_t c, int pattern, 
             int64_t* jbuf = malloc(sizeof(int64_t) * n);
 #pragma omp for schedule(dynamic, 1)
             for (int64_t qb = 0; qb < nq; ++qb) {
-                tile_row_counts(pattern, parts[g], n, B, l, c, qb, cnt, jbuf);
+                tile_row_counts(pattern, part, w, n, B, l, c, qb, cnt, jbuf);
                 int64_t m = 0;
                 for (int64_t kb = 0; kb < nq; ++kb) m += cnt[kb] > 0;
                 rowcnt[qb] = m;
@@ -585,7 +645,7 @@ int oracle_layout_fill(int64_t n, int64_t B, int64_t l, int64_t c, int pattern, 
             int64_t* jbuf = malloc(sizeof(int64_t) * n);
 #pragma omp for schedule(dynamic, 1)
             for (int64_t qb = 0; qb < nq; ++qb) {
-                tile_row_counts(pattern, parts[g], n, B, l, c, qb, cnt, jbuf);
+                tile_row_counts(pattern, part, w, n, B, l, c, qb, cnt, jbuf);
                 int64_t e = rp[qb];
                 for (int64_t kb = 0; kb < nq; ++kb) {
                     if (cnt[kb] == 0) continue;

@@ -138,3 +138,27 @@ def test_strided_a1_a2_counts_closed_form(orc):
     nq = n // B
     np.testing.assert_array_equal(np.diff(a1["row_ptr"]), [1] + [2] * (nq - 1))
     np.testing.assert_array_equal(np.diff(a2["row_ptr"]), np.arange(1, nq + 1))
+
+
+FIXED_PER_HEAD = 2
+PER_HEAD_LAYOUT_SHAPES = [  # (n, B, l, c)
+    (256, 16, 32, 8), (256, 64, 128, 32), (240, 16, 20, 6), (192, 32, 24, 5), (128, 16, 16, 16), (384, 64, 256, 32),
+]
+
+
+@pytest.mark.parametrize("n,B,l,c", PER_HEAD_LAYOUT_SHAPES)
+@pytest.mark.parametrize("mode", [A1, A2, MERGED, INTERLEAVED])
+def test_per_head_layouts_equal_tiles_of_definition(orc, n, B, l, c, mode):
+    """One layout per distinct head set: A2 / merged layout s holds subblock
+    s; alternating heads have layout 0 for A1 and 1 + s for A2 with
+    subblock s; A1 alone has one."""
+    S = l // c
+    lay = orc.layout(n, B, l, c, FIXED_PER_HEAD, mode)
+    if mode == A1:
+        masks = [dense.part_mask(FIXED, A1, n, l, c)]
+    elif mode == INTERLEAVED:
+        masks = [dense.part_mask(FIXED, A1, n, l, c)] + [dense.part_mask(FIXED, A2, n, l, c, s) for s in range(S)]
+    else:
+        masks = [dense.part_mask(FIXED, mode, n, l, c, s) for s in range(S)]
+    assert lay["n_layouts"] == len(masks)
+    check_layout_against_mask(lay, masks, B)

@@ -20,8 +20,9 @@ MUTANTS = {
     "lse_sign": ("*lse = m + log(z);", "*lse = m - log(z);"),
     "max_added": ("z += exp(sbuf[a] - m);", "z += exp(sbuf[a] + m);"),
     "strided_a1_bound": ("int64_t t = imax(0, i - l); /* A1", "int64_t t = imax(0, i - l + 1); /* A1"),
-    "fixed_a2_first_column": ("cnt = put_range(out, cnt, L * l + l - c, imin(L * l + l - 1, i));",
-                              "cnt = put_range(out, cnt, L * l + l - c - 1, imin(L * l + l - 1, i));"),
+    "fixed_a2_first_column": ("cnt = put_range(out, cnt, L * l + w, imin(L * l + w + c - 1, i));",
+                              "cnt = put_range(out, cnt, L * l + w - 1, imin(L * l + w + c - 1, i));"),
+    "fixed_shared_window": ("if (pattern != O_FIXED_PER_HEAD) return l - c;", "if (pattern != O_FIXED_PER_HEAD) return l - c - 1;"),
     "fixed_own_block_summary_dropped": ("for (int64_t L = 0; L <= blk; ++L)", "for (int64_t L = 0; L < blk; ++L)"),
     "qk_row_swapped": ("int64_t qi = row_base(P, bh, i), kj = row_base(P, bh, j);",
                        "int64_t qi = row_base(P, bh, j), kj = row_base(P, bh, i);"),
@@ -33,6 +34,9 @@ MUTANTS = {
     "interleave_swapped": ("return (h % 2 == 0) ? O_PART_A1 : O_PART_A2;", "return (h % 2 == 0) ? O_PART_A2 : O_PART_A1;"),
     "empty_row_lse": ("*lse = -INFINITY;", "*lse = 0.0;"),
     "tile_kind_threshold": ("kind[e] = (uint8_t)(cnt[kb] == B * B ? 0 : 1);", "kind[e] = (uint8_t)(cnt[kb] >= B ? 0 : 1);"),
+    "per_head_subblock_order": ("return l - (h % (l / c) + 1) * c;", "return (h % (l / c)) * c;"),
+    "per_head_window_upper_dropped": ("int summary = (j % l) >= w && (j % l) < w + c;", "int summary = (j % l) >= w;"),
+    "per_head_layout_shift": ("s = g == 0 ? 0 : g - 1;", "s = g;"),
     "transpose_row_index": ("row_idx[pos] = (int32_t)qb;", "row_idx[pos] = (int32_t)col_idx[e];"),
 }
 

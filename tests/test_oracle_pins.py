@@ -325,3 +325,109 @@ def test_bf16_inputs_are_read_exactly(orc):
     o_64, lse_64 = orc.forward(as64, as64, as64, **kw)
     np.testing.assert_array_equal(o_bits, o_64)
     np.testing.assert_array_equal(lse_bits, lse_64)
+
+
+# ---------------------------------------------------------------------------
+# Distinct summary subblocks per head (pattern 2, Sec. 4.3 closing remark)
+# ---------------------------------------------------------------------------
+FIXED_PER_HEAD = 2
+PER_HEAD_SHAPES = [(64, 8, 2), (96, 16, 4), (100, 12, 5), (48, 48, 48), (40, 64, 5), (64, 8, 1)]
+
+
+def test_per_head_worked_example(orc):
+    ex = json.load(open(os.path.join(GOLDEN, "fixed_per_head_l8_c2_example.json")))
+    l, c = ex["l"], ex["c"]
+    n = 4 * l
+    for h, cols in ex["windows"].items():
+        h = int(h)
+        # the window shows in A2 of the last row as the first block's members
+        s = orc.head_row_set(FIXED_PER_HEAD, A2, n, l, c, h, n - 1)
+        np.testing.assert_array_equal(s[s < l], cols)
+    for case in ex["a2_rows"]:
+        np.testing.assert_array_equal(orc.head_row_set(FIXED_PER_HEAD, A2, n, l, c, case["head"], case["row"]),
+                                      case["set"])
+    for case in ex["merged_rows"]:
+        np.testing.assert_array_equal(orc.head_row_set(FIXED_PER_HEAD, MERGED, n, l, c, case["head"], case["row"]),
+                                      case["set"])
+
+
+@pytest.mark.parametrize("mode", [A1, A2, MERGED, INTERLEAVED])
+@pytest.mark.parametrize("n,l,c", PER_HEAD_SHAPES)
+def test_per_head_sets_equal_predicate_and_transpose(orc, mode, n, l, c):
+    for h in range(l // c + 2):
+        mask = dense.head_mask(FIXED_PER_HEAD, mode, h, n, l, c)
+        for i in range(n):
+            np.testing.assert_array_equal(orc.head_row_set(FIXED_PER_HEAD, mode, n, l, c, h, i), np.nonzero(mask[i])[0])
+        for j in range(n):
+            np.testing.assert_array_equal(orc.head_col_set(FIXED_PER_HEAD, mode, n, l, c, h, j),
+                                          np.nonzero(mask[:, j])[0])
+
+
+@pytest.mark.parametrize("n,l,c", [(96, 16, 4), (64, 8, 2), (90, 9, 3), (64, 8, 8)])
+def test_per_head_windows_partition_earlier_blocks(orc, n, l, c):
+    """With c | l the l/c heads' windows tile each block: over heads 0 .. l/c - 1,
+    every position of an earlier block is in exactly one head's A2, and head 0
+    (and every head h = 0 mod l/c) has the plain fixed pattern's set."""
+    S = l // c
+    for i in range(n):
+        blk0 = (i // l) * l
+        hits = np.zeros(blk0, dtype=np.int64)
+        for h in range(S):
+            s = orc.head_row_set(FIXED_PER_HEAD, A2, n, l, c, h, i)
+            hits[s[s < blk0]] += 1
+        np.testing.assert_array_equal(hits, 1)
+        for h in (0, S, 2 * S):
+            for part in (A2, MERGED):
+                np.testing.assert_array_equal(orc.head_row_set(FIXED_PER_HEAD, part, n, l, c, h, i),
+                                              orc.row_set(FIXED, part, n, l, c, i))
+
+
+@pytest.mark.parametrize("n,l,c", [(256, 16, 4), (250, 32, 8), (192, 12, 4)])
+def test_per_head_two_step_reachability(orc, n, l, c):
+    """Validity (Sec. 4.2) across the heads: with A2 the union of the heads'
+    windows (they tile the block when c | l), every j <= i reaches i in two
+    steps.  One head alone is valid only for subblock 0: positions of an
+    earlier block after its window reach no later block through A2."""
+    S = l // c
+
+    def masks(h):
+        m1 = np.zeros((n, n), dtype=np.int64)
+        m2 = np.zeros((n, n), dtype=np.int64)
+        for i in range(n):
+            m1[i, orc.head_row_set(FIXED_PER_HEAD, A1, n, l, c, h, i)] = 1
+            m2[i, orc.head_row_set(FIXED_PER_HEAD, A2, n, l, c, h, i)] = 1
+        return m1, m2
+
+    tril = np.tril(np.ones((n, n), dtype=bool))
+    m1, m2u = masks(0)
+    np.testing.assert_array_equal((m1 + m2u @ m1) > 0, tril)
+    for h in range(1, S):
+        m1h, m2 = masks(h)
+        np.testing.assert_array_equal(m1h, m1)
+        assert not np.array_equal((m1 + m2 @ m1) > 0, tril)
+        m2u = m2u + m2
+    np.testing.assert_array_equal((m1 + m2u @ m1) > 0, tril)
+
+
+@pytest.mark.parametrize("mode,n,l,c", [(A2, 128, 16, 4), (MERGED, 192, 32, 8), (INTERLEAVED, 160, 16, 4)])
+def test_per_head_oracle_matches_dense_numpy(orc, mode, n, l, c):
+    b, h, d = 1, 5, 16
+    scale = d ** -0.5
+    q, k, v, dout = (_np(x) for x in _inputs(b, h, n, d, seed=47))
+    res = orc.backward(q, k, v, dout, pattern=FIXED_PER_HEAD, mode=mode, l=l, c=c, scale=scale)
+    for hh in range(h):
+        mask = dense.head_mask(FIXED_PER_HEAD, mode, hh, n, l, c)
+        o, lse, dq, dk, dv = dense.attention_grads(q[0, hh], k[0, hh], v[0, hh], dout[0, hh], mask, scale)
+        np.testing.assert_allclose(res["o"][0, hh], o, atol=1e-12, rtol=0)
+        np.testing.assert_array_equal(np.isneginf(res["lse"][0, hh]), np.isneginf(lse))
+        fin = np.isfinite(lse)
+        np.testing.assert_allclose(res["lse"][0, hh][fin], lse[fin], atol=1e-12, rtol=0)
+        for name, ref in (("dq", dq), ("dk", dk), ("dv", dv)):
+            np.testing.assert_allclose(res[name][0, hh], ref, atol=1e-11, rtol=0, err_msg=name)
+    idx = np.array([[0, hh, i] for hh in range(h) for i in (0, 3, n // 2 + 1, n - 1)])
+    o_r, _ = orc.forward_rows(q, k, v, idx, pattern=FIXED_PER_HEAD, mode=mode, l=l, c=c, scale=scale)
+    dk_c, dv_c = orc.backward_cols(q, k, v, dout, idx, pattern=FIXED_PER_HEAD, mode=mode, l=l, c=c, scale=scale)
+    sel = (idx[:, 0], idx[:, 1], idx[:, 2])
+    np.testing.assert_allclose(o_r, res["o"][sel], atol=1e-13, rtol=0)
+    np.testing.assert_allclose(dk_c, res["dk"][sel], atol=1e-13, rtol=0)
+    np.testing.assert_allclose(dv_c, res["dv"][sel], atol=1e-13, rtol=0)
