@@ -17,6 +17,11 @@
  *   strided A2 = { j <= i : (i - j) mod l == 0 }
  *   fixed   A1 = { j <= i : floor(j / l) == floor(i / l) }
  *   fixed   A2 = { j <= i : j mod l >= l - c }             (1 <= c <= l)
+ * and, with a distinct summary subblock per head (Sec. 4.3, closing remark on
+ * the fixed pattern: heads may look at different c-wide subblocks of each
+ * l-block), for head h with s = h mod floor(l / c):
+ *   fixed-per-head A2 = { j <= i : l-(s+1)c <= j mod l < l-sc }
+ * (s = 0 is the plain fixed pattern).
  * A row whose set is empty (fixed A2 alone, first block) yields O_i = 0,
  * LSE_i = -inf and no gradient.
  *
@@ -56,8 +61,10 @@ typedef enum {
     SA_ERR_HIP = -4               /* the HIP runtime reported an error */
 } sa_status;
 
-/* Connectivity pattern, Sec. 4.3. */
-typedef enum { SA_STRIDED = 0, SA_FIXED = 1 } sa_pattern;
+/* Connectivity pattern, Sec. 4.3.  SA_FIXED_PER_HEAD is the fixed pattern
+ * with a distinct summary subblock per head (see above); it needs
+ * floor(l / c) <= 64, else SA_ERR_UNSUPPORTED. */
+typedef enum { SA_STRIDED = 0, SA_FIXED = 1, SA_FIXED_PER_HEAD = 2 } sa_pattern;
 
 /* Head combination, Sec. 5.1:
  *   SA_MODE_A1 / SA_MODE_A2: one factor for the whole call (eq. sepwpmat: a
@@ -83,18 +90,32 @@ enum { SA_TILE_FULL = 0, SA_TILE_MASKED = 1 };
  *   n          sequence length, 1 <= n < 2^31, a multiple of `block`
  *   block      tile edge B in {16, 32, 64}
  *   stride_l   l >= 1 (Sec. 4.3); any l >= n makes A1 dense causal
- *   summary_c  c: 1 <= c <= l for SA_FIXED, must be 0 for SA_STRIDED
+ *   summary_c  c: 1 <= c <= l for SA_FIXED and SA_FIXED_PER_HEAD, must be 0
+ *              for SA_STRIDED
  *   pattern    sa_pattern
  *   head_mode  sa_head_mode
  */
 
 /*
+ * Number of block layouts of a call (host only, no device work): one per
+ * distinct set of its heads.
+ *   SA_STRIDED, SA_FIXED: 2 for SA_MODE_INTERLEAVED (layout 0 holds A1,
+ *       layout 1 holds A2), else 1.
+ *   SA_FIXED_PER_HEAD, S = floor(l / c): SA_MODE_A1 1; SA_MODE_A2 and
+ *       SA_MODE_MERGED S, layout s for subblock s (head h reads layout
+ *       h mod S); SA_MODE_INTERLEAVED 1 + S, layout 0 for A1 and 1 + s for A2
+ *       with subblock s (odd head h reads layout 1 + h mod S).
+ */
+int sparse_attn_layout_count(int32_t stride_l, int32_t summary_c, int32_t pattern, int32_t head_mode,
+                             int32_t* n_layouts);
+
+/*
  * Size query for the block layout (host only, synchronous, no device work).
  * Sec. 5.5: the product is computed over B x B blocks; a block (qb, kb) with
  * kb <= qb is present when any pair (i, j) in it is attended.
- * Outputs: *n_layouts = 2 for SA_MODE_INTERLEAVED (layout 0 holds A1, layout
- * 1 holds A2), else 1; nnz[0..1] = present blocks per layout (nnz[1] = 0 when
- * there is one layout).  Each layout needs nq + 1 row and column pointers,
+ * Outputs: *n_layouts as sparse_attn_layout_count gives it; nnz[g] = present
+ * blocks of layout g.  nnz must hold max(2, n_layouts) entries (entries past
+ * n_layouts are set to 0).  Each layout needs nq + 1 row and column pointers,
  * nq = n / block.
  */
 int sparse_attn_layout_size(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,

@@ -10,30 +10,53 @@ namespace {
 
 using sa::Pattern;
 
+// Summary subblocks per l-block that heads can be spread over; beyond this the
+// per-subblock layouts would outgrow any useful head count.
+constexpr int kMaxSubblocks = 64;
+
 struct PatternArgs {
     int64_t n;
-    int32_t block, l, c, pattern, mode;
+    int32_t block, l, c;
+    int32_t pattern;  // STRIDED or FIXED (SA_FIXED_PER_HEAD is FIXED with sub > 0)
+    int32_t mode;
+    int32_t sub;      // summary subblocks, 0 = one window for all heads
     int64_t nq;
     int n_layouts;
 };
+
+// Pattern, stride and summary width (shared by the block and decoding entry
+// points): internal pattern and subblock count.
+int check_pattern_code(int32_t l, int32_t c, int32_t pattern, int32_t mode, int32_t* internal, int32_t* sub) {
+    if (l < 1) return SA_ERR_INVALID;
+    if (pattern != SA_STRIDED && pattern != SA_FIXED && pattern != SA_FIXED_PER_HEAD) return SA_ERR_INVALID;
+    if (mode < SA_MODE_A1 || mode > SA_MODE_INTERLEAVED) return SA_ERR_INVALID;
+    if (pattern != SA_STRIDED && (c < 1 || c > l)) return SA_ERR_INVALID;
+    if (pattern == SA_STRIDED && c != 0) return SA_ERR_INVALID;
+    *internal = pattern == SA_STRIDED ? sa::STRIDED : sa::FIXED;
+    *sub = 0;
+    if (pattern == SA_FIXED_PER_HEAD) {
+        if (l / c > kMaxSubblocks) return SA_ERR_UNSUPPORTED;
+        *sub = l / c;
+    }
+    return SA_OK;
+}
 
 int check_pattern(int64_t n, int32_t block, int32_t l, int32_t c, int32_t pattern, int32_t mode,
                   PatternArgs* out) {
     if (block != 16 && block != 32 && block != 64) return SA_ERR_INVALID;
     if (n < 1 || n > INT32_MAX || n % block != 0) return SA_ERR_INVALID;
-    if (l < 1) return SA_ERR_INVALID;
-    if (pattern != SA_STRIDED && pattern != SA_FIXED) return SA_ERR_INVALID;
-    if (mode < SA_MODE_A1 || mode > SA_MODE_INTERLEAVED) return SA_ERR_INVALID;
-    if (pattern == SA_FIXED && (c < 1 || c > l)) return SA_ERR_INVALID;
-    if (pattern == SA_STRIDED && c != 0) return SA_ERR_INVALID;
+    int32_t internal = 0, sub = 0;
+    const int st = check_pattern_code(l, c, pattern, mode, &internal, &sub);
+    if (st != SA_OK) return st;
     out->n = n;
     out->block = block;
     out->l = l;
     out->c = c;
-    out->pattern = pattern;
+    out->pattern = internal;
     out->mode = mode;
+    out->sub = sub;
     out->nq = n / block;
-    out->n_layouts = mode == SA_MODE_INTERLEAVED ? 2 : 1;
+    out->n_layouts = sa::layout_count(mode, sub);
     return SA_OK;
 }
 
@@ -43,6 +66,7 @@ Pattern pattern_of_layout(const PatternArgs& p, int g) {
     s.part = sa::part_of_layout(p.mode, g);
     s.l = p.l;
     s.c = p.c;
+    s.w = sa::summary_start(p.l, p.c, sa::subblock_of_layout(p.mode, p.sub, g));
     return s;
 }
 
@@ -85,7 +109,8 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.scale = scale;
     a.scale_log2 = scale * sa::kLog2eHost;
     a.period_bits = sa::host_period_bits(p.l);
-    sa::host_summary_pattern(p.l, p.c, &a.sum_lo, &a.sum_hi);
+    sa::summary_words(p.l, p.c, p.l - p.c, &a.sum_lo, &a.sum_hi);
+    a.sub = p.sub;
     a.dl = sa::make_divl(p.l);
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;
@@ -97,13 +122,10 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
 }
 
 // Pattern arguments of a decoding step (no block size: S_pos is enumerated).
-int check_decode_pattern(int64_t pos, int32_t l, int32_t c, int32_t pattern, int32_t mode) {
-    if (pos < 0 || pos > INT32_MAX || l < 1) return SA_ERR_INVALID;
-    if (pattern != SA_STRIDED && pattern != SA_FIXED) return SA_ERR_INVALID;
-    if (mode < SA_MODE_A1 || mode > SA_MODE_INTERLEAVED) return SA_ERR_INVALID;
-    if (pattern == SA_FIXED && (c < 1 || c > l)) return SA_ERR_INVALID;
-    if (pattern == SA_STRIDED && c != 0) return SA_ERR_INVALID;
-    return SA_OK;
+int check_decode_pattern(int64_t pos, int32_t l, int32_t c, int32_t pattern, int32_t mode, int32_t* internal,
+                         int32_t* sub) {
+    if (pos < 0 || pos > INT32_MAX) return SA_ERR_INVALID;
+    return check_pattern_code(l, c, pattern, mode, internal, sub);
 }
 int check_decode_shape(int32_t batch, int32_t heads, int32_t d, int32_t dtype) {
     if (batch < 1 || heads < 1 || (int64_t)batch * heads > INT32_MAX / 2) return SA_ERR_INVALID;
@@ -123,12 +145,26 @@ int sparse_attn_layout_size(int64_t n, int32_t block, int32_t stride_l, int32_t 
     int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
     if (st != SA_OK) return st;
     if (!n_layouts || !nnz) return SA_ERR_INVALID;
-    int64_t counts[2] = {0, 0};
-    for (int g = 0; g < p.n_layouts; ++g) counts[g] = sa::layout_count_host(pattern_of_layout(p, g), n, block);
-    if (counts[0] + counts[1] > INT32_MAX) return SA_ERR_UNSUPPORTED;  // int32 layout indices
+    int64_t counts[1 + kMaxSubblocks] = {0};
+    int64_t total = 0;
+    for (int g = 0; g < p.n_layouts; ++g) {
+        counts[g] = sa::layout_count_host(pattern_of_layout(p, g), n, block);
+        total += counts[g];
+    }
+    if (total > INT32_MAX) return SA_ERR_UNSUPPORTED;  // int32 layout indices
     *n_layouts = p.n_layouts;
-    nnz[0] = counts[0];
-    nnz[1] = counts[1];
+    const int entries = p.n_layouts > 2 ? p.n_layouts : 2;
+    for (int g = 0; g < entries; ++g) nnz[g] = counts[g];
+    return SA_OK;
+}
+
+int sparse_attn_layout_count(int32_t stride_l, int32_t summary_c, int32_t pattern, int32_t head_mode,
+                             int32_t* n_layouts) {
+    int32_t internal = 0, sub = 0;
+    const int st = check_pattern_code(stride_l, summary_c, pattern, head_mode, &internal, &sub);
+    if (st != SA_OK) return st;
+    if (!n_layouts) return SA_ERR_INVALID;
+    *n_layouts = sa::layout_count(head_mode, sub);
     return SA_OK;
 }
 
@@ -144,7 +180,7 @@ int sparse_attn_layout(int64_t n, int32_t block, int32_t stride_l, int32_t summa
     for (int g = 0; g < p.n_layouts; ++g) total += sa::layout_count_host(pattern_of_layout(p, g), n, block);
     if (total > INT32_MAX) return SA_ERR_UNSUPPORTED;
     if (capacity < total) return SA_ERR_BUFFER_TOO_SMALL;
-    hipError_t e = sa::layout_launch(n, block, pattern, head_mode, stride_l, summary_c, p.n_layouts,
+    hipError_t e = sa::layout_launch(n, block, p.pattern, head_mode, p.sub, stride_l, summary_c, p.n_layouts,
                                      row_ptr, col_idx, kind, col_ptr, row_idx, kind_t,
                                      static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
@@ -216,12 +252,14 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
 int sparse_attn_decode_workspace_size(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t pattern,
                                       int32_t head_mode, int32_t batch, int32_t heads, int32_t d_head,
                                       int32_t dtype, size_t* bytes) {
-    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode);
+    int32_t internal = 0, sub = 0;
+    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode, &internal, &sub);
     if (st != SA_OK) return st;
     st = check_decode_shape(batch, heads, d_head, dtype);
     if (st != SA_OK) return st;
     if (!bytes) return SA_ERR_INVALID;
-    *bytes = sa::decode_workspace_bytes(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head);
+    *bytes = sa::decode_workspace_bytes(internal, head_mode, sub, (int32_t)pos, stride_l, summary_c, batch, heads,
+                                        d_head);
     return SA_OK;
 }
 
@@ -230,7 +268,8 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
                        const int64_t* q_strides, const void* k_cache, const void* v_cache,
                        const int64_t* kv_strides, float softmax_scale, void* o, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream) {
-    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode);
+    int32_t internal = 0, sub = 0;
+    int st = check_decode_pattern(pos, stride_l, summary_c, pattern, head_mode, &internal, &sub);
     if (st != SA_OK) return st;
     st = check_decode_shape(batch, heads, d_head, dtype);
     if (st != SA_OK) return st;
@@ -243,11 +282,11 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
         if (kv_strides[t] < 0 || kv_strides[t] % unit != 0) return SA_ERR_INVALID;
     if (kv_strides[2] < d_head) return SA_ERR_INVALID;
     if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
-    const size_t need =
-        sa::decode_workspace_bytes(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head);
+    const size_t need = sa::decode_workspace_bytes(internal, head_mode, sub, (int32_t)pos, stride_l, summary_c, batch,
+                                                   heads, d_head);
     if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
     if (!workspace || !aligned16(workspace)) return SA_ERR_INVALID;
-    hipError_t e = sa::decode_launch(pattern, head_mode, (int32_t)pos, stride_l, summary_c, batch, heads, d_head,
+    hipError_t e = sa::decode_launch(internal, head_mode, sub, (int32_t)pos, stride_l, summary_c, batch, heads, d_head,
                                      dtype, q, q_strides, k_cache, v_cache, kv_strides, softmax_scale, o, lse,
                                      workspace, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;

@@ -77,69 +77,69 @@ __device__ inline int64_t queue_heads(int64_t bh_count, int x) {
 constexpr int kItemShift = 29;
 __device__ inline int32_t item_code(int kb, int half) { return kb | (half << kItemShift); }
 
-// In the fixed pattern with B = 64, a key block whose upper 32 keys are
-// summary keys and whose lower 32 are not is split into its two halves: the
-// lower keys meet only the blocks of their own l-block, the upper keys every
-// block of the column.  Each half is then shared by all four waves (its two
-// 16-key groups times the two 32-query halves of a block), where the whole
-// block would leave the two waves of the lower keys idle on every block away
-// from the diagonal.
-__device__ inline bool split_column(const AttnArgs& a, int g, int kb) {
-    if (a.pattern != FIXED || a.block != 64) return false;
-    const MaskParams mp{a.pattern, part_of_layout(a.mode, g), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
-    return mp.part != PART_A1 && summary_bits(mp, mod_l(a.dl, 64 * kb)) == 0xFFFFFFFF00000000ull;
+// In the fixed pattern with B = 64, a key block half of whose keys (the
+// upper or the lower 32) are summary keys and the other half not is split
+// into its two halves: the other keys meet only the blocks of their own
+// l-block, the summary keys every block of the column.  Each half is then
+// shared by all four waves (its two 16-key groups times the two 32-query
+// halves of a block), where the whole block would leave the two waves of the
+// other keys idle on every block away from the diagonal.  Returns 0 (no
+// split), 1 (upper keys are the summary keys) or 2 (lower keys are).
+__device__ inline int split_column(const AttnArgs& a, int g, int kb) {
+    if (a.pattern != FIXED || a.block != 64) return 0;
+    const MaskParams mp = mask_params(a, a.pattern, part_of_layout(a.mode, g), subblock_of_layout(a.mode, a.sub, g));
+    if (mp.part == PART_A1) return 0;
+    const uint64_t bits = summary_bits(mp, mod_l(a.dl, 64 * kb));
+    return bits == 0xFFFFFFFF00000000ull ? 1 : (bits == 0x00000000FFFFFFFFull ? 2 : 0);
 }
 
-// Workgroup 0 of the pre kernel: empty queues; per layout the items (2 nq
-// slots) ordered by length class, empty slots last (order inside a class is
-// arbitrary; it only affects scheduling); and in queue[kQueues] the largest
-// item count of a layout.
-__device__ void build_schedule(const AttnArgs& a, unsigned long long* queue, int32_t* order) {
+// Workgroup g < n_layouts of the pre kernel: layout g's items (2 nq slots)
+// ordered by length class, empty slots last (order inside a class is
+// arbitrary; it only affects scheduling), and its item count in items[g].
+// Workgroup 0 also empties the queues.
+__device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* queue, int32_t* items_out,
+                               int32_t* order) {
     __shared__ int cls_pos[kLengthClasses];
     __shared__ int items;
     const int tid = threadIdx.x;
-    if (tid < kQueues) queue[tid] = 0ull;
-    const int n_layouts = a.mode == MODE_INTERLEAVED ? 2 : 1;
-    const int lower_cls = length_class(2);  // a lower half meets at most a few blocks
-    int max_items = 0;
-    for (int g = 0; g < n_layouts; ++g) {
-        const int32_t* cp = a.col_ptr + (int64_t)g * (a.nq + 1);
-        int32_t* ord = order + (int64_t)g * 2 * a.nq;
-        for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
-        __syncthreads();
-        for (int kb = tid; kb < a.nq; kb += blockDim.x) {
-            atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
-            if (split_column(a, g, kb)) atomicAdd(&cls_pos[lower_cls], 1);
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int run = 0;
-            for (int i = 0; i < kLengthClasses; ++i) {
-                const int c = cls_pos[i];
-                cls_pos[i] = run;
-                run += c;
-            }
-            items = run;
-        }
-        __syncthreads();
-        for (int kb = tid; kb < a.nq; kb += blockDim.x) {
-            const bool split = split_column(a, g, kb);
-            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, split ? 2 : 0);
-            if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 1);
-        }
-        for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
-        max_items = max_items > items ? max_items : items;
-        __syncthreads();
+    if (g == 0 && tid < kQueues) queue[tid] = 0ull;
+    const int lower_cls = length_class(2);  // a half of non-summary keys meets at most a few blocks
+    const int32_t* cp = a.col_ptr + (int64_t)g * (a.nq + 1);
+    int32_t* ord = order + (int64_t)g * 2 * a.nq;
+    for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
+    __syncthreads();
+    for (int kb = tid; kb < a.nq; kb += blockDim.x) {
+        atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+        if (split_column(a, g, kb)) atomicAdd(&cls_pos[lower_cls], 1);
     }
-    if (tid == 0) queue[kQueues] = (unsigned long long)max_items;
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int i = 0; i < kLengthClasses; ++i) {
+            const int c = cls_pos[i];
+            cls_pos[i] = run;
+            run += c;
+        }
+        items = run;
+    }
+    __syncthreads();
+    for (int kb = tid; kb < a.nq; kb += blockDim.x) {
+        const int split = split_column(a, g, kb);
+        // the summary half takes the column's class, the other half the short one
+        ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] =
+            item_code(kb, split == 0 ? 0 : (split == 1 ? 2 : 1));
+        if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, split == 1 ? 1 : 2);
+    }
+    for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
+    if (tid == 0) items_out[g] = items;
 }
 
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
 bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, const float* __restrict__ lse,
                float* __restrict__ ndelta, float* __restrict__ nlse2, unsigned long long* __restrict__ queue,
-               int32_t* __restrict__ order) {
-    if (blockIdx.x == 0 && queue) build_schedule(a, queue, order);
+               int32_t* __restrict__ items, int32_t* __restrict__ order) {
+    if (queue && (int)blockIdx.x < layout_count(a.mode, a.sub)) build_schedule(a, blockIdx.x, queue, items, order);
     const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     if (row >= rows) return;
@@ -202,8 +202,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
+    const int lay = head_layout(a, h);
+    const MaskParams mp = head_mask_params(a, PAT, MODE, h);
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
@@ -237,7 +237,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
-    // A step stages one block, or two upper halves (see RowStepper) as one tile
+    // A step stages one block, or two summary halves (see RowStepper) as one tile
     constexpr bool kPairs = PAT == FIXED && BLK == 64;
     auto load_step = [&](RowStep s, int stage) {
         const uint32_t kdst = sK_base + stage * kTileBytes, vdst = sV_base + stage * kTileBytes;
@@ -246,7 +246,11 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             ld.issue(k + kbase, kdst);
             ld.issue(v + kbase, vdst);
         } else if constexpr (kPairs) {
-            const int64_t lo = base + ((int64_t)s.a * BLK + BLK / 2) * a.ss, hi = base + (int64_t)s.b * BLK * a.ss;
+            // the summary halves: upper (window at 32 mod 64) or lower (at 0 mod
+            // 64); issue_halves takes tile rows 0..31 from lo and 32..63 from hi
+            const int half_off = (mp.w & 63) == 0 ? 0 : BLK / 2;
+            const int64_t lo = base + ((int64_t)s.a * BLK + half_off) * a.ss;
+            const int64_t hi = base + ((int64_t)s.b * BLK - (BLK / 2 - half_off)) * a.ss;
             ld.issue_halves(k + lo, k + hi, kdst);
             ld.issue_halves(v + lo, v + hi, vdst);
         }
@@ -264,9 +268,9 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         const RowStep nxt = steps.next();
         const int kb = cur.a;
         const int j0 = kb * BLK;
-        // a pair of upper halves is attended everywhere
+        // a pair of summary halves is attended everywhere
         const bool masked =
-            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // this step is in LDS everywhere; the other stage is free
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
@@ -454,7 +458,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
                      const float* __restrict__ nlse2, const float* __restrict__ ndelta,
                      uint16_t* __restrict__ dk, uint16_t* __restrict__ dv,
-                     unsigned long long* __restrict__ queue, const int32_t* __restrict__ order) {
+                     unsigned long long* __restrict__ queue, const int32_t* __restrict__ items,
+                     const int32_t* __restrict__ order) {
     using C = DkvCfg<D, BLK, PAT>;
     constexpr bool kHalves = PAT == FIXED && BLK == 64;  // items may be 32-key halves
     static_assert(!kHalves || (C::NW == 4 && C::KBW == 1 && C::QC == 2), "half items: 4 waves of 16 keys");
@@ -480,9 +485,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     // on; a claim is (queue << 56 | index), kNoWork once all queues are dry.
     constexpr unsigned long long kNoWork = ~0ull;
     int qx = 0, q_left = kQueues;
-    uint64_t per_layout = 0;  // item slots taken per (batch, head)
+    uint64_t per_layout = 0;  // item slots taken per (batch, head): the largest item count of a layout
     if (tid == 0) {
-        per_layout = queue[kQueues];
+        const int n_layouts = layout_count(a.mode, a.sub);
+        for (int gl = 0; gl < n_layouts; ++gl)
+            per_layout = (uint64_t)items[gl] > per_layout ? (uint64_t)items[gl] : per_layout;
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
         qx = (int)(xcc % kQueues);
@@ -514,16 +521,16 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int rank = __builtin_amdgcn_readfirstlane((int)(t / (uint64_t)nx));  // position in the length order
         const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
         const int h = bh % a.heads, b = bh / a.heads;
-        const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
+        const int lay = head_layout(a, h);
         const int32_t code = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
-        if (code < 0) {  // an empty slot (a layout with fewer items than the other)
+        if (code < 0) {  // an empty slot (a layout with fewer items than another)
             if (tid == 0) sItem[(it + 1) & 1] = next;
             __syncthreads();
             continue;
         }
         const int kb = code & ((1 << kItemShift) - 1);
         const int half = kHalves ? code >> kItemShift : 0;
-        const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
+        const MaskParams mp = head_mask_params(a, PAT, MODE, h);
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
@@ -545,7 +552,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
                 vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
             }
-            cl[kbw] = col_lane(j, a.dl, a.c);
+            cl[kbw] = col_lane(j, a.dl, a.c, mp.w);
         }
         // summary keys of this key block (fixed pattern), bit = key offset in the block
         const uint64_t key_summary = PAT == FIXED ? summary_bits(mp, mod_l(a.dl, kb * BLK)) & kTileBits : 0ull;
@@ -561,9 +568,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
         const int e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
         int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
-        if (half == 1) {
-            // the lower keys are attended only inside their own l-block: the
-            // column's first entries (the query blocks ascend)
+        if (half != 0 && ((key_summary >> (32 * (half - 1))) & 0xFFFFFFFFull) == 0ull) {
+            // the non-summary half is attended only inside its own l-block:
+            // the column's first entries (the query blocks ascend)
             int near = 0;
             while (near < len &&
                    !far_block(FIXED, a.dl, BLK * __builtin_amdgcn_readfirstlane(row_idx[e0 + near]), kb * BLK, BLK))
@@ -594,7 +601,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
             const bool masked =
-                !block_full32(PAT, mp.part, a.dl, a.c, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+                !block_full32(PAT, mp.part, a.dl, a.c, mp.w, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
             wait_loads_upto<0>();
             __syncthreads();  // block sidx is in LDS everywhere; the other stage is free
             if (sidx + 1 < len) load_block(qb_next, st ^ 1);
@@ -811,8 +818,9 @@ bwd_dq_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restri
     const int i = blockIdx.x * 64 + threadIdx.x;
     if (i >= a.n) return;
     const int qb = i / a.block;
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+    const int lay = head_layout(a, h);
     const int part = part_of_head(a.mode, h);
+    const int32_t wst = window_start(a, subblock_of_head(a.sub, h));
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowid = ((int64_t)b * a.heads + h) * a.n + i;
     const float L = lse[rowid], nDi = ndelta[rowid];
@@ -826,7 +834,7 @@ bwd_dq_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restri
         const bool full = a.kind[e] == TILE_FULL;
         for (int jj = 0; jj < a.block; ++jj) {
             const int jx = kb * a.block + jj;
-            if (!full && !attended(a.pattern, part, a.l, a.c, i, jx)) continue;
+            if (!full && !attended(a.pattern, part, a.l, a.c, wst, i, jx)) continue;
             const float* kr = k + base + (int64_t)jx * a.ss;
             const float* vr = v + base + (int64_t)jx * a.ss;
             float s = 0.f, dp = 0.f;
@@ -852,8 +860,9 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
     const int jx = blockIdx.x * 64 + threadIdx.x;
     if (jx >= a.n) return;
     const int kb = jx / a.block;
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+    const int lay = head_layout(a, h);
     const int part = part_of_head(a.mode, h);
+    const int32_t wst = window_start(a, subblock_of_head(a.sub, h));
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const float* kr = k + base + (int64_t)jx * a.ss;
@@ -866,7 +875,7 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
         const bool full = a.kind_t[e] == TILE_FULL;
         for (int ii = 0; ii < a.block; ++ii) {
             const int i = qb * a.block + ii;
-            if (!full && !attended(a.pattern, part, a.l, a.c, i, jx)) continue;
+            if (!full && !attended(a.pattern, part, a.l, a.c, wst, i, jx)) continue;
             const float* qr = q + base + (int64_t)i * a.ss;
             const float* gr = dout + base + (int64_t)i * a.ss;
             float s = 0.f, dp = 0.f;
@@ -889,28 +898,31 @@ bwd_dkdv_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __rest
 }
 
 // Workspace: -D [rows] and -LSE log2 e [rows] (fp32), then (16-byte aligned)
-// the kQueues queue counters, the item count per layout, and the item order
-// of each layout (2 nq slots).
+// the kQueues queue counters (uint64), the item count of each layout
+// (int32), and the item order of each layout (2 nq int32 slots).
 struct BwdWorkspace {
     float* ndelta;  // -D
     float* nlse2;   // -LSE log2 e
     unsigned long long* queue;
+    int32_t* items;
     int32_t* order;
 };
 
 constexpr int64_t align16(int64_t x) { return (x + 15) / 16 * 16; }
 
 int64_t bwd_workspace_size(int64_t rows, int64_t nq, int n_layouts) {
-    return align16(2 * rows * (int64_t)sizeof(float)) + (kQueues + 1) * 8 + n_layouts * 2 * nq * 4;
+    return align16(2 * rows * (int64_t)sizeof(float)) + kQueues * 8 + (int64_t)n_layouts * 4 +
+           (int64_t)n_layouts * 2 * nq * 4;
 }
 
-BwdWorkspace bwd_workspace(void* ws, int64_t rows) {
+BwdWorkspace bwd_workspace(void* ws, int64_t rows, int n_layouts) {
     char* p = static_cast<char*>(ws);
     BwdWorkspace w;
     w.ndelta = reinterpret_cast<float*>(p);
     w.nlse2 = w.ndelta + rows;
     w.queue = reinterpret_cast<unsigned long long*>(p + align16(2 * rows * (int64_t)sizeof(float)));
-    w.order = reinterpret_cast<int32_t*>(w.queue + kQueues + 1);
+    w.items = reinterpret_cast<int32_t*>(w.queue + kQueues);
+    w.order = w.items + n_layouts;
     return w;
 }
 
@@ -943,7 +955,7 @@ hipError_t launch_bwd_f32(const AttnArgs& a, const void* q, const void* k, const
     float* ndelta = ws.ndelta;
     hipLaunchKernelGGL((bwd_pre_kernel<D, float>), dim3((unsigned)((rows + 255) / 256)), dim3(256),
                        0, stream, a, (const float*)o, (const float*)dout, lse, ndelta, ws.nlse2,
-                       (unsigned long long*)nullptr, (int32_t*)nullptr);
+                       (unsigned long long*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
     dim3 grid((unsigned)((a.n + 63) / 64), (unsigned)a.heads, (unsigned)a.batch);
     hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), grid, dim3(64), 0, stream, a, (const float*)q,
                        (const float*)k, (const float*)v, (const float*)dout, lse, ndelta, (float*)dq);
@@ -960,9 +972,10 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     float* ndelta = ws.ndelta;
     float* nlse2 = ws.nlse2;
-    hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)((rows + 255) / 256)),
-                       dim3(256), 0, stream, a, (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2,
-                       ws.queue, ws.order);
+    const int64_t pre_groups = (rows + 255) / 256 > layout_count(a.mode, a.sub) ? (rows + 255) / 256
+                                                                                 : layout_count(a.mode, a.sub);
+    hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, a,
+                       (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
@@ -980,7 +993,7 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK, PAT>::NT), 0,
                            stream, a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
                            (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,
-                           ws.queue, ws.order);
+                           ws.queue, ws.items, ws.order);
         return hipGetLastError();
     });
 }
@@ -1005,7 +1018,7 @@ size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
                       void* dv, void* workspace, hipStream_t stream) {
-    const BwdWorkspace ws = bwd_workspace(workspace, (int64_t)a.batch * a.heads * a.n);
+    const BwdWorkspace ws = bwd_workspace(workspace, (int64_t)a.batch * a.heads * a.n, layout_count(a.mode, a.sub));
     if (dtype == 1) {
         switch (a.d) {
         case 32: return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);

@@ -29,6 +29,7 @@ constexpr int kMaxWorkgroups = 4096;  // splits are capped at this over all (bat
 
 struct DecodeArgs {
     int pattern, mode, heads, splits;
+    int32_t sub;  // summary subblocks (0: one window for all heads)
     int32_t pos, l, c;
     DivL dc;
     int64_t qsb, qsh;        // q and o strides
@@ -81,7 +82,8 @@ decode_split_kernel(DecodeArgs a, const T* __restrict__ q, const T* __restrict__
     const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid % 64, w = tid / 64;
     const int slot = lane / LPK, ds = lane % LPK;  // key slot of the lane; its elements are 8 ds .. 8 ds + 7
-    const DecodeSet S(a.pattern, part_of_head(a.mode, h), a.pos, a.l, a.c, a.dc);
+    const DecodeSet S(a.pattern, part_of_head(a.mode, h), a.pos, a.l, a.c,
+                      (int32_t)summary_start(a.l, a.c, subblock_of_head(a.sub, h)), a.dc);
     const int64_t per = (S.count + a.splits - 1) / a.splits;
     const int64_t t0 = (int64_t)split * per < S.count ? (int64_t)split * per : S.count;
     const int64_t t1 = t0 + per < S.count ? t0 + per : S.count;
@@ -193,14 +195,17 @@ hipError_t launch(const DecodeArgs& a, int batch, const void* q, const void* k, 
 
 }  // namespace
 
-// Ranges per (batch, head): about kKeysPerSplit keys each, at most
-// kMaxWorkgroups workgroups in all (and at least one range).
-int decode_splits(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int64_t batch, int64_t heads) {
+// Ranges per (batch, head): about kKeysPerSplit keys each (for the largest
+// set of a head), at most kMaxWorkgroups workgroups in all (and at least one
+// range).
+int decode_splits(int pattern, int mode, int32_t sub, int32_t pos, int32_t l, int32_t c, int64_t batch,
+                  int64_t heads) {
     const DivL dc = make_divl(c > 0 ? c : 1);
     int64_t count = 0;
-    const int parts = mode == MODE_INTERLEAVED ? 2 : 1;
-    for (int g = 0; g < parts; ++g) {
-        const DecodeSet S(pattern, part_of_layout(mode, g), pos, l, c, dc);
+    const int sets = layout_count(mode, sub);
+    for (int g = 0; g < sets; ++g) {
+        const int32_t w = (int32_t)summary_start(l, c, subblock_of_layout(mode, sub, g));
+        const DecodeSet S(pattern, part_of_layout(mode, g), pos, l, c, w, dc);
         count = S.count > count ? S.count : count;
     }
     int64_t splits = (count + kKeysPerSplit - 1) / kKeysPerSplit;
@@ -210,20 +215,22 @@ int decode_splits(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int6
     return (int)splits;
 }
 
-size_t decode_workspace_bytes(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int64_t batch,
-                              int64_t heads, int d) {
-    return (size_t)batch * heads * decode_splits(pattern, mode, pos, l, c, batch, heads) * (d + 2) * sizeof(float);
+size_t decode_workspace_bytes(int pattern, int mode, int32_t sub, int32_t pos, int32_t l, int32_t c,
+                              int64_t batch, int64_t heads, int d) {
+    return (size_t)batch * heads * decode_splits(pattern, mode, sub, pos, l, c, batch, heads) * (d + 2) *
+           sizeof(float);
 }
 
-hipError_t decode_launch(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int batch, int heads, int d,
-                         int dtype, const void* q, const int64_t* q_strides, const void* k, const void* v,
+hipError_t decode_launch(int pattern, int mode, int32_t sub, int32_t pos, int32_t l, int32_t c, int batch, int heads,
+                         int d, int dtype, const void* q, const int64_t* q_strides, const void* k, const void* v,
                          const int64_t* kv_strides, float scale, void* o, float* lse, void* workspace,
                          hipStream_t stream) {
     DecodeArgs a;
     a.pattern = pattern;
     a.mode = mode;
     a.heads = heads;
-    a.splits = decode_splits(pattern, mode, pos, l, c, batch, heads);
+    a.sub = sub;
+    a.splits = decode_splits(pattern, mode, sub, pos, l, c, batch, heads);
     a.pos = pos;
     a.l = l;
     a.c = c;

@@ -61,8 +61,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
-    const int lay = MODE == MODE_INTERLEAVED ? (h & 1) : 0;
-    const MaskParams mp{PAT, part_of_head(MODE, h), a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi};
+    const int lay = head_layout(a, h);
+    const MaskParams mp = head_mask_params(a, PAT, MODE, h);
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int row0 = qb * BLK + w * C::RW;  // first query row of this wave
 
@@ -86,7 +86,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
-    // A step stages one block, or two upper halves (see RowStepper) as one tile
+    // A step stages one block, or two summary halves (see RowStepper) as one tile
     constexpr bool kPairs = PAT == FIXED && BLK == 64;
     auto load_step = [&](RowStep s, int stage) {
         const uint32_t kdst = sK_base + stage * kTileBytes, vdst = sV_base + stage * kTileBytes;
@@ -95,7 +95,11 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             ld.issue(k + kbase, kdst);
             ld.issue(v + kbase, vdst);
         } else if constexpr (kPairs) {
-            const int64_t lo = base + ((int64_t)s.a * BLK + BLK / 2) * a.ss, hi = base + (int64_t)s.b * BLK * a.ss;
+            // the summary halves: upper (window at 32 mod 64) or lower (at 0 mod
+            // 64); issue_halves takes tile rows 0..31 from lo and 32..63 from hi
+            const int half_off = (mp.w & 63) == 0 ? 0 : BLK / 2;
+            const int64_t lo = base + ((int64_t)s.a * BLK + half_off) * a.ss;
+            const int64_t hi = base + ((int64_t)s.b * BLK - (BLK / 2 - half_off)) * a.ss;
             ld.issue_halves(k + lo, k + hi, kdst);
             ld.issue_halves(v + lo, v + hi, vdst);
         }
@@ -119,9 +123,9 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         const RowStep nxt = steps.next();
         const int kb = cur.a;
         const int j0 = kb * BLK;
-        // a pair of upper halves is attended everywhere
+        // a pair of summary halves is attended everywhere
         const bool masked =
-            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // this step is in LDS everywhere; the other stage is free
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
@@ -321,8 +325,9 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
     const int i = blockIdx.x * 64 + threadIdx.x;
     if (i >= a.n) return;
     const int qb = i / a.block;
-    const int lay = a.mode == MODE_INTERLEAVED ? (h & 1) : 0;
+    const int lay = head_layout(a, h);
     const int part = part_of_head(a.mode, h);
+    const int32_t wst = window_start(a, subblock_of_head(a.sub, h));
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
 
     float qr[D], acc[D];
@@ -337,7 +342,7 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
         const bool full = a.kind[e] == TILE_FULL;
         for (int jj = 0; jj < a.block; ++jj) {
             const int j = kb * a.block + jj;
-            if (!full && !attended(a.pattern, part, a.l, a.c, i, j)) continue;
+            if (!full && !attended(a.pattern, part, a.l, a.c, wst, i, j)) continue;
             const float* kr = k + base + (int64_t)j * a.ss;
             float s = 0.f;
             for (int t = 0; t < D; ++t) s = fmaf(qr[t], kr[t], s);

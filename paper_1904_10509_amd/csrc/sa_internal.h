@@ -7,6 +7,7 @@
 
 #include <type_traits>
 
+#include "sa_mask.h"
 #include "sa_pattern.h"
 
 namespace sa {
@@ -16,7 +17,7 @@ constexpr float kLog2eHost = 1.4426950408889634f;
 // Present blocks of one layout, counted on the host with the O(1) test.
 int64_t layout_count_host(const Pattern& p, int64_t n, int64_t B);
 
-hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode, int64_t l,
+hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode, int32_t sub, int64_t l,
                          int64_t c, int n_layouts, int32_t* row_ptr, int32_t* col_idx,
                          uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
                          hipStream_t stream);
@@ -58,7 +59,8 @@ struct AttnArgs {
     float scale;           // softmax scale (> 0)
     float scale_log2;      // scale * log2(e)
     uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
-    uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64)
+    uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64, subblock 0)
+    int32_t sub;           // fixed: 0 = one summary window for all heads, else floor(l / c) subblocks
     DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;
@@ -67,6 +69,26 @@ struct AttnArgs {
     const int32_t* row_idx;
     const uint8_t* kind_t;
 };
+
+// Layout that head h reads.
+__host__ __device__ inline int head_layout(const AttnArgs& a, int h) { return layout_of_head(a.mode, a.sub, h); }
+
+// First summary position of subblock s inside an l-block (fixed pattern).
+__host__ __device__ inline int32_t window_start(const AttnArgs& a, int s) {
+    return (int32_t)summary_start(a.l, a.c, s);
+}
+
+// Mask parameters of one part and summary subblock s.  With distinct
+// subblocks and l <= 64 the 128-position summary words are built here (a few
+// scalar steps per workgroup); otherwise they come with the call.
+__device__ inline MaskParams mask_params(const AttnArgs& a, int pattern, int part, int s) {
+    MaskParams mp{pattern, part, a.l, a.c, a.period_bits, a.sum_lo, a.sum_hi, window_start(a, s)};
+    if (pattern == FIXED && s != 0 && a.l <= 64) summary_words(a.l, a.c, mp.w, &mp.sum_lo, &mp.sum_hi);
+    return mp;
+}
+__device__ inline MaskParams head_mask_params(const AttnArgs& a, int pattern, int mode, int h) {
+    return mask_params(a, pattern, part_of_head(mode, h), subblock_of_head(a.sub, h));
+}
 
 // Forward.  q, k, v, o use the strides in `a`; lse is [batch, heads, n].
 hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
@@ -89,10 +111,10 @@ inline hipError_t with_full_body(const AttnArgs& a, F&& f) {
     }
 }
 
-size_t decode_workspace_bytes(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int64_t batch,
-                              int64_t heads, int d);
-hipError_t decode_launch(int pattern, int mode, int32_t pos, int32_t l, int32_t c, int batch, int heads, int d,
-                         int dtype, const void* q, const int64_t* q_strides, const void* k, const void* v,
+size_t decode_workspace_bytes(int pattern, int mode, int32_t sub, int32_t pos, int32_t l, int32_t c,
+                              int64_t batch, int64_t heads, int d);
+hipError_t decode_launch(int pattern, int mode, int32_t sub, int32_t pos, int32_t l, int32_t c, int batch, int heads,
+                         int d, int dtype, const void* q, const int64_t* q_strides, const void* k, const void* v,
                          const int64_t* kv_strides, float scale, void* o, float* lse, void* workspace,
                          hipStream_t stream);
 

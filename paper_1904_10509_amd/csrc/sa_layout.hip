@@ -30,6 +30,7 @@ struct LayoutArgs {
     int32_t block;
     int32_t pattern;
     int32_t mode;
+    int32_t sub;  // summary subblocks (0: one window for all heads)
     int64_t l, c;
 };
 
@@ -39,6 +40,7 @@ __device__ inline Pattern pattern_of(const LayoutArgs& a, int g) {
     p.part = part_of_layout(a.mode, g);
     p.l = a.l;
     p.c = a.c;
+    p.w = summary_start(a.l, a.c, subblock_of_layout(a.mode, a.sub, g));
     return p;
 }
 
@@ -161,7 +163,7 @@ int64_t layout_count_host(const Pattern& p, int64_t n, int64_t B) {
     return total;
 }
 
-hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode, int64_t l,
+hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode, int32_t sub, int64_t l,
                          int64_t c, int n_layouts, int32_t* row_ptr, int32_t* col_idx,
                          uint8_t* kind, int32_t* col_ptr, int32_t* row_idx, uint8_t* kind_t,
                          hipStream_t stream) {
@@ -170,6 +172,7 @@ hipError_t layout_launch(int64_t n, int32_t block, int32_t pattern, int32_t mode
     a.block = block;
     a.pattern = pattern;
     a.mode = mode;
+    a.sub = sub;
     a.l = l;
     a.c = c;
     dim3 grid((unsigned)a.nq, (unsigned)n_layouts);

@@ -9,7 +9,9 @@
 //   strided A1        i - l <= j              (an interval)
 //   strided A2        i - j == 0 mod l        (bits at a period of l)
 //   fixed A1          same l-block            (an interval)
-//   fixed A2          j mod l >= l - c        (c-wide runs at a period of l)
+//   fixed A2          w <= j mod l < w + c    (c-wide runs at a period of l;
+//                                             w = l - c unless heads have
+//                                             their own subblocks)
 // Elements then test one bit each.
 #pragma once
 
@@ -42,17 +44,19 @@ __device__ inline int mod_pos(int x, int l) {
 struct MaskParams {
     int pattern, part, l, c;
     uint64_t period_bits;  // strided: bits at multiples of l below 64
-    uint64_t sum_lo, sum_hi;  // fixed, l <= 64: summary positions p mod l >= l - c, p < 128
+    uint64_t sum_lo, sum_hi;  // fixed, l <= 64: summary positions p < 128 (w <= p mod l < w + c)
+    int w;                 // fixed: first summary position inside an l-block
 };
 
-// Summary columns (j mod l >= l - c) among j0 .. j0 + 63, as bits over j - j0;
-// r0 = j0 mod l.  For l <= 64 it is the precomputed 128-position pattern
-// shifted by r0; for l > 64 at most two runs of the pattern reach the 64
-// positions (the third would start at 3l - c - r0 > 2l - c >= l > 64).
+// Summary columns (w <= j mod l < w + c) among j0 .. j0 + 63, as bits over
+// j - j0; r0 = j0 mod l.  For l <= 64 it is the precomputed 128-position
+// pattern shifted by r0; for l > 64 the runs start at w - r0 + k l, and only
+// k = 0 (which may begin before j0) and k = 1 reach the 64 positions (k = -1
+// ends at w + c - 1 - r0 - l < 0, k = 2 starts past 2l - r0 > l > 64).
 // Wave-uniform arguments: evaluated on the scalar unit.
 __device__ inline uint64_t summary_bits(const MaskParams& p, int r0) {
     if (p.l <= 64) return r0 == 0 ? p.sum_lo : (p.sum_lo >> r0) | (p.sum_hi << (64 - r0));
-    const int s = p.l - p.c - r0;
+    const int s = p.w - r0;
     return bit_range(s, s + p.c - 1) | bit_range(s + p.l, s + p.l + p.c - 1);
 }
 
@@ -131,11 +135,12 @@ __device__ inline bool far_block(int pattern, const DivL& dl, int i0, int j0, in
 
 // The steps of a walk along one block row: a step is one present block, or,
 // with PAIRS (fixed pattern, B = 64), two consecutive blocks whose attended
-// keys, the same for every row, are exactly their upper 32, computed together
-// as one unmasked block made of the two upper halves.  When c = 32 and l is a
-// multiple of 64, every present block away from the diagonal is such a block
-// (only the last block of an l-block holds summary keys, exactly its upper
-// 32), and the blocks away from the diagonal are those below far_end, the
+// keys, the same for every row, are exactly one half of each (the upper 32
+// or the lower 32), computed together as one unmasked block made of the two
+// halves.  When c = 32, l is a multiple of 64 and the summary window starts
+// at a multiple of 32, every present block away from the diagonal is such a
+// block (only one block of an l-block holds summary keys, exactly one half of
+// it), and the blocks away from the diagonal are those below far_end, the
 // first block of the row's l-block: so one compare per entry decides.
 // RowStep::a < 0: the row is done; RowStep::b < 0: block a alone.  Entries are
 // read with scalar loads.
@@ -148,7 +153,7 @@ struct RowStepper {
     int e, e1;    // next entry, end of the row
     int far_end;  // pairs are formed below this key block; 0: no pairs
     __device__ static int pair_bound(const MaskParams& p, const DivL& dl, int i0) {
-        if (p.pattern != FIXED || p.part == PART_A1 || p.c != 32 || p.l % 64 != 0) return 0;
+        if (p.pattern != FIXED || p.part == PART_A1 || p.c != 32 || p.l % 64 != 0 || p.w % 32 != 0) return 0;
         return (i0 - mod_l(dl, i0)) / 64;
     }
     __device__ RowStep next() {
@@ -184,11 +189,11 @@ struct ColLane {
     int j;         // key column
     int j_mod;     // j mod l
     int blk0;      // first row of j's l-block
-    bool summary;  // fixed pattern: j mod l >= l - c
+    bool summary;  // fixed pattern: w <= j mod l < w + c
 };
-__device__ inline ColLane col_lane(int j, const DivL& dl, int c) {
+__device__ inline ColLane col_lane(int j, const DivL& dl, int c, int w) {
     const int m = mod_l(dl, j);
-    return ColLane{j, m, j - m, m >= dl.l - c};
+    return ColLane{j, m, j - m, m >= w && m < w + c};
 }
 
 // Attended queries i0 + ii (bit ii) of the lane's column; i0_mod = i0 mod l.
@@ -242,12 +247,19 @@ inline uint64_t host_period_bits(int64_t l) {
     return bits;
 }
 
-// Summary positions p < 128 with p mod l >= l - c, as two words (fixed, l <= 64).
-inline void host_summary_pattern(int64_t l, int64_t c, uint64_t* lo, uint64_t* hi) {
-    *lo = *hi = 0ull;
-    if (l > 64 || c < 1) return;
-    for (int64_t p = 0; p < 128; ++p)
-        if (p % l >= l - c) (p < 64 ? *lo : *hi) |= 1ull << (p % 64);
+// Summary positions p < 128 with w <= p mod l < w + c, as two words (fixed,
+// l <= 64): the runs w + k l .. w + k l + c - 1.
+__host__ __device__ inline void summary_words(int64_t l, int64_t c, int64_t w, uint64_t* lo, uint64_t* hi) {
+    uint64_t a = 0ull, b = 0ull;
+    if (l <= 64 && c >= 1) {
+        for (int64_t s = w; s < 128; s += l) {
+            const int64_t e = s + c - 1 < 127 ? s + c - 1 : 127;
+            if (s < 64) a |= (~0ull << s) & (~0ull >> (63 - (e < 63 ? e : 63)));
+            if (e >= 64) b |= (~0ull << (s > 64 ? s - 64 : 0)) & (~0ull >> (63 - (e - 64)));
+        }
+    }
+    *lo = a;
+    *hi = b;
 }
 
 }  // namespace sa

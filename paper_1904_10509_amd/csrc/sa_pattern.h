@@ -19,6 +19,7 @@ struct Pattern {
     int32_t part;     // PART_A1, PART_A2 or PART_MERGED
     int64_t l;        // stride
     int64_t c;        // summary width (fixed pattern)
+    int64_t w;        // first summary position inside an l-block (fixed pattern)
 };
 
 // Factor a head uses (Sec. 5.1).
@@ -33,18 +34,43 @@ __host__ __device__ inline int part_of_layout(int mode, int g) {
     return part_of_head(mode, 0);
 }
 
+// Summary subblocks (Sec. 4.3, closing remark on the fixed pattern: heads may
+// attend different c-wide subblocks of each l-block).  `sub` = 0: every head
+// uses the last c positions of each block.  sub = floor(l / c) > 0: subblock
+// s, numbered from the end of the block, holds positions l - (s + 1) c ..
+// l - s c - 1, and head h uses s = h mod sub.  Layouts, one per distinct set:
+// A1 alone 1; A2 or merged `sub`, layout s for subblock s; alternating heads
+// 1 + sub, layout 0 for A1 and 1 + s for A2 with subblock s.
+__host__ __device__ inline int64_t summary_start(int64_t l, int64_t c, int64_t s) { return l - (s + 1) * c; }
+
+__host__ __device__ inline int layout_count(int mode, int sub) {
+    if (sub == 0 || mode == MODE_A1) return mode == MODE_INTERLEAVED ? 2 : 1;
+    return mode == MODE_INTERLEAVED ? 1 + sub : sub;
+}
+__host__ __device__ inline int subblock_of_head(int sub, int h) { return sub > 0 ? h % sub : 0; }
+__host__ __device__ inline int layout_of_head(int mode, int sub, int h) {
+    if (mode == MODE_INTERLEAVED) return (h & 1) ? 1 + subblock_of_head(sub, h) : 0;
+    return mode == MODE_A1 ? 0 : subblock_of_head(sub, h);
+}
+__host__ __device__ inline int subblock_of_layout(int mode, int sub, int g) {
+    if (sub == 0 || mode == MODE_A1) return 0;
+    return mode == MODE_INTERLEAVED ? (g == 0 ? 0 : g - 1) : g;
+}
+
 __host__ __device__ inline int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 __host__ __device__ inline int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
-// First fixed-pattern summary column >= x (x >= 0).
-__host__ __device__ inline int64_t first_summary_at_or_after(int64_t x, int64_t l, int64_t c) {
-    int64_t r = x % l;
-    return r >= l - c ? x : x - r + (l - c);
+// First fixed-pattern summary column >= x (x >= 0); the summary columns are
+// the positions w .. w + c - 1 of every l-block.
+__host__ __device__ inline int64_t first_summary_at_or_after(int64_t x, int64_t l, int64_t c, int64_t w) {
+    const int64_t r = x % l;
+    if (r < w) return x - r + w;
+    return r < w + c ? x : x - r + l + w;
 }
 
 // Is any pair of the block rows [r0, r1] x columns [c0, c1] attended?  The
 // caller guarantees c0 <= r1 (blocks on or below the diagonal).
-__host__ __device__ inline bool block_present_part(int pattern, int part, int64_t l, int64_t c,
+__host__ __device__ inline bool block_present_part(int pattern, int part, int64_t l, int64_t c, int64_t w,
                                                    int64_t r0, int64_t r1, int64_t c0, int64_t c1) {
     if (pattern == STRIDED) {
         int64_t dmin = r0 - c1, dmax = r1 - c0;  // every difference i - j in between occurs
@@ -56,15 +82,15 @@ __host__ __device__ inline bool block_present_part(int pattern, int part, int64_
         // some l-block meets both the rows and the columns
         return max64(r0 / l, c0 / l) <= min64(r1 / l, c1 / l);
     }
-    return first_summary_at_or_after(c0, l, c) <= min64(c1, r1);
+    return first_summary_at_or_after(c0, l, c, w) <= min64(c1, r1);
 }
 
 __host__ __device__ inline bool block_present(const Pattern& p, int64_t r0, int64_t r1, int64_t c0,
                                               int64_t c1) {
     if (p.part == PART_MERGED)
-        return block_present_part(p.pattern, PART_A1, p.l, p.c, r0, r1, c0, c1) ||
-               block_present_part(p.pattern, PART_A2, p.l, p.c, r0, r1, c0, c1);
-    return block_present_part(p.pattern, p.part, p.l, p.c, r0, r1, c0, c1);
+        return block_present_part(p.pattern, PART_A1, p.l, p.c, p.w, r0, r1, c0, c1) ||
+               block_present_part(p.pattern, PART_A2, p.l, p.c, p.w, r0, r1, c0, c1);
+    return block_present_part(p.pattern, p.part, p.l, p.c, p.w, r0, r1, c0, c1);
 }
 
 // Number of integers in [lo, hi].
@@ -79,9 +105,9 @@ __host__ __device__ inline int64_t strided_hits(int64_t i, int64_t l, int64_t lo
 }
 
 // Number of summary columns in [0, x] (x >= -1).
-__host__ __device__ inline int64_t summary_upto(int64_t x, int64_t l, int64_t c) {
+__host__ __device__ inline int64_t summary_upto(int64_t x, int64_t l, int64_t c, int64_t w) {
     int64_t m = x + 1;
-    return (m / l) * c + max64(0, m % l - (l - c));
+    return (m / l) * c + min64(c, max64(0, m % l - w));
 }
 
 // |S_i intersected with [lo, hi]| for one part (lo >= 0).
@@ -98,9 +124,9 @@ __host__ __device__ inline int64_t attended_in_range(const Pattern& p, int64_t i
     int64_t blk0 = (i / p.l) * p.l;
     int64_t own = span(max64(lo, blk0), hi);
     if (p.part == PART_A1) return own;
-    if (p.part == PART_A2) return summary_upto(hi, p.l, p.c) - summary_upto(lo - 1, p.l, p.c);
+    if (p.part == PART_A2) return summary_upto(hi, p.l, p.c, p.w) - summary_upto(lo - 1, p.l, p.c, p.w);
     int64_t hi2 = min64(hi, blk0 - 1);
-    int64_t earlier = hi2 >= lo ? summary_upto(hi2, p.l, p.c) - summary_upto(lo - 1, p.l, p.c) : 0;
+    int64_t earlier = hi2 >= lo ? summary_upto(hi2, p.l, p.c, p.w) - summary_upto(lo - 1, p.l, p.c, p.w) : 0;
     return own + earlier;
 }
 
@@ -108,7 +134,7 @@ __host__ __device__ inline int64_t attended_in_range(const Pattern& p, int64_t i
 // attended, evaluated in O(1) on the scalar unit by the kernels (the layout
 // builder counts pairs instead).  Exact for every part except fixed merged,
 // where it may answer false for a full block, which only costs masking work.
-__host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int64_t c, int64_t r0,
+__host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int64_t c, int64_t w, int64_t r0,
                                            int64_t r1, int64_t c0, int64_t c1) {
     if (r0 < c1) return false;  // meets the diagonal: the causal cut runs through it
     if (pattern == STRIDED) {
@@ -116,7 +142,8 @@ __host__ __device__ inline bool block_full(int pattern, int part, int64_t l, int
         return r1 - c0 <= l || (part == PART_MERGED && l == 1);
     }
     const bool one_block = c0 / l == r1 / l;                                   // all pairs in one l-block
-    const bool all_summary = c == l || (c0 / l == c1 / l && c0 % l >= l - c);  // every column a summary
+    const bool all_summary =  // every column a summary
+        c == l || (c0 / l == c1 / l && c0 % l >= w && c1 % l < w + c);
     if (part == PART_A1) return one_block;
     if (part == PART_A2) return all_summary;
     return one_block || all_summary;
@@ -146,8 +173,8 @@ __host__ __device__ inline int32_t div_l(const DivL& d, int32_t x) {
 __host__ __device__ inline int32_t mod_l(const DivL& d, int32_t x) { return x - div_l(d, x) * d.l; }
 
 // block_full in 32-bit arithmetic (all coordinates below 2^31).
-__host__ __device__ inline bool block_full32(int pattern, int part, const DivL& dl, int32_t c, int32_t r0, int32_t r1,
-                                             int32_t c0, int32_t c1) {
+__host__ __device__ inline bool block_full32(int pattern, int part, const DivL& dl, int32_t c, int32_t w, int32_t r0,
+                                             int32_t r1, int32_t c0, int32_t c1) {
     const int32_t l = dl.l;
     if (r0 < c1) return false;
     if (pattern == STRIDED) {
@@ -156,7 +183,8 @@ __host__ __device__ inline bool block_full32(int pattern, int part, const DivL& 
     }
     const int32_t c0_blk = div_l(dl, c0);
     const bool one_block = c0_blk == div_l(dl, r1);
-    const bool all_summary = c == l || (c0_blk == div_l(dl, c1) && c0 - c0_blk * l >= l - c);
+    const bool all_summary =
+        c == l || (c0_blk == div_l(dl, c1) && c0 - c0_blk * l >= w && c1 - c0_blk * l < w + c);
     if (part == PART_A1) return one_block;
     if (part == PART_A2) return all_summary;
     return one_block || all_summary;
@@ -167,16 +195,18 @@ __host__ __device__ inline bool block_full32(int pattern, int part, const DivL& 
 // exactly once.  Order: the A1 interval ascending, then the A2 positions
 // outside it (strided: pos - 2l, pos - 3l, ...; fixed: the summary columns of
 // the earlier l-blocks, ascending).  A2 alone: strided pos, pos - l, ...;
-// fixed the summary columns up to pos, ascending.  dc divides by c (fixed).
+// fixed the summary columns up to pos, ascending.  dc divides by c; the
+// summary columns are the positions w .. w + c - 1 of every l-block (fixed).
 struct DecodeSet {
     int pattern, part;
-    int32_t pos, l, c;
+    int32_t pos, l, c, w;
     int32_t a1_lo;      // A1 is [a1_lo, a1_lo + n1)
     int64_t n1;         // up to 2^31 (pos = 2^31 - 1 with A1 from 0)
     int64_t count;
     DivL dc;
-    __host__ __device__ DecodeSet(int pattern_, int part_, int32_t pos_, int32_t l_, int32_t c_, const DivL& dc_)
-        : pattern(pattern_), part(part_), pos(pos_), l(l_), c(c_), dc(dc_) {
+    __host__ __device__ DecodeSet(int pattern_, int part_, int32_t pos_, int32_t l_, int32_t c_, int32_t w_,
+                                  const DivL& dc_)
+        : pattern(pattern_), part(part_), pos(pos_), l(l_), c(c_), w(w_), dc(dc_) {
         const int32_t lblk = pos / l;
         if (pattern == STRIDED) {
             a1_lo = pos - l > 0 ? pos - l : 0;
@@ -187,15 +217,16 @@ struct DecodeSet {
         } else {
             a1_lo = lblk * l;
             n1 = (int64_t)pos - a1_lo + 1;
-            const int32_t first_sum = a1_lo + l - c;  // first summary column of pos's l-block
+            const int32_t first_sum = a1_lo + w;  // first summary column of pos's l-block
+            const int32_t own = pos >= first_sum ? (pos - first_sum + 1 < c ? pos - first_sum + 1 : c) : 0;
             if (part == PART_A1) count = n1;
-            else if (part == PART_A2) count = (int64_t)lblk * c + (pos >= first_sum ? pos - first_sum + 1 : 0);
+            else if (part == PART_A2) count = (int64_t)lblk * c + own;
             else count = n1 + (int64_t)lblk * c;
         }
     }
     __host__ __device__ int32_t summary(int32_t u) const {  // u-th summary column from position 0
         const int32_t blk = div_l(dc, u);
-        return blk * l + l - c + (u - blk * c);
+        return blk * l + w + (u - blk * c);
     }
     __host__ __device__ int32_t at(int64_t t) const {
         if (pattern == STRIDED) {
@@ -210,7 +241,7 @@ struct DecodeSet {
 };
 
 // Element predicate in 32-bit arithmetic (0 <= i, j < 2^31).
-__host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32_t c, int32_t i,
+__host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32_t c, int32_t w, int32_t i,
                                          int32_t j) {
     if (j > i) return false;
     if (pattern == STRIDED) {
@@ -220,7 +251,8 @@ __host__ __device__ inline bool attended(int pattern, int part, int32_t l, int32
         return part == PART_A1 ? a1 : (part == PART_A2 ? a2 : (a1 || a2));
     }
     bool a1 = (i / l) == (j / l);
-    bool a2 = (j % l) >= l - c;
+    const int32_t r = j % l;
+    bool a2 = r >= w && r < w + c;
     return part == PART_A1 ? a1 : (part == PART_A2 ? a2 : (a1 || a2));
 }
 

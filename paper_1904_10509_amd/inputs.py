@@ -15,7 +15,7 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-STRIDED, FIXED = 0, 1
+STRIDED, FIXED, FIXED_PER_HEAD = 0, 1, 2
 MODE_A1, MODE_A2, MODE_MERGED, MODE_INTERLEAVED = 0, 1, 2, 3
 F32, BF16 = 0, 1
 
@@ -47,7 +47,7 @@ class Workload:
     def describe(self) -> dict:
         return {
             "workload": self.name,
-            "pattern": "strided" if self.pattern == STRIDED else "fixed",
+            "pattern": ["strided", "fixed", "fixed_per_head"][self.pattern],
             "mode": ["A1", "A2", "merged", "interleaved"][self.mode],
             "n": self.n, "stride": self.stride, "summary": self.summary,
             "block": self.block, "batch": self.batch, "heads": self.heads,
@@ -81,6 +81,12 @@ WORKLOADS = {
                  "image context of 3,072, fixed pattern"),
         Workload("strided_n3072_l128_merged", STRIDED, MODE_MERGED, 3072, 128, 0, 64, 4, 2, 128, BF16, 10,
                  "image context of 3,072, strided pattern"),
+        # the fixed pattern with a distinct summary subblock per head (head h
+        # uses positions l-(s+1)c .. l-sc-1 of each block, s = h mod l/c)
+        Workload("fixed_per_head_n65536_l256_c32_merged", FIXED_PER_HEAD, MODE_MERGED, 65536, 256, 32, 64, 1, 8,
+                 64, BF16, 11, "audio sequence of 65,536; the 8 heads take the 8 subblocks of each block"),
+        Workload("fixed_per_head_n12288_l128_c32_merged", FIXED_PER_HEAD, MODE_MERGED, 12288, 128, 32, 64, 2, 8,
+                 64, BF16, 12, "text context of 12,288; 8 heads over 4 subblocks"),
     ]
 }
 

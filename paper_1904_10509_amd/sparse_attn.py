@@ -19,12 +19,13 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_attn.so")
 
 SA_OK, SA_ERR_INVALID, SA_ERR_UNSUPPORTED, SA_ERR_BUFFER_TOO_SMALL, SA_ERR_HIP = 0, -1, -2, -3, -4
-SA_STRIDED, SA_FIXED = 0, 1
+SA_STRIDED, SA_FIXED, SA_FIXED_PER_HEAD = 0, 1, 2
 SA_MODE_A1, SA_MODE_A2, SA_MODE_MERGED, SA_MODE_INTERLEAVED = 0, 1, 2, 3
 SA_F32, SA_BF16 = 0, 1
 SA_TILE_FULL, SA_TILE_MASKED = 0, 1
 
 EXPORTED = (
+    "sparse_attn_layout_count",
     "sparse_attn_layout_size",
     "sparse_attn_layout",
     "sparse_attn_fwd",
@@ -53,6 +54,7 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
         L = ctypes.CDLL(LIB_PATH)
+        L.sparse_attn_layout_count.argtypes = [_i32, _i32, _i32, _i32, _vp]
         L.sparse_attn_layout_size.argtypes = _PAT + [_vp, _vp]
         L.sparse_attn_layout.argtypes = _PAT + [_vp] * 6 + [_i64, _vp]
         L.sparse_attn_fwd.argtypes = _PAT + [_vp] * 3 + [_i32] * 4 + [_vp] * 4 + [_f32, _vp, _vp, _vp]
@@ -112,13 +114,21 @@ def _dtype_code(t):
 # ---------------------------------------------------------------------------
 # Entry points, same names and argument order as the C ABI
 # ---------------------------------------------------------------------------
-def sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode):
+def sparse_attn_layout_count(stride_l, summary_c, pattern, head_mode):
     ng = ctypes.c_int32(0)
-    nnz = (ctypes.c_int64 * 2)(0, 0)
+    st = lib().sparse_attn_layout_count(stride_l, summary_c, pattern, head_mode, ctypes.byref(ng))
+    _check("sparse_attn_layout_count", st)
+    return ng.value
+
+
+def sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode):
+    entries = max(2, sparse_attn_layout_count(stride_l, summary_c, pattern, head_mode))
+    ng = ctypes.c_int32(0)
+    nnz = (ctypes.c_int64 * entries)()
     st = lib().sparse_attn_layout_size(n, block, stride_l, summary_c, pattern, head_mode,
                                        ctypes.byref(ng), nnz)
     _check("sparse_attn_layout_size", st)
-    return ng.value, [nnz[0], nnz[1]][: ng.value]
+    return ng.value, list(nnz)[: ng.value]
 
 
 def sparse_attn_layout(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,

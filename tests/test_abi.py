@@ -47,6 +47,9 @@ SIZE_CASES = [
     (3072, 32, 128, 32, 1, 3), (240, 16, 20, 1, 1, 2), (192, 64, 24, 10, 1, 1), (128, 16, 500, 3, 1, 2),
     (512, 64, 256, 32, 1, 2), (512, 16, 48, 48, 1, 3), (12288, 64, 128, 0, 0, 2),
     (65536, 64, 256, 32, 1, 2),
+    # distinct summary subblocks per head (pattern 2)
+    (256, 16, 32, 8, 2, 0), (256, 16, 32, 8, 2, 1), (256, 64, 128, 32, 2, 2), (240, 16, 20, 6, 2, 3),
+    (512, 64, 256, 32, 2, 3), (65536, 64, 128, 32, 2, 2), (128, 16, 16, 16, 2, 2),
 ]
 
 
@@ -65,7 +68,9 @@ def test_layout_size_matches_oracle(L, orc, n, B, l, c, pattern, mode):
     (256, 16, 8, 3, 0, 2),    # c given for strided
     (256, 16, 8, 0, 1, 2),    # c = 0 for fixed
     (256, 16, 8, 9, 1, 2),    # c > l
-    (256, 16, 8, 0, 2, 2),    # unknown pattern
+    (256, 16, 8, 0, 2, 2),    # c = 0 for fixed with subblocks per head
+    (256, 16, 8, 9, 2, 2),    # c > l
+    (256, 16, 8, 0, 3, 2),    # unknown pattern
     (256, 16, 8, 0, 0, 4),    # unknown mode
     (0, 16, 8, 0, 0, 2),      # n < 1
 ])
@@ -73,6 +78,20 @@ def test_layout_size_rejects_invalid(L, args):
     ng = ctypes.c_int32(0)
     nnz = (ctypes.c_int64 * 2)()
     assert L.sparse_attn_layout_size(*args, ctypes.byref(ng), nnz) == sa.SA_ERR_INVALID
+
+
+def test_layout_count(L):
+    ng = ctypes.c_int32(0)
+    for (l, c, pattern, mode), expect in [((16, 0, 0, 2), 1), ((16, 0, 0, 3), 2), ((16, 4, 1, 3), 2),
+                                          ((16, 4, 2, 0), 1), ((16, 4, 2, 1), 4), ((16, 4, 2, 2), 4),
+                                          ((16, 4, 2, 3), 5), ((20, 6, 2, 2), 3), ((128, 2, 2, 3), 65)]:
+        assert L.sparse_attn_layout_count(l, c, pattern, mode, ctypes.byref(ng)) == 0
+        assert ng.value == expect, (l, c, pattern, mode)
+    # more than 64 subblocks per block, or a missing output
+    assert L.sparse_attn_layout_count(130, 2, 2, 2, ctypes.byref(ng)) == sa.SA_ERR_UNSUPPORTED
+    assert L.sparse_attn_layout_count(16, 4, 2, 2, None) == sa.SA_ERR_INVALID
+    nnz = (ctypes.c_int64 * 2)()
+    assert L.sparse_attn_layout_size(256, 16, 130, 2, 2, 2, ctypes.byref(ng), nnz) == sa.SA_ERR_UNSUPPORTED
 
 
 FAKE = 0x100000  # never dereferenced: every call below fails validation first
@@ -110,18 +129,20 @@ def test_fwd_rejects_invalid(L, over, expect):
 def test_bwd_workspace_and_errors(L):
     out = ctypes.c_size_t(0)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
-    # D_i and the base-2 LSE per row, 8 queue counters and the item count, the
-    # item order of the one layout (two slots per key block)
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
+    # D_i and the base-2 LSE per row, 8 queue counters, the item count of the
+    # one layout, its item order (two slots per key block)
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 4 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 64, sa.SA_F32, ctypes.byref(out)) == 0
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 4 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 8, 1, 3, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
-    assert out.value == 2 * 2 * 3 * 256 * 4 + 9 * 8 + 2 * 2 * 4 * (256 // 16)  # interleaved: two layouts
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 2 * (4 + 2 * 4 * (256 // 16))  # interleaved: two layouts
+    assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 4, 2, 3, 2, 3, 64, sa.SA_BF16, ctypes.byref(out)) == 0
+    assert out.value == 2 * 2 * 3 * 256 * 4 + 8 * 8 + 5 * (4 + 2 * 4 * (256 // 16))  # A1 + four subblocks
     assert L.sparse_attn_bwd_workspace_size(256, 16, 16, 0, 0, 2, 2, 3, 40, sa.SA_F32, ctypes.byref(out)) == \
         sa.SA_ERR_UNSUPPORTED
     strides = (ctypes.c_int64 * 3)(256 * 64, 256 * 64, 64)
     common = [256, 16, 16, 0, 0, 2] + [FAKE] * 6 + [1, 1, 64, sa.SA_BF16] + [FAKE] * 6 + [strides, 0.125] + [FAKE] * 3
-    need = 2 * 256 * 4 + 9 * 8 + 2 * 4 * (256 // 16)
+    need = 2 * 256 * 4 + 8 * 8 + 4 + 2 * 4 * (256 // 16)
     assert L.sparse_attn_bwd(*common, FAKE, need - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
     assert L.sparse_attn_bwd(*common, None, need, None) == sa.SA_ERR_INVALID
     bad = list(common)
@@ -157,6 +178,13 @@ def test_decode_workspace_and_errors(L):
     assert L.sparse_attn_decode_workspace_size(2**31 - 1, 2**31 - 1, 0, sa.SA_STRIDED, sa.SA_MODE_A1, 64, 8, 128,
                                                sa.SA_BF16, ctypes.byref(out)) == 0
     assert out.value == 64 * 8 * 8 * 130 * 4
+    # subblocks per head, A2 at pos 65,335 (position 55 of its block): subblock 7 (positions 0..31) holds
+    # 255 * 32 + 32 = 8,192 keys, the most of any head: 32 ranges
+    assert L.sparse_attn_decode_workspace_size(65335, 256, 32, sa.SA_FIXED_PER_HEAD, sa.SA_MODE_A2, 1, 8, 64,
+                                               sa.SA_BF16, ctypes.byref(out)) == 0
+    assert out.value == 8 * 32 * 66 * 4
+    assert L.sparse_attn_decode_workspace_size(10, 256, 2, sa.SA_FIXED_PER_HEAD, sa.SA_MODE_A2, 1, 8, 64,
+                                               sa.SA_BF16, ctypes.byref(out)) == sa.SA_ERR_UNSUPPORTED
     bad = [
         (-1, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),
         (2**31, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, 1, 64, sa.SA_BF16, sa.SA_ERR_INVALID),

@@ -13,7 +13,7 @@ from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, to64
 
 pytestmark = pytest.mark.gpu
 
-S, F = sa.SA_STRIDED, sa.SA_FIXED
+S, F, P = sa.SA_STRIDED, sa.SA_FIXED, sa.SA_FIXED_PER_HEAD
 A1, A2, MG, IL = sa.SA_MODE_A1, sa.SA_MODE_A2, sa.SA_MODE_MERGED, sa.SA_MODE_INTERLEAVED
 
 # (pattern, mode, n of the cache, l, c, d, dtype, batch, heads)
@@ -28,12 +28,17 @@ CASES = [
     (F, A2, 1500, 128, 32, 32, torch.bfloat16, 2, 2),
     (F, IL, 3072, 128, 32, 128, torch.bfloat16, 2, 2),
     (F, A1, 900, 96, 40, 64, torch.bfloat16, 1, 1),
+    # a distinct summary subblock per head (heads covering every subblock)
+    (P, MG, 2048, 128, 32, 64, torch.bfloat16, 1, 4),
+    (P, A2, 1500, 128, 32, 64, torch.bfloat16, 2, 5),
+    (P, IL, 1000, 48, 12, 128, torch.bfloat16, 1, 8),
+    (P, A2, 600, 32, 8, 32, torch.float32, 1, 4),
 ]
 
 
 def positions(n, l):
     """First and last positions, l-block and stride edges, a few inside."""
-    ps = {0, 1, l - 1, l, l + 1, 2 * l, 3 * l - 1, n // 2, n - 2, n - 1}
+    ps = {0, 1, l // 2, l - 1, l, l + 1, 2 * l, 3 * l - 1, n // 2, n - 2, n - 1}
     return sorted(p for p in ps if 0 <= p < n)
 
 

@@ -17,7 +17,7 @@ from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, run_gpu, to64
 
 pytestmark = pytest.mark.gpu
 
-S, F = sa.SA_STRIDED, sa.SA_FIXED
+S, F, P = sa.SA_STRIDED, sa.SA_FIXED, sa.SA_FIXED_PER_HEAD
 A1, A2, MG, IL = sa.SA_MODE_A1, sa.SA_MODE_A2, sa.SA_MODE_MERGED, sa.SA_MODE_INTERLEAVED
 
 
@@ -31,6 +31,9 @@ LAYOUT_CASES = [
     (F, 192, 64, 24, 10), (F, 128, 16, 500, 3), (F, 64, 64, 16, 4), (F, 384, 32, 128, 32),
     (F, 512, 64, 256, 32), (S, 3072, 32, 128, 0), (F, 3072, 32, 128, 32), (S, 12288, 64, 128, 0),
     (F, 65536, 64, 256, 32),
+    # a distinct summary subblock per head: one layout per subblock
+    (P, 256, 16, 32, 8), (P, 256, 64, 128, 32), (P, 240, 16, 20, 6), (P, 512, 64, 256, 32), (P, 192, 32, 48, 10),
+    (P, 16384, 64, 128, 32),
 ]
 
 
@@ -84,6 +87,22 @@ SMALL_CASES = [
     # more (batch, head) pairs than the dK / dV kernel has queues, not a multiple of them
     (S, MG, 256, 32, 32, 0, 32, torch.bfloat16, 3, 5),
     (F, IL, 256, 16, 64, 16, 32, torch.bfloat16, 3, 3),
+    # a distinct summary subblock per head, heads covering every subblock: with
+    # B = 64 and c = 32 the windows alternate between the upper and the lower
+    # halves of blocks (pairs of upper or of lower halves, split key blocks of
+    # either kind); l = 96 (blocks straddle l-blocks); l <= 64 (summary words
+    # built per head); fp32; more heads than subblocks
+    (P, MG, 1024, 64, 128, 32, 64, torch.bfloat16, 1, 4),
+    (P, A2, 1024, 64, 128, 32, 64, torch.bfloat16, 2, 4),
+    (P, IL, 1024, 64, 128, 32, 128, torch.bfloat16, 1, 8),
+    (P, MG, 768, 64, 256, 32, 64, torch.bfloat16, 1, 8),
+    (P, MG, 512, 64, 192, 32, 32, torch.bfloat16, 1, 6),
+    (P, MG, 768, 64, 96, 32, 64, torch.bfloat16, 1, 3),
+    (P, MG, 512, 32, 64, 16, 64, torch.bfloat16, 1, 5),
+    (P, A2, 512, 16, 48, 12, 32, torch.bfloat16, 1, 4),
+    (P, MG, 512, 64, 48, 10, 64, torch.bfloat16, 1, 4),
+    (P, IL, 256, 32, 64, 16, 128, torch.float32, 1, 4),
+    (P, A1, 256, 32, 64, 16, 64, torch.bfloat16, 1, 3),
 ]
 
 
@@ -135,7 +154,8 @@ def sample_index(w, rng, count):
 
 @pytest.mark.parametrize("name", ["strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged",
                                   "dense_n12288_merged", "fixed_n12288_l128_c32_merged", "dense_n3072_merged",
-                                  "fixed_n3072_l128_c32_merged", "strided_n3072_l128_merged"])
+                                  "fixed_n3072_l128_c32_merged", "strided_n3072_l128_merged",
+                                  "fixed_per_head_n65536_l256_c32_merged", "fixed_per_head_n12288_l128_c32_merged"])
 def test_workload_sampled(name):
     w = WORKLOADS[name]
     x = workload_inputs(w)

@@ -26,3 +26,13 @@ def test_decode_set_enumerates_s_pos(tmp_path):
                    capture_output=True)
     out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0 and out.stdout.startswith("ok"), out.stdout + out.stderr
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
+def test_summary_window_closed_forms(tmp_path):
+    exe = tmp_path / "check_pattern_window"
+    subprocess.run([HIPCC, "-O2", "-std=c++17", "-I", os.path.join(ROOT, "paper_1904_10509_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "host", "check_pattern_window.cpp"), "-o", str(exe)], check=True,
+                   capture_output=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0 and out.stdout.startswith("ok"), out.stdout + out.stderr
