@@ -28,10 +28,26 @@ HBM_PEAK_GBS = 8000.0
 BENCH_WORKLOADS = ("strided_n12288_l128_merged", "fixed_n65536_l256_c32_merged")
 
 
+def heads_per_layout(w, n_layouts):
+    """Heads reading each layout: alternating heads split A1 (layout 0) and A2;
+    with a summary subblock per head, head h reads the layout of subblock
+    h mod (l / c) (layout 1 + that subblock for the odd heads when they
+    alternate)."""
+    from paper_1904_10509_amd.inputs import FIXED_PER_HEAD, MODE_A1, MODE_INTERLEAVED
+    sub = w.stride // w.summary if w.pattern == FIXED_PER_HEAD else 0
+    counts = [0] * n_layouts
+    for h in range(w.heads):
+        if w.mode == MODE_INTERLEAVED:
+            g = (1 + (h % sub if sub else 0)) if h % 2 else 0
+        else:
+            g = 0 if (w.mode == MODE_A1 or sub == 0) else h % sub
+        counts[g] += 1
+    return counts
+
+
 def credited_flops(w, nnz):
-    """14 B^2 d per present block per (batch, head); interleaved heads split the layouts."""
-    heads_per_layout = [w.heads] if len(nnz) == 1 else [(w.heads + 1) // 2, w.heads // 2]
-    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout))
+    """14 B^2 d per present block per (batch, head), over the layout each head reads."""
+    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout(w, len(nnz))))
     return 14.0 * w.block * w.block * w.d_head * blocks, 4.0 * w.block * w.block * w.d_head * blocks
 
 
@@ -41,13 +57,13 @@ def mfma_flops_upper_bound(w, nnz):
     (QK^T, dO V^T, dS K), dK/dV kernel 4 (QK^T, dO V^T, P^T dO, dS^T Q).  The
     kernels skip the products of 32-wide chunks in which no pair of a wave's
     rows and columns is attended, so the work issued is at most this."""
-    heads_per_layout = [w.heads] if len(nnz) == 1 else [(w.heads + 1) // 2, w.heads // 2]
-    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout))
+    blocks = sum(z * w.batch * hpl for z, hpl in zip(nnz, heads_per_layout(w, len(nnz))))
     return 18.0 * w.block * w.block * w.d_head * blocks
 
 
 def attended_pairs(w):
-    """sum_i |S_i| per (batch, head) for the merged sets of Sec. 4.3 (closed forms)."""
+    """sum_i |S_i| per (batch, head) for the merged sets of Sec. 4.3 (closed forms;
+    with a summary subblock per head every head has the same count)."""
     import numpy as np
     from paper_1904_10509_amd.inputs import MODE_MERGED, STRIDED
     if w.mode != MODE_MERGED:
@@ -202,6 +218,8 @@ def table2(args):
 DECODE = {
     "fixed n=65,536 (l 256, c 32, 8 heads of 64)":
         dict(n=65536, l=256, c=32, pattern=1, heads=8, d=64, batch=32, seed=21),
+    "fixed, a summary subblock per head, n=65,536 (l 256, c 32, 8 heads of 64)":
+        dict(n=65536, l=256, c=32, pattern=2, heads=8, d=64, batch=32, seed=23),
     "strided n=1,048,576 (l 1,024, 4 heads of 64)":
         dict(n=1048576, l=1024, c=0, pattern=0, heads=4, d=64, batch=16, seed=22),
 }
@@ -248,7 +266,8 @@ def decode_bench(args):
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / args.steps
-        # |S_pos| of the merged sets (closed forms of Sec. 4.3), averaged over the timed positions
+        # |S_pos| of the merged sets (closed forms of Sec. 4.3, the same for every
+        # summary subblock), averaged over the timed positions
         rows = 0
         for pos in positions[args.warmup:]:
             if c["pattern"] == 0:
