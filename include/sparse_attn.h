@@ -233,6 +233,46 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
                        const int64_t* kv_strides, float softmax_scale, void* o, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/*
+ * Strided pattern, merged heads (SA_STRIDED, SA_MODE_MERGED), with the A2
+ * part computed by transposition (Sec. 5.5: reordered by residue mod l, a
+ * stride of l becomes a local window).  Same results as sparse_attn_fwd /
+ * sparse_attn_bwd over the merged layout, computed as
+ *   the band  A1 = {max(0, i-l) .. i}: the block kernels over the strided A1
+ *             layout (sparse_attn_layout with SA_MODE_A1 and the same n,
+ *             block, stride_l, summary_c = 0), and
+ *   the rest  {i - k l : k >= 2}: in each residue class (positions r + m l,
+ *             m < M = n / l), query m attends keys m' <= m - 2, dense causal
+ *             attention over blocks of class_block class positions,
+ * combined through their log-sum-exps (the sets are disjoint).
+ * Requirements beyond the common ones: l divides n; class_block in
+ * {16, 32, 64} divides M; M / class_block <= 4096 and batch * heads <= 65535
+ * (else SA_ERR_UNSUPPORTED); q, k, v, o, dout, dq, dk, dv contiguous
+ * [batch, heads, n, d_head] (no strides argument).
+ * Workspace: device memory of at least sparse_attn_transposed_workspace_size
+ * bytes, 256-byte aligned (SA_ERR_INVALID otherwise); one size serves both
+ * calls.  It holds a dense causal class layout, shifted copies of Q, O and
+ * dO, partial outputs and gradients, and the backward scratch; its contents
+ * on entry are ignored and calls sharing one workspace must not overlap.
+ * The row pointers are those of the A1 layout; the backward also takes its
+ * column form.  Outputs as for sparse_attn_fwd / sparse_attn_bwd.
+ */
+int sparse_attn_transposed_workspace_size(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                                          int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, size_t* bytes);
+
+int sparse_attn_fwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                               const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind, int32_t batch,
+                               int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                               const void* v, float softmax_scale, void* o, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+int sparse_attn_bwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                               const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                               const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                               int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                               const void* v, const void* o, const void* dout, const float* lse, float softmax_scale,
+                               void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream);
+
 const char* sparse_attn_status_string(int status);
 
 #ifdef __cplusplus

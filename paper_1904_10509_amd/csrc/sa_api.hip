@@ -134,6 +134,86 @@ int check_decode_shape(int32_t batch, int32_t heads, int32_t d, int32_t dtype) {
     return SA_OK;
 }
 
+// Merged strided heads by transposition: the band (strided A1, blocks of
+// `block`) and the dense causal class attention (M = n / l positions per
+// class, blocks of `class_block`), with the workspace regions of both calls.
+constexpr int64_t kMaxClassBlockRows = 4096;
+
+struct TransposedPlan {
+    PatternArgs band, cls;
+    int64_t rows, M, mq, nnz_c;
+    int64_t strides[3], class_strides[3];
+    size_t lay, t1, t2, t3, l1, l2, g1, g2, g3, bw, total;  // byte offsets
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+int plan_transposed(int64_t n, int32_t block, int32_t l, int32_t class_block, int32_t batch, int32_t heads, int32_t d,
+                    int32_t dtype, TransposedPlan* p) {
+    int st = check_pattern(n, block, l, 0, SA_STRIDED, SA_MODE_A1, &p->band);
+    if (st != SA_OK) return st;
+    if (n % l != 0) return SA_ERR_INVALID;
+    p->M = n / l;
+    st = check_pattern(p->M, class_block, (int32_t)p->M, 0, SA_STRIDED, SA_MODE_A1, &p->cls);
+    if (st != SA_OK) return st;
+    p->mq = p->M / class_block;
+    if (p->mq > kMaxClassBlockRows) return SA_ERR_UNSUPPORTED;
+    p->nnz_c = p->mq * (p->mq + 1) / 2;
+    if (batch < 1 || heads < 1) return SA_ERR_INVALID;
+    if ((int64_t)batch * heads > 65535) return SA_ERR_UNSUPPORTED;  // a grid dimension of the class call
+    p->strides[0] = (int64_t)heads * n * d;
+    p->strides[1] = n * d;
+    p->strides[2] = d;
+    p->class_strides[0] = n * d;  // (batch, head) pairs
+    p->class_strides[1] = d;      // residue classes
+    p->class_strides[2] = (int64_t)l * d;
+    st = check_tensor_args(p->band, batch, heads, d, dtype, p->strides);
+    if (st != SA_OK) return st;
+    if ((int64_t)batch * heads > INT32_MAX) return SA_ERR_INVALID;
+    st = check_tensor_args(p->cls, batch * heads, l, d, dtype, p->class_strides);
+    if (st != SA_OK) return st;
+    p->rows = (int64_t)batch * heads * n;
+    const size_t tensor = (size_t)p->rows * d * (dtype == SA_BF16 ? 2 : 4);
+    const size_t stats = (size_t)p->rows * sizeof(float);
+    const size_t lay = 2 * (size_t)(p->mq + 1) * 4 + 2 * (size_t)p->nnz_c * 5 + 64;
+    size_t off = 0;
+    p->lay = off;
+    off += align256(lay);
+    size_t* tensors[] = {&p->t1, &p->t2, &p->t3, &p->g1, &p->g2, &p->g3};
+    for (size_t* t : tensors) {
+        *t = off;
+        off += align256(tensor);
+    }
+    p->l1 = off;
+    off += align256(stats);
+    p->l2 = off;
+    off += align256(stats);
+    const size_t bw_band = sa::bwd_workspace_bytes(batch, heads, n, p->band.nq, 1);
+    const size_t bw_cls = sa::bwd_workspace_bytes((int64_t)batch * heads, l, p->M, p->cls.nq, 1);
+    p->bw = off;
+    off += align256(bw_band > bw_cls ? bw_band : bw_cls);
+    p->total = off;
+    return SA_OK;
+}
+
+// Class layout arrays inside the workspace.
+struct ClassLayout {
+    int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
+    uint8_t *kind, *kind_t;
+};
+ClassLayout class_layout(const TransposedPlan& p, char* ws) {
+    ClassLayout c;
+    char* b = ws + p.lay;
+    const size_t ptrs = (size_t)(p.mq + 1) * 4, idx = (size_t)p.nnz_c * 4;
+    c.row_ptr = reinterpret_cast<int32_t*>(b);
+    c.col_ptr = reinterpret_cast<int32_t*>(b + ptrs);
+    c.col_idx = reinterpret_cast<int32_t*>(b + 2 * ptrs);
+    c.row_idx = reinterpret_cast<int32_t*>(b + 2 * ptrs + idx);
+    c.kind = reinterpret_cast<uint8_t*>(b + 2 * ptrs + 2 * idx);
+    c.kind_t = c.kind + p.nnz_c;
+    return c;
+}
+
 }  // namespace
 
 extern "C" {
@@ -289,6 +369,95 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
     hipError_t e = sa::decode_launch(internal, head_mode, sub, (int32_t)pos, stride_l, summary_c, batch, heads, d_head,
                                      dtype, q, q_strides, k_cache, v_cache, kv_strides, softmax_scale, o, lse,
                                      workspace, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+int sparse_attn_transposed_workspace_size(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                                          int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, size_t* bytes) {
+    TransposedPlan p;
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    if (st != SA_OK) return st;
+    if (!bytes) return SA_ERR_INVALID;
+    *bytes = p.total;
+    return SA_OK;
+}
+
+int sparse_attn_fwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                               const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind, int32_t batch,
+                               int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                               const void* v, float softmax_scale, void* o, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    TransposedPlan p;
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !q || !k || !v || !o || !lse) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
+    if (workspace_bytes < p.total) return SA_ERR_BUFFER_TOO_SMALL;
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return SA_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    const ClassLayout cl = class_layout(p, ws);
+    float* lse1 = reinterpret_cast<float*>(ws + p.l1);
+    float* lse2 = reinterpret_cast<float*>(ws + p.l2);
+    hipError_t e = sa::causal_layout_launch((int32_t)p.mq, cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx,
+                                            cl.kind_t, s);
+    // the band: strided A1 over the caller's layout, into the workspace
+    const sa::AttnArgs band = make_args(p.band, batch, heads, d_head, p.strides, softmax_scale, row_ptr, col_idx,
+                                        kind, nullptr, nullptr, nullptr);
+    if (e == hipSuccess) e = sa::fwd_launch(band, dtype, q, k, v, ws + p.t3, lse1, s);
+    // the rest: queries two class steps up, dense causal per class
+    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, q, ws + p.t1, p.rows, n, d_head, 2 * (int64_t)stride_l, s);
+    const sa::AttnArgs cls = make_args(p.cls, batch * heads, stride_l, d_head, p.class_strides, softmax_scale,
+                                       cl.row_ptr, cl.col_idx, cl.kind, nullptr, nullptr, nullptr);
+    if (e == hipSuccess) e = sa::fwd_launch(cls, dtype, ws + p.t1, k, v, ws + p.t2, lse2, s);
+    if (e == hipSuccess)
+        e = sa::merge_launch(dtype, ws + p.t3, lse1, ws + p.t2, lse2, o, lse, p.rows, n, d_head, stride_l, s);
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+int sparse_attn_bwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
+                               const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                               const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                               int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
+                               const void* v, const void* o, const void* dout, const float* lse, float softmax_scale,
+                               void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+    TransposedPlan p;
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
+    if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(dq) ||
+        !aligned16(dk) || !aligned16(dv))
+        return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
+    if (workspace_bytes < p.total) return SA_ERR_BUFFER_TOO_SMALL;
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return SA_ERR_INVALID;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    const ClassLayout cl = class_layout(p, ws);
+    float* lse_c = reinterpret_cast<float*>(ws + p.l1);
+    const int64_t shift = 2 * (int64_t)stride_l;
+    hipError_t e = sa::causal_layout_launch((int32_t)p.mq, cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx,
+                                            cl.kind_t, s);
+    // the band, given the merged O and LSE: written to dq, dk, dv
+    const sa::AttnArgs band = make_args(p.band, batch, heads, d_head, p.strides, softmax_scale, row_ptr, col_idx,
+                                        kind, col_ptr, row_idx, kind_t);
+    if (e == hipSuccess) e = sa::bwd_launch(band, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws + p.bw, s);
+    // the rest: shifted copies of Q, O, dO and the class-order LSE (+inf on the padded tail)
+    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, q, ws + p.t1, p.rows, n, d_head, shift, s);
+    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, o, ws + p.t2, p.rows, n, d_head, shift, s);
+    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, dout, ws + p.t3, p.rows, n, d_head, shift, s);
+    if (e == hipSuccess) e = sa::shift_lse_launch(lse, lse_c, p.rows, n, stride_l, s);
+    const sa::AttnArgs cls = make_args(p.cls, batch * heads, stride_l, d_head, p.class_strides, softmax_scale,
+                                       cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx, cl.kind_t);
+    if (e == hipSuccess)
+        e = sa::bwd_launch(cls, dtype, ws + p.t1, k, v, ws + p.t2, ws + p.t3, lse_c, ws + p.g1, ws + p.g2,
+                           ws + p.g3, ws + p.bw, s);
+    // sums: dq of position i takes row i - 2l of the shifted copy
+    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dq, ws + p.g1, p.rows, n, d_head, shift, s);
+    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dk, ws + p.g2, p.rows, n, d_head, 0, s);
+    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dv, ws + p.g3, p.rows, n, d_head, 0, s);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

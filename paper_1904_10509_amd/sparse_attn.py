@@ -33,6 +33,9 @@ EXPORTED = (
     "sparse_attn_bwd",
     "sparse_attn_decode_workspace_size",
     "sparse_attn_decode",
+    "sparse_attn_transposed_workspace_size",
+    "sparse_attn_fwd_transposed",
+    "sparse_attn_bwd_transposed",
     "sparse_attn_status_string",
 )
 
@@ -64,6 +67,11 @@ def lib():
         _DEC = [_i64, _i32, _i32, _i32, _i32]  # pos, stride_l, summary_c, pattern, head_mode
         L.sparse_attn_decode_workspace_size.argtypes = _DEC + [_i32] * 4 + [_vp]
         L.sparse_attn_decode.argtypes = _DEC + [_i32] * 4 + [_vp] * 5 + [_f32] + [_vp] * 3 + [_sz, _vp]
+        _TR = [_i64, _i32, _i32, _i32]  # n, block, stride_l, class_block
+        L.sparse_attn_transposed_workspace_size.argtypes = _TR + [_i32] * 4 + [_vp]
+        L.sparse_attn_fwd_transposed.argtypes = _TR + [_vp] * 3 + [_i32] * 4 + [_vp] * 3 + [_f32] + [_vp] * 3 + [_sz, _vp]
+        L.sparse_attn_bwd_transposed.argtypes = (_TR + [_vp] * 6 + [_i32] * 4 + [_vp] * 6 + [_f32] + [_vp] * 4
+                                                 + [_sz, _vp])
         L.sparse_attn_status_string.argtypes = [ctypes.c_int]
         L.sparse_attn_status_string.restype = ctypes.c_char_p
         for name in EXPORTED[:-1]:
@@ -358,6 +366,73 @@ def backward_a2_transposed(q, k, v, o, dout, lse, stride_l, class_layout: Layout
     sparse_attn_bwd(*class_layout.pattern_args, *class_layout.row_args, *class_layout.col_args, b * h, stride_l,
                     d, dtype, q, k, v, o, dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
                     workspace.numel() * workspace.element_size(), stream)
+    return dq, dk, dv
+
+
+def sparse_attn_transposed_workspace_size(n, block, stride_l, class_block, batch, heads, d_head, dtype):
+    out = ctypes.c_size_t(0)
+    st = lib().sparse_attn_transposed_workspace_size(n, block, stride_l, class_block, batch, heads, d_head, dtype,
+                                                     ctypes.byref(out))
+    _check("sparse_attn_transposed_workspace_size", st)
+    return out.value
+
+
+def sparse_attn_fwd_transposed(n, block, stride_l, class_block, row_ptr, col_idx, kind, batch, heads, d_head, dtype,
+                               q, k, v, softmax_scale, o, lse, workspace, workspace_bytes, stream=None):
+    st = lib().sparse_attn_fwd_transposed(n, block, stride_l, class_block, _ptr(row_ptr), _ptr(col_idx), _ptr(kind),
+                                          batch, heads, d_head, dtype, _ptr(q), _ptr(k), _ptr(v), softmax_scale,
+                                          _ptr(o), _ptr(lse), _ptr(workspace), workspace_bytes,
+                                          _stream(stream, q.device))
+    _check("sparse_attn_fwd_transposed", st)
+
+
+def sparse_attn_bwd_transposed(n, block, stride_l, class_block, row_ptr, col_idx, kind, col_ptr, row_idx, kind_t,
+                               batch, heads, d_head, dtype, q, k, v, o, dout, lse, softmax_scale, dq, dk, dv,
+                               workspace, workspace_bytes, stream=None):
+    st = lib().sparse_attn_bwd_transposed(n, block, stride_l, class_block, _ptr(row_ptr), _ptr(col_idx), _ptr(kind),
+                                          _ptr(col_ptr), _ptr(row_idx), _ptr(kind_t), batch, heads, d_head, dtype,
+                                          _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), softmax_scale,
+                                          _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace_bytes,
+                                          _stream(stream, q.device))
+    _check("sparse_attn_bwd_transposed", st)
+
+
+def band_layout(n, block, stride_l, device="cuda", stream=None):
+    """The strided A1 layout the merged transposed path takes for its band."""
+    return build_layout(n, block, stride_l, 0, SA_STRIDED, SA_MODE_A1, device=device, stream=stream)
+
+
+def _transposed_workspace(q, band: Layout, class_block, workspace):
+    b, h, n, d = q.shape
+    need = sparse_attn_transposed_workspace_size(n, band.block, band.stride_l, class_block, b, h, d, _dtype_code(q))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def forward_merged_transposed(q, k, v, band: Layout, class_block, softmax_scale=None, out=None, lse=None,
+                              workspace=None, stream=None):
+    """O and LSE of strided merged attention, A2 by transposition; contiguous [b, h, n, d] tensors."""
+    b, h, n, d = q.shape
+    if band.pattern != SA_STRIDED or band.head_mode != SA_MODE_A1 or band.n != n:
+        raise ValueError("band must be the strided A1 layout of this n")
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if lse is None else lse
+    ws, nbytes = _transposed_workspace(q, band, class_block, workspace)
+    sparse_attn_fwd_transposed(n, band.block, band.stride_l, class_block, *band.row_args, b, h, d, _dtype_code(q),
+                               q, k, v, _scale(softmax_scale, d), o, lse, ws, nbytes, stream)
+    return o, lse
+
+
+def backward_merged_transposed(q, k, v, o, dout, lse, band: Layout, class_block, softmax_scale=None, grads=None,
+                               workspace=None, stream=None):
+    """dq, dk, dv of strided merged attention, A2 by transposition."""
+    b, h, n, d = q.shape
+    dq, dk, dv = grads if grads is not None else (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    ws, nbytes = _transposed_workspace(q, band, class_block, workspace)
+    sparse_attn_bwd_transposed(n, band.block, band.stride_l, class_block, *band.row_args, *band.col_args, b, h, d,
+                               _dtype_code(q), q, k, v, o, dout, lse, _scale(softmax_scale, d), dq, dk, dv, ws,
+                               nbytes, stream)
     return dq, dk, dv
 
 

@@ -217,3 +217,51 @@ def test_decode_workspace_and_errors(L):
     assert call(scale=-1.0) == sa.SA_ERR_INVALID
     assert call(wsb=need - 1) == sa.SA_ERR_BUFFER_TOO_SMALL
     assert call(ws=None) == sa.SA_ERR_INVALID
+
+
+def test_transposed_workspace_and_errors(L):
+    """Workspace of the merged transposed path: a dense causal class layout, six
+    tensors of the input's size (shifted Q, O, dO; partial gradients), two
+    fp32 row statistics, and the larger of the two backward workspaces, each
+    region 256-byte aligned."""
+    def a256(x):
+        return (x + 255) // 256 * 256
+
+    def bwd_ws(rows, nq):
+        return (8 * rows + 15) // 16 * 16 + 8 * 8 + 4 + 2 * 4 * nq
+
+    out = ctypes.c_size_t(0)
+    n, B, l, CB, b, h, d = 12288, 64, 128, 32, 2, 8, 64
+    assert L.sparse_attn_transposed_workspace_size(n, B, l, CB, b, h, d, sa.SA_BF16, ctypes.byref(out)) == 0
+    rows, mq = b * h * n, (n // l) // CB
+    nnz_c = mq * (mq + 1) // 2
+    expect = (a256(2 * (mq + 1) * 4 + 2 * nnz_c * 5 + 64) + 6 * a256(rows * d * 2) + 2 * a256(rows * 4)
+              + a256(max(bwd_ws(rows, n // B), bwd_ws(rows, mq))))
+    assert out.value == expect
+    bad = [
+        ((12288, 64, 100, 32, 2, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # l does not divide n
+        ((12288, 64, 128, 24, 2, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # class block not supported
+        ((12288, 64, 256, 64, 2, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # 48 class positions, blocks of 64
+        ((12288, 64, 128, 32, 2, 8, 48, sa.SA_BF16), sa.SA_ERR_UNSUPPORTED),  # d
+        ((12288, 64, 128, 32, 0, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # batch
+        ((12288, 64, 128, 32, 256, 256, 64, sa.SA_BF16), sa.SA_ERR_UNSUPPORTED),  # batch * heads > 65,535
+        ((2 ** 20 * 16, 64, 16, 16, 1, 1, 64, sa.SA_BF16), sa.SA_ERR_UNSUPPORTED),  # 65,536 class block rows
+    ]
+    for args, expect in bad:
+        assert L.sparse_attn_transposed_workspace_size(*args, ctypes.byref(out)) == expect, args
+    assert L.sparse_attn_transposed_workspace_size(n, B, l, CB, b, h, d, sa.SA_BF16, None) == sa.SA_ERR_INVALID
+    # validation before any launch: workspace size and alignment, scale, pointers (fake device pointers)
+    L.sparse_attn_transposed_workspace_size(n, B, l, CB, b, h, d, sa.SA_BF16, ctypes.byref(out))
+    need = out.value
+    fwd = [n, B, l, CB] + [FAKE] * 3 + [b, h, d, sa.SA_BF16] + [FAKE] * 3 + [0.125] + [FAKE] * 2
+    assert L.sparse_attn_fwd_transposed(*fwd, FAKE, need - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
+    assert L.sparse_attn_fwd_transposed(*fwd, FAKE + 16, need, None) == sa.SA_ERR_INVALID  # not 256-aligned
+    assert L.sparse_attn_fwd_transposed(*fwd, None, need, None) == sa.SA_ERR_INVALID
+    bad_scale = list(fwd)
+    bad_scale[14] = 0.0
+    assert L.sparse_attn_fwd_transposed(*bad_scale, FAKE, need, None) == sa.SA_ERR_INVALID
+    bwd = [n, B, l, CB] + [FAKE] * 6 + [b, h, d, sa.SA_BF16] + [FAKE] * 6 + [0.125] + [FAKE] * 3
+    assert L.sparse_attn_bwd_transposed(*bwd, FAKE, need - 1, None) == sa.SA_ERR_BUFFER_TOO_SMALL
+    no_col = list(bwd)
+    no_col[7] = None
+    assert L.sparse_attn_bwd_transposed(*no_col, FAKE, need, None) == sa.SA_ERR_INVALID

@@ -53,3 +53,68 @@ def test_transposed_a2_equals_block_path_closely():
     o_b, _ = sa.forward(q, k, v, sa.build_layout(n, 64, l, 0, sa.SA_STRIDED, sa.SA_MODE_A2, device=dev))
     torch.cuda.synchronize()
     assert max_err(to64(o_t), to64(o_b)) <= 2e-2
+
+
+# Merged strided heads (A1 u A2) with A2 by transposition: the band through the
+# strided A1 layout, the rest ({i - k l : k >= 2}) per residue class, merged
+# through their log-sum-exps, against the oracle's merged strided pattern.
+# (n, l, band block, class block, d, dtype, batch, heads)
+MERGED_CASES = [
+    (512, 16, 16, 32, 64, torch.float32, 1, 2),
+    (1024, 16, 32, 16, 32, torch.bfloat16, 1, 3),
+    (2048, 64, 64, 32, 64, torch.bfloat16, 2, 2),
+    (4096, 64, 64, 64, 128, torch.bfloat16, 1, 2),
+    (4096, 256, 64, 16, 64, torch.bfloat16, 1, 2),  # 16 positions per class: one class block
+    (1600, 25, 16, 32, 64, torch.bfloat16, 1, 2),   # a stride that is not a multiple of the block
+    (512, 8, 16, 64, 128, torch.float32, 2, 1),
+]
+
+
+def run_merged(x, n, l, B, CB, scale, dev):
+    q, k, v, dout = (x[name].to(dev) for name in ("q", "k", "v", "dout"))
+    band = sa.band_layout(n, B, l, device=dev)
+    o, lse = sa.forward_merged_transposed(q, k, v, band, CB, scale)
+    dq, dk, dv = sa.backward_merged_transposed(q, k, v, o, dout, lse, band, CB, scale)
+    torch.cuda.synchronize()
+    return {"o": to64(o), "lse": to64(lse), "dq": to64(dq), "dk": to64(dk), "dv": to64(dv)}
+
+
+@pytest.mark.parametrize("n,l,B,CB,d,dtype,batch,heads", MERGED_CASES)
+def test_merged_transposed_matches_oracle(n, l, B, CB, d, dtype, batch, heads):
+    dev = device()
+    x = make_inputs(batch, heads, n, d, dtype, seed=n + l + CB + d + 3)
+    scale = d ** -0.5
+    got = run_merged(x, n, l, B, CB, scale, dev)
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=sa.SA_STRIDED, mode=sa.SA_MODE_MERGED, l=l, c=0, scale=scale)
+    for name in ("o", "dq", "dk", "dv"):
+        assert max_err(got[name], ref[name]) <= TOL[dtype], (name, max_err(got[name], ref[name]))
+    assert max_err(got["lse"], ref["lse"]) <= LSE_TOL[dtype]
+
+
+def test_merged_transposed_text_workload_sampled():
+    """The text workload (12,288 positions, l = 128, 2 x 8 heads of 64): sampled
+    rows and columns against the oracle, and all outputs against the block
+    path over the merged layout within the bf16 tolerance."""
+    from paper_1904_10509_amd.inputs import WORKLOADS, workload_inputs
+    from gpu_util import run_gpu
+    dev = device()
+    w = WORKLOADS["strided_n12288_l128_merged"]
+    x = workload_inputs(w)
+    got = run_merged(x, w.n, w.stride, w.block, 32, w.scale, dev)
+    blk = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=0, pattern=w.pattern, mode=w.mode, scale=w.scale)
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        assert max_err(got[name], blk[name]) <= 2e-2, (name, max_err(got[name], blk[name]))
+    rng = np.random.default_rng(5)
+    idx = [0, 1, 127, 128, 129, 255, 256, 257, 6000, w.n - 1] + list(rng.integers(0, w.n, 30))
+    sel = np.stack([rng.integers(0, w.batch, len(idx)), rng.integers(0, w.heads, len(idx)), np.array(idx)], axis=1)
+    xi = oracle_inputs(x)
+    kw = dict(pattern=w.pattern, mode=w.mode, l=w.stride, c=0, scale=w.scale)
+    o, lse = orc_mod.forward_rows(*xi[:3], sel, **kw)
+    dq = orc_mod.backward_rows(*xi, sel, **kw)
+    dk, dv = orc_mod.backward_cols(*xi, sel, **kw)
+    r = (sel[:, 0], sel[:, 1], sel[:, 2])
+    assert max_err(got["o"][r], o) <= 2e-2
+    assert max_err(got["lse"][r], lse) <= 1e-3
+    assert max_err(got["dq"][r], dq) <= 2e-2
+    assert max_err(got["dk"][r], dk) <= 2e-2
+    assert max_err(got["dv"][r], dv) <= 2e-2
