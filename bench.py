@@ -298,16 +298,20 @@ TRANSPOSED = {
 
 
 def transposed_bench(args):
-    """Forward + backward time of strided A2 attention, block-sparse against
-    transposed, with FLOPs counted per attended pair (14 d per pair and head:
-    4 d forward, 10 d backward), the honest count for both."""
+    """Forward + backward time of strided A2 attention and of strided merged
+    attention (A1 u A2), block-sparse against transposed, with FLOPs counted
+    per attended pair (14 d per pair and head: 4 d forward, 10 d backward),
+    the honest count for both."""
     import torch
+
+    import numpy as np
 
     from paper_1904_10509_amd import sparse_attn as sa
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    out = {"metric": "strided A2 fwd+bwd: block-sparse vs transposed (Sec. 5.5)", "unit": "ms", "dtype": "bf16",
+    out = {"metric": "strided A2 and merged fwd+bwd: block-sparse vs transposed (Sec. 5.5)", "unit": "ms",
+           "dtype": "bf16",
            "data": "synthetic", "steps": args.steps, "warmup": args.warmup, "shapes": {}}
     for name, c in TRANSPOSED.items():
         g = torch.Generator(device=dev).manual_seed(c["seed"])
@@ -354,7 +358,50 @@ def transposed_bench(args):
         res["transposed"]["class_layout_blocks"] = lay_t.nnz
         res["speedup"] = res["block"]["ms"] / res["transposed"]["ms"]
         res["attended_pairs"] = pairs
+        del lay_b, lay_t, ws_b, ws_t, lse_t
+
+        # merged heads: the merged layout against the band + transposed rest
+        i = np.arange(c["n"], dtype=np.int64)
+        m_pairs = int((np.minimum(i, c["l"]) + 1 + np.maximum(0, i // c["l"] - 1)).sum()) * c["batch"] * c["heads"]
+        m_flop = 14.0 * c["d"] * m_pairs
+        lay_m = sa.build_layout(c["n"], c["block"], c["l"], 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, device=dev)
+        band = sa.band_layout(c["n"], c["block"], c["l"], device=dev)
+        ws_m = torch.empty(max(16, sa.sparse_attn_bwd_workspace_size(*lay_m.pattern_args, c["batch"], c["heads"],
+                                                                     c["d"], sa.SA_BF16)), dtype=torch.uint8,
+                           device=dev)
+        ws_mt = torch.empty(sa.sparse_attn_transposed_workspace_size(c["n"], c["block"], c["l"], c["class_block"],
+                                                                     c["batch"], c["heads"], c["d"], sa.SA_BF16),
+                            dtype=torch.uint8, device=dev)
+
+        def merged_block_step():
+            sa.forward(q, k, v, lay_m, out=o, lse=lse_b)
+            sa.backward(q, k, v, o, dout, lse_b, lay_m, grads=grads, workspace=ws_m)
+
+        def merged_transposed_step():
+            sa.forward_merged_transposed(q, k, v, band, c["class_block"], out=o, lse=lse_b, workspace=ws_mt)
+            sa.backward_merged_transposed(q, k, v, o, dout, lse_b, band, c["class_block"], grads=grads,
+                                          workspace=ws_mt)
+
+        merged = {}
+        for kind, fn in (("block", merged_block_step), ("transposed", merged_transposed_step)):
+            for _ in range(args.warmup):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            merged[kind] = {"ms": ms, "pair_tflops": m_flop / (ms * 1e-3) / 1e12}
+        merged["block"]["layout_blocks"] = lay_m.nnz
+        merged["transposed"]["band_layout_blocks"] = band.nnz
+        merged["speedup"] = merged["block"]["ms"] / merged["transposed"]["ms"]
+        merged["attended_pairs"] = m_pairs
+        res["merged"] = merged
         out["shapes"][name] = res
+        del lay_m, band, ws_m, ws_mt
         del q, k, v, dout, o, grads
         torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)

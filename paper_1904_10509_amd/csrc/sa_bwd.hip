@@ -494,7 +494,25 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
         qx = (int)(xcc % kQueues);
     }
+    // Thread 0 claims slots from the queues with one atomic per slot.  With
+    // claim_chunk = 0 (short columns, a few blocks each) there are no
+    // atomics: the atomics of all workgroups on a counter are serialised
+    // device-wide, and a claim would wait longer than the column takes.
+    // Workgroup w then takes the slots w, w + G, w + 2G, ... (G workgroups)
+    // of the rank-major order (every (batch, head) of the longest columns
+    // first), encoded as queue slots.
+    const bool fixed_slots = a.claim_chunk == 0;
+    uint64_t next_slot = blockIdx.x;
     auto claim = [&]() -> unsigned long long {
+        if (fixed_slots) {
+            if (next_slot >= per_layout * (uint64_t)bh_count) return kNoWork;
+            const uint64_t s = next_slot;
+            next_slot += gridDim.x;
+            const uint64_t rank = s / (uint64_t)bh_count;
+            const int bh = (int)(s - rank * (uint64_t)bh_count);
+            const int x = bh % kQueues;
+            return ((uint64_t)x << 56) | (rank * (uint64_t)queue_heads(bh_count, x) + (uint64_t)(bh / kQueues));
+        }
         while (q_left > 0) {
             const uint64_t t = atomicAdd(queue + qx, 1ull);
             if (t < per_layout * (uint64_t)queue_heads(bh_count, qx)) return ((uint64_t)qx << 56) | t;
@@ -978,6 +996,12 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                        (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
+    // dK / dV work in a fixed order, without atomics (see the kernel), where
+    // column lengths change smoothly (strided: a band and a stride's worth of
+    // rows per column) or columns are a few blocks long; claimed from the
+    // queues where they swing (fixed: long summary columns among short ones)
+    AttnArgs ak = a;
+    ak.claim_chunk = (a.pattern == STRIDED || a.nq <= 8) ? 0 : 1;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
         with_full_body<PAT>(a, [&](auto fb) {
@@ -991,7 +1015,7 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
         hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK, PAT>::NT), 0,
-                           stream, a, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
+                           stream, ak, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
                            (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,
                            ws.queue, ws.items, ws.order);
         return hipGetLastError();

@@ -61,6 +61,7 @@ struct AttnArgs {
     uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
     uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64, subblock 0)
     int32_t sub;           // fixed: 0 = one summary window for all heads, else floor(l / c) subblocks
+    int32_t claim_chunk;   // dK / dV: 1 = slots claimed by atomics, 0 = fixed order (set by the backward launcher)
     DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;
