@@ -494,24 +494,39 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
         qx = (int)(xcc % kQueues);
     }
-    // Thread 0 claims slots from the queues with one atomic per slot.  With
-    // claim_chunk = 0 (short columns, a few blocks each) there are no
-    // atomics: the atomics of all workgroups on a counter are serialised
-    // device-wide, and a claim would wait longer than the column takes.
-    // Workgroup w then takes the slots w, w + G, w + 2G, ... (G workgroups)
-    // of the rank-major order (every (batch, head) of the longest columns
-    // first), encoded as queue slots.
-    const bool fixed_slots = a.claim_chunk == 0;
-    uint64_t next_slot = blockIdx.x;
+    // How thread 0 finds the next slot (a.claim_mode, chosen by the launcher):
+    //   CLAIM_QUEUES: from the queue counters, one atomic per slot, stealing
+    //     from the other queues once its own is dry;
+    //   CLAIM_ROUND_ROBIN: workgroup w takes the slots w, w + G, w + 2G, ... (G
+    //     workgroups) of the rank-major order (every (batch, head) of the
+    //     longest columns first), with no atomics;
+    //   CLAIM_SERPENTINE: workgroup w serves head w mod (batch heads) alone and
+    //     takes that head's ranks in serpentine order over the J workgroups of
+    //     the head (j, 2J - 1 - j, 2J + j, ...), which evens out the sums of
+    //     sorted column lengths, with no atomics.
+    // The atomics of all workgroups on one counter are serialised
+    // device-wide; with many short columns a claim waits longer than a column
+    // takes, hence the fixed orders.  Every mode yields queue-encoded slots.
+    uint64_t next_slot = blockIdx.x, sweep = 0;
+    auto encode = [&](uint64_t rank, int bh) -> unsigned long long {
+        const int x = bh % kQueues;
+        return ((uint64_t)x << 56) | (rank * (uint64_t)queue_heads(bh_count, x) + (uint64_t)(bh / kQueues));
+    };
     auto claim = [&]() -> unsigned long long {
-        if (fixed_slots) {
+        if (a.claim_mode == CLAIM_ROUND_ROBIN) {
             if (next_slot >= per_layout * (uint64_t)bh_count) return kNoWork;
             const uint64_t s = next_slot;
             next_slot += gridDim.x;
             const uint64_t rank = s / (uint64_t)bh_count;
-            const int bh = (int)(s - rank * (uint64_t)bh_count);
-            const int x = bh % kQueues;
-            return ((uint64_t)x << 56) | (rank * (uint64_t)queue_heads(bh_count, x) + (uint64_t)(bh / kQueues));
+            return encode(rank, (int)(s - rank * (uint64_t)bh_count));
+        }
+        if (a.claim_mode == CLAIM_SERPENTINE) {
+            const int bh = (int)(blockIdx.x % (uint64_t)bh_count);
+            const uint64_t j = blockIdx.x / (uint64_t)bh_count;
+            const uint64_t J = (gridDim.x - bh + bh_count - 1) / bh_count;  // workgroups of this head
+            const uint64_t k = sweep++;
+            const uint64_t rank = k * J + ((k & 1) ? J - 1 - j : j);
+            return rank < per_layout ? encode(rank, bh) : kNoWork;
         }
         while (q_left > 0) {
             const uint64_t t = atomicAdd(queue + qx, 1ull);
@@ -996,12 +1011,7 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                        (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
-    // dK / dV work in a fixed order, without atomics (see the kernel), where
-    // column lengths change smoothly (strided: a band and a stride's worth of
-    // rows per column) or columns are a few blocks long; claimed from the
-    // queues where they swing (fixed: long summary columns among short ones)
     AttnArgs ak = a;
-    ak.claim_chunk = (a.pattern == STRIDED || a.nq <= 8) ? 0 : 1;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
         with_full_body<PAT>(a, [&](auto fb) {
@@ -1014,6 +1024,14 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         const int64_t slots = resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>>(DkvCfg<D, BLK, PAT>::NT);
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
+        // order of the dK / dV work (see the kernel): a fixed order where column
+        // lengths change smoothly (strided: a band and a stride's worth of rows
+        // per column) or columns are a few blocks long; serpentine per head
+        // where long summary columns alternate with short ones (fixed) and each
+        // head has a few workgroups; the queues otherwise
+        const int64_t bh_count = (int64_t)a.batch * a.heads;
+        ak.claim_mode = (PAT == STRIDED || a.nq <= 8) ? CLAIM_ROUND_ROBIN
+                        : (bh_count * 4 <= (int64_t)qgrid ? CLAIM_SERPENTINE : CLAIM_QUEUES);
         hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK, PAT>::NT), 0,
                            stream, ak, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
                            (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,

@@ -49,6 +49,9 @@ inline hipError_t with_pattern_mode(int pattern, int mode, F&& f) {
     }
 }
 
+// Orders in which the dK / dV kernel takes its work.
+enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2 };
+
 // Everything a kernel needs to know about one call.
 struct AttnArgs {
     int32_t pattern, mode;
@@ -61,7 +64,7 @@ struct AttnArgs {
     uint64_t period_bits;  // bits at multiples of l below 64 (strided masks)
     uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64, subblock 0)
     int32_t sub;           // fixed: 0 = one summary window for all heads, else floor(l / c) subblocks
-    int32_t claim_chunk;   // dK / dV: 1 = slots claimed by atomics, 0 = fixed order (set by the backward launcher)
+    int32_t claim_mode;    // dK / dV work order, one of CLAIM_* (set by the backward launcher)
     DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;
