@@ -117,6 +117,25 @@ def test_parity_small(pattern, mode, n, B, l, c, d, dtype, batch, heads):
     assert max_err(got["lse"], ref["lse"]) <= LSE_TOL[dtype], max_err(got["lse"], ref["lse"])
 
 
+def test_parity_dkdv_work_orders():
+    """The dK / dV kernel takes its work in one of three orders: round-robin
+    (strided, or columns of at most 8 blocks), serpentine per head (fixed, at
+    least four workgroups per (batch, head)) and atomic queues (fixed with
+    more (batch, head) pairs than a quarter of the resident workgroups).  The
+    last needs many heads: 16 x 16 here.  Each order must cover every column
+    exactly once, so all must match the oracle."""
+    dev = device()
+    for pattern, n, B, l, c, batch, heads in [(F, 1024, 64, 128, 32, 16, 16),   # queues
+                                               (F, 1024, 64, 128, 32, 1, 3),    # serpentine
+                                               (S, 1024, 64, 128, 0, 2, 5),     # round-robin
+                                               (F, 512, 64, 128, 32, 2, 2)]:    # 8 key blocks: round-robin
+        x = make_inputs(batch, heads, n, 32, torch.bfloat16, seed=batch * heads + n)
+        got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=MG, scale=32 ** -0.5, dev=dev)
+        ref = orc_mod.backward(*oracle_inputs(x), pattern=pattern, mode=MG, l=l, c=c, scale=32 ** -0.5)
+        for name in ("o", "dq", "dk", "dv"):
+            assert max_err(got[name], ref[name]) <= 2e-2, (pattern, batch, heads, name, max_err(got[name], ref[name]))
+
+
 def test_workload_fp32_full():
     w = WORKLOADS["strided_n256_l16_f32"]
     x = workload_inputs(w)
