@@ -20,15 +20,18 @@
 // key blocks holding summary columns are long), and a hardware placement of
 // one workgroup per column can then pile the long columns onto a few compute
 // units.  The dkdv grid is therefore sized to the resident capacity of the
-// device and workgroups claim columns from atomic counters in the workspace:
-//   - one queue per XCD (the die whose L2 serves the workgroup), holding the
-//     heads bh = x (mod 8), so the columns of a head share one L2;
-//   - inside a queue, longest columns first (the pre kernel sorts the key
-//     blocks of each layout by column length into length classes), so the
-//     long columns of a head start together and walk the same Q / dO tiles
-//     at about the same time;
-//   - a workgroup whose own queue is empty takes work from the others, so
-//     every column is processed whatever the placement of workgroups is.
+// device, the pre kernel sorts the key blocks of each layout by column length
+// (longest first, so the long columns of a head start together and walk the
+// same Q / dO tiles at about the same time), and each workgroup takes its
+// columns in one of three orders chosen per call:
+//   - serpentine per head (fixed pattern, a few workgroups per head): one
+//     head per workgroup, ranks j, 2J - 1 - j, 2J + j, ... over the head's J
+//     workgroups, which evens out the sums of the sorted lengths;
+//   - round-robin over the rank-major order (strided pattern, short columns);
+//   - atomic counters, one queue per XCD holding the heads bh = x (mod 8),
+//     with stealing once a queue is dry (the remaining cases).
+// The first two use no atomics: claims on one counter are serialised across
+// the device and, with short columns, take longer than the columns.
 // The dq kernel repeats the S and dP products of the dkdv kernel; those two
 // extra products per block are the price of having no reduction across
 // workgroups.
