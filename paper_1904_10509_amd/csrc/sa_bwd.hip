@@ -261,6 +261,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     wait_loads_upto<0>();  // register loads done before the ring starts
     // two-stage ring; the next step's blocks are read one step ahead
     RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    // strided blocks away from the band are single diagonals (see the step)
+    const bool diag_far = PAT == STRIDED && mp.part != PART_A1 && a.l % BLK == 0;
     RowStep cur = steps.next();
     if (cur.a >= 0) load_step(cur, 0);
     TileReader<D> rd;
@@ -279,6 +281,38 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
+        if constexpr (PAT == STRIDED) {
+            // a single diagonal (see the forward): per row one score, one dS and
+            // dQ += dS k as a rank-1 step in registers
+            if (diag_far && far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    const int kk = w * C::RW + 16 * u + r;  // this lane's row, and its key, in the block
+                    float sp = 0.f, dpp = 0.f;
+#pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) {
+                        const bf16x8 kv = ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g));
+                        const bf16x8 vv = ld_bf16x8(tV + Swz<D>::off(kk, 32 * ks + 8 * g));
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            sp = fmaf((float)qf[u][ks][e], (float)kv[e], sp);
+                            dpp = fmaf((float)of[u][ks][e], (float)vv[e], dpp);
+                        }
+                    }
+                    const float pr = exp2_fast(fmaf(sum_over_g(sp), c2, nl2[u]));
+                    const float ds = pr * (sum_over_g(dpp) + nd4[u][0]);
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        const bf16x4 kq =
+                            __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(tK + Swz<D>::off(kk, 16 * db + 4 * g)));
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) dqacc[u][db][t] = fmaf(ds, (float)kq[t], dqacc[u][db][t]);
+                    }
+                }
+                cur = nxt;
+                return true;
+            }
+        }
         // With FULL_BODY the step body exists twice: for blocks attended
         // everywhere (every chunk class a compile-time ALL, no mask and no
         // branch on classes) and for the others (see with_full_body).
@@ -613,6 +647,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 ++near;
             len = near;
         }
+        // strided blocks away from the band are single diagonals (see the step)
+        const bool diag_far = PAT == STRIDED && mp.part != PART_A1 && a.l % BLK == 0;
         // The column is walked from its last query block down: the long
         // columns of a head, started together, then visit the same query
         // blocks at about the same time and share those Q / dO tiles in L2.
@@ -645,6 +681,43 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint16_t* tO = sdO[st];
             const float* tL = sL[st];
             const float* tD = sDl[st];
+            if constexpr (PAT == STRIDED) {
+                // a single diagonal (see the forward): key kk of the block meets
+                // query kk only, so dV += p dO and dK += dS q are rank-1 steps in
+                // registers
+                if (diag_far && far_block(PAT, a.dl, i0, kb * BLK, BLK)) {
+#pragma unroll
+                    for (int kbw = 0; kbw < C::KBW; ++kbw) {
+                        const int kk = 16 * kgrp(kbw) + r;  // this lane's key, and its query, in the block
+                        float sp = 0.f, dpp = 0.f;
+#pragma unroll
+                        for (int ks = 0; ks < C::KS; ++ks) {
+                            const bf16x8 qv = ld_bf16x8(tQ + Swz<D>::off(kk, 32 * ks + 8 * g));
+                            const bf16x8 ov = ld_bf16x8(tO + Swz<D>::off(kk, 32 * ks + 8 * g));
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) {
+                                sp = fmaf((float)kf[kbw][ks][e], (float)qv[e], sp);
+                                dpp = fmaf((float)vf[kbw][ks][e], (float)ov[e], dpp);
+                            }
+                        }
+                        const float pr = exp2_fast(fmaf(sum_over_g(sp), c2, tL[kk]));
+                        const float ds = pr * (sum_over_g(dpp) + tD[kk]);
+#pragma unroll
+                        for (int db = 0; db < C::DB; ++db) {
+                            const bf16x4 oq = __builtin_bit_cast(
+                                bf16x4, *reinterpret_cast<const uint2*>(tO + Swz<D>::off(kk, 16 * db + 4 * g)));
+                            const bf16x4 qq = __builtin_bit_cast(
+                                bf16x4, *reinterpret_cast<const uint2*>(tQ + Swz<D>::off(kk, 16 * db + 4 * g)));
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) {
+                                dvacc[kbw][db][t] = fmaf(pr, (float)oq[t], dvacc[kbw][db][t]);
+                                dkacc[kbw][db][t] = fmaf(ds, (float)qq[t], dkacc[kbw][db][t]);
+                            }
+                        }
+                    }
+                    return;
+                }
+            }
             // The step body exists twice: for blocks attended everywhere (every
             // chunk class a compile-time ALL unless a half item leaves a query
             // half to the other waves, no mask) and for the others, in both

@@ -113,6 +113,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     // two-stage ring; the next step's blocks are read one step ahead (scalar
     // loads, off the vector-memory counter the ring waits on)
     RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    // strided blocks away from the band are single diagonals (see the step)
+    const bool diag_far = PAT == STRIDED && mp.part != PART_A1 && a.l % BLK == 0;
     RowStep cur = steps.next();
     if (cur.a >= 0) load_step(cur, 0);
     TileReader<D> rd;
@@ -131,6 +133,41 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
         const uint16_t* tK = sK[st];
         const uint16_t* tV = sV[st];
+        if constexpr (PAT == STRIDED) {
+            // A strided block away from the band, with l a multiple of B, holds
+            // exactly its main diagonal (row i0 + t attends key j0 + t): each row
+            // gains one score, so the online softmax takes a rank-1 step in
+            // registers, q . k and O += p v, instead of a masked chunk of
+            // products.
+            if (diag_far && far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+#pragma unroll
+                for (int u = 0; u < C::QBW; ++u) {
+                    const int kk = w * C::RW + 16 * u + r;  // this lane's row, and its key, in the block
+                    float part = 0.f;
+#pragma unroll
+                    for (int ks = 0; ks < C::KS; ++ks) {
+                        const bf16x8 kv = ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g));
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) part = fmaf((float)qf[u][ks][e], (float)kv[e], part);
+                    }
+                    const float sc = sum_over_g(part);
+                    const float m_new = fmaxf(m_run[u], sc);
+                    const float alpha = exp2_fast((m_run[u] - m_new) * c2);  // 0 while m was -inf
+                    const float pr = exp2_fast((sc - m_new) * c2);
+                    l_run[u] = fmaf(l_run[u], alpha, g == 0 ? pr : 0.f);  // one lane of the row counts p
+                    m_run[u] = m_new;
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        const bf16x4 vv =
+                            __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(tV + Swz<D>::off(kk, 16 * db + 4 * g)));
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) oacc[u][db][t] = fmaf(oacc[u][db][t], alpha, pr * (float)vv[t]);
+                    }
+                }
+                cur = nxt;
+                return true;
+            }
+        }
         // With FULL_BODY the step body exists twice: for blocks attended
         // everywhere (every chunk class a compile-time ALL, no mask and no
         // branch on classes) and for the others (see with_full_body).
