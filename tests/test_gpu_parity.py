@@ -87,6 +87,14 @@ SMALL_CASES = [
     # more (batch, head) pairs than the dK / dV kernel has queues, not a multiple of them
     (S, MG, 256, 32, 32, 0, 32, torch.bfloat16, 3, 5),
     (F, IL, 256, 16, 64, 16, 32, torch.bfloat16, 3, 3),
+    # strided with l a multiple of B: blocks before the band are single
+    # diagonals, taken as rank-1 steps (A2 alone, merged, alternating heads,
+    # B = 16 / 32 / 64, d = 32 / 64 / 128, l = B and l = 4B)
+    (S, A2, 512, 32, 64, 0, 64, torch.bfloat16, 1, 2),
+    (S, IL, 768, 64, 128, 0, 128, torch.bfloat16, 2, 2),
+    (S, MG, 1024, 16, 32, 0, 32, torch.bfloat16, 1, 2),
+    (S, MG, 1024, 64, 256, 0, 64, torch.bfloat16, 1, 3),
+    (S, A2, 1024, 64, 64, 0, 128, torch.bfloat16, 2, 1),
     # a distinct summary subblock per head, heads covering every subblock: with
     # B = 64 and c = 32 the windows alternate between the upper and the lower
     # halves of blocks (pairs of upper or of lower halves, split key blocks of
