@@ -452,3 +452,26 @@ class SparseAttention(torch.autograd.Function):
         q, k, v, o, lse = ctx.saved_tensors
         dq, dk, dv = backward(q, k, v, o, dout.contiguous(), lse, ctx.layout, ctx.softmax_scale)
         return dq, dk, dv, None, None
+
+
+class SparseAttentionTransposed(torch.autograd.Function):
+    """Autograd wrapper of strided merged attention with A2 by transposition
+    (band = the strided A1 layout, class_block = the block of the per-class
+    dense causal attention); saves O and LSE, recomputes the weights."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, band, class_block, softmax_scale=None):
+        q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+        o, lse = forward_merged_transposed(q, k, v, band, class_block, softmax_scale)
+        ctx.save_for_backward(q, k, v, o, lse)
+        ctx.band = band
+        ctx.class_block = class_block
+        ctx.softmax_scale = softmax_scale
+        return o
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, o, lse = ctx.saved_tensors
+        dq, dk, dv = backward_merged_transposed(q, k, v, o, dout.contiguous(), lse, ctx.band, ctx.class_block,
+                                                ctx.softmax_scale)
+        return dq, dk, dv, None, None, None

@@ -118,3 +118,18 @@ def test_merged_transposed_text_workload_sampled():
     assert max_err(got["dq"][r], dq) <= 2e-2
     assert max_err(got["dk"][r], dk) <= 2e-2
     assert max_err(got["dv"][r], dv) <= 2e-2
+
+
+def test_merged_transposed_autograd_wrapper():
+    dev = device()
+    n, l, B, CB, d = 1024, 32, 32, 32, 64
+    x = make_inputs(1, 2, n, d, torch.bfloat16, seed=27)
+    band = sa.band_layout(n, B, l, device=dev)
+    q, k, v = (x[name].to(dev).requires_grad_(True) for name in ("q", "k", "v"))
+    o = sa.SparseAttentionTransposed.apply(q, k, v, band, CB, None)
+    (o.float() * x["dout"].to(dev).float()).sum().backward()
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=sa.SA_STRIDED, mode=sa.SA_MODE_MERGED, l=l, c=0,
+                           scale=d ** -0.5)
+    assert max_err(to64(o), ref["o"]) <= 2e-2
+    for name, t in (("dq", q), ("dk", k), ("dv", v)):
+        assert max_err(to64(t.grad), ref[name]) <= 2e-2, name
