@@ -67,6 +67,7 @@ MERGED_CASES = [
     (4096, 256, 64, 16, 64, torch.bfloat16, 1, 2),  # 16 positions per class: one class block
     (1600, 25, 16, 32, 64, torch.bfloat16, 1, 2),   # a stride that is not a multiple of the block
     (512, 8, 16, 64, 128, torch.float32, 2, 1),
+    (256, 1, 16, 64, 32, torch.bfloat16, 1, 2),     # l = 1: one class, the whole sequence
 ]
 
 
