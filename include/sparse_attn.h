@@ -30,7 +30,9 @@
  *   - Device pointers point to memory allocated by the caller; the library
  *     allocates no device memory and keeps no mutable global state.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *     Device work is enqueued asynchronously; nothing synchronizes.
+ *     Device work is enqueued asynchronously; nothing synchronizes.  The
+ *     device work of a call is kernel launches only (no memset, no
+ *     allocation), so it can be captured into a HIP graph.
  *   - Every argument is validated before anything is enqueued.  On error a
  *     negative sa_status is returned and no work is enqueued.  After the
  *     launches, a HIP launch error is reported as SA_ERR_HIP.  The library
