@@ -134,3 +134,38 @@ def test_merged_transposed_autograd_wrapper():
     assert max_err(to64(o), ref["o"]) <= 2e-2
     for name, t in (("dq", q), ("dk", k), ("dv", v)):
         assert max_err(to64(t.grad), ref[name]) <= 2e-2, name
+
+
+def test_merged_transposed_n1048576_sampled():
+    """The audio shape (1,048,576 positions, l = 1,024, 4 heads of 64, classes
+    of 1,024 in blocks of 64): sampled rows and columns against the oracle's
+    merged strided pattern, gathered on the device."""
+    from paper_1904_10509_amd.inputs import WORKLOADS, workload_inputs
+    w = WORKLOADS["strided_n1048576_l1024_merged"]
+    dev = device()
+    x = workload_inputs(w)
+    q, k, v, dout = (x[name].to(dev) for name in ("q", "k", "v", "dout"))
+    band = sa.band_layout(w.n, w.block, w.stride, device=dev)
+    o, lse = sa.forward_merged_transposed(q, k, v, band, 64, w.scale)
+    dq, dk, dv = sa.backward_merged_transposed(q, k, v, o, dout, lse, band, 64, w.scale)
+    torch.cuda.synchronize()
+    for t in (o, dq, dk, dv):
+        assert bool(torch.isfinite(t).all())
+    rng = np.random.default_rng(w.seed + 1)
+    idx = [0, 1, 1023, 1024, 2047, 2048, 2049, 3072, w.n // 2, w.n - 1] + list(rng.integers(0, w.n, 22))
+    sel = np.stack([rng.integers(0, w.batch, len(idx)), rng.integers(0, w.heads, len(idx)), np.array(idx)], axis=1)
+
+    def gather(t):
+        ix = torch.as_tensor(sel, device=dev)
+        return to64(t[ix[:, 0], ix[:, 1], ix[:, 2]])
+
+    xi = oracle_inputs(x)
+    kw = dict(pattern=w.pattern, mode=w.mode, l=w.stride, c=0, scale=w.scale)
+    o_ref, lse_ref = orc_mod.forward_rows(*xi[:3], sel, **kw)
+    dq_ref = orc_mod.backward_rows(*xi, sel, **kw)
+    dk_ref, dv_ref = orc_mod.backward_cols(*xi, sel, **kw)
+    assert max_err(gather(o), o_ref) <= 2e-2
+    assert max_err(gather(lse), lse_ref) <= 1e-3
+    assert max_err(gather(dq), dq_ref) <= 2e-2
+    assert max_err(gather(dk), dk_ref) <= 2e-2
+    assert max_err(gather(dv), dv_ref) <= 2e-2
