@@ -402,6 +402,14 @@ def band_layout(n, block, stride_l, device="cuda", stream=None):
     return build_layout(n, block, stride_l, 0, SA_STRIDED, SA_MODE_A1, device=device, stream=stream)
 
 
+def _check_contiguous(*tensors):
+    """The transposed entry points take no strides: [b, h, n, d] contiguous, one shape."""
+    shape = tensors[0].shape
+    for t in tensors:
+        if t.dim() != 4 or t.shape != shape or not t.is_contiguous():
+            raise ValueError("the transposed path takes contiguous [batch, heads, n, d] tensors of one shape")
+
+
 def _transposed_workspace(q, band: Layout, class_block, workspace):
     b, h, n, d = q.shape
     need = sparse_attn_transposed_workspace_size(n, band.block, band.stride_l, class_block, b, h, d, _dtype_code(q))
@@ -417,7 +425,10 @@ def forward_merged_transposed(q, k, v, band: Layout, class_block, softmax_scale=
     if band.pattern != SA_STRIDED or band.head_mode != SA_MODE_A1 or band.n != n:
         raise ValueError("band must be the strided A1 layout of this n")
     o = torch.empty_like(q) if out is None else out
+    _check_contiguous(q, k, v, o)
     lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if lse is None else lse
+    if not lse.is_contiguous() or lse.shape != (b, h, n):
+        raise ValueError("lse must be a contiguous [batch, heads, n] tensor")
     ws, nbytes = _transposed_workspace(q, band, class_block, workspace)
     sparse_attn_fwd_transposed(n, band.block, band.stride_l, class_block, *band.row_args, b, h, d, _dtype_code(q),
                                q, k, v, _scale(softmax_scale, d), o, lse, ws, nbytes, stream)
@@ -428,7 +439,12 @@ def backward_merged_transposed(q, k, v, o, dout, lse, band: Layout, class_block,
                                workspace=None, stream=None):
     """dq, dk, dv of strided merged attention, A2 by transposition."""
     b, h, n, d = q.shape
+    if band.pattern != SA_STRIDED or band.head_mode != SA_MODE_A1 or band.n != n:
+        raise ValueError("band must be the strided A1 layout of this n")
     dq, dk, dv = grads if grads is not None else (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    _check_contiguous(q, k, v, o, dout, dq, dk, dv)
+    if not lse.is_contiguous() or lse.shape != (b, h, n):
+        raise ValueError("lse must be a contiguous [batch, heads, n] tensor")
     ws, nbytes = _transposed_workspace(q, band, class_block, workspace)
     sparse_attn_bwd_transposed(n, band.block, band.stride_l, class_block, *band.row_args, *band.col_args, b, h, d,
                                _dtype_code(q), q, k, v, o, dout, lse, _scale(softmax_scale, d), dq, dk, dv, ws,

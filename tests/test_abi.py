@@ -265,3 +265,17 @@ def test_transposed_workspace_and_errors(L):
     no_col = list(bwd)
     no_col[7] = None
     assert L.sparse_attn_bwd_transposed(*no_col, FAKE, need, None) == sa.SA_ERR_INVALID
+
+
+def test_transposed_binding_rejects_strided_views():
+    """The transposed entry points take no strides; the binding refuses views
+    that are not contiguous before anything reaches the library."""
+    import torch
+    q = torch.zeros(1, 2, 64, 32, dtype=torch.bfloat16)
+    band = sa.Layout(64, 16, 16, 0, sa.SA_STRIDED, sa.SA_MODE_A1, 1, [1], *([torch.zeros(1)] * 6))
+    view = torch.zeros(1, 2, 64, 64, dtype=torch.bfloat16)[..., :32]
+    with pytest.raises(ValueError, match="contiguous"):
+        sa.forward_merged_transposed(q, view, q, band, 16)
+    with pytest.raises(ValueError, match="strided A1"):
+        sa.forward_merged_transposed(q, q, q, sa.Layout(64, 16, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, [1],
+                                                        *([torch.zeros(1)] * 6)), 16)
