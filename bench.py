@@ -123,28 +123,36 @@ def copy_calibration(torch, dev):
     del src, dst
 
 
-def cpu_baseline(workloads, inputs):
-    """Time the fp64 oracle on one (batch, head) slice of each workload, full
-    sequence, and scale by batch * heads to the whole step."""
+def cpu_baseline(workloads, inputs, budget_s=10.0):
+    """Time the fp64 oracle on whole (batch, head) slices of each workload, full
+    sequence, slice after slice until about budget_s seconds of CPU work are
+    spent (at least one slice per workload), and scale the mean time per slice
+    by batch * heads to the whole step."""
     from oracle import oracle
     from paper_1904_10509_amd.inputs import as_oracle_array
 
-    est_s, credited, parts = 0.0, 0.0, []
+    est_s, credited, parts, spent = 0.0, 0.0, [], 0.0
     for w, nnz, x in workloads:
-        sl = [as_oracle_array(x[name][:1, :1]) for name in ("q", "k", "v", "dout")]
-        t0 = time.perf_counter()
-        oracle.backward(*sl, pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
-        dt = time.perf_counter() - t0
-        est_s += dt * w.batch * w.heads
+        times = []
+        for sidx in range(w.batch * w.heads):
+            b, h = divmod(sidx, w.heads)
+            sl = [as_oracle_array(x[name][b:b + 1, h:h + 1]) for name in ("q", "k", "v", "dout")]
+            t0 = time.perf_counter()
+            oracle.backward(*sl, pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
+            times.append(time.perf_counter() - t0)
+            spent += times[-1]
+            if spent >= budget_s:
+                break
+        est_s += sum(times) / len(times) * w.batch * w.heads
         credited += credited_flops(w, nnz)[0]
-        parts.append(f"{w.name}: 1 of {w.batch * w.heads} (batch, head) slices in {dt:.2f} s")
+        parts.append(f"{w.name}: {len(times)} of {w.batch * w.heads} (batch, head) slices in {sum(times):.2f} s")
     return {
         "value": credited / est_s / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
         "sample": "; ".join(parts) + "; full fwd+bwd (the oracle's backward recomputes its forward),"
-                  " time scaled by batch*heads",
+                  " mean time per slice scaled by batch*heads",
         "est_step_s": est_s,
     }
 
