@@ -291,13 +291,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
                     float sp = 0.f, dpp = 0.f;
 #pragma unroll
                     for (int ks = 0; ks < C::KS; ++ks) {
-                        const bf16x8 kv = ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g));
-                        const bf16x8 vv = ld_bf16x8(tV + Swz<D>::off(kk, 32 * ks + 8 * g));
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            sp = fmaf((float)qf[u][ks][e], (float)kv[e], sp);
-                            dpp = fmaf((float)of[u][ks][e], (float)vv[e], dpp);
-                        }
+                        sp += dot_bf16x8(qf[u][ks], ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g)));
+                        dpp += dot_bf16x8(of[u][ks], ld_bf16x8(tV + Swz<D>::off(kk, 32 * ks + 8 * g)));
                     }
                     const float pr = exp2_fast(fmaf(sum_over_g(sp), c2, nl2[u]));
                     const float ds = pr * (sum_over_g(dpp) + nd4[u][0]);
@@ -692,13 +687,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                         float sp = 0.f, dpp = 0.f;
 #pragma unroll
                         for (int ks = 0; ks < C::KS; ++ks) {
-                            const bf16x8 qv = ld_bf16x8(tQ + Swz<D>::off(kk, 32 * ks + 8 * g));
-                            const bf16x8 ov = ld_bf16x8(tO + Swz<D>::off(kk, 32 * ks + 8 * g));
-#pragma unroll
-                            for (int e = 0; e < 8; ++e) {
-                                sp = fmaf((float)kf[kbw][ks][e], (float)qv[e], sp);
-                                dpp = fmaf((float)vf[kbw][ks][e], (float)ov[e], dpp);
-                            }
+                            sp += dot_bf16x8(kf[kbw][ks], ld_bf16x8(tQ + Swz<D>::off(kk, 32 * ks + 8 * g)));
+                            dpp += dot_bf16x8(vf[kbw][ks], ld_bf16x8(tO + Swz<D>::off(kk, 32 * ks + 8 * g)));
                         }
                         const float pr = exp2_fast(fmaf(sum_over_g(sp), c2, tL[kk]));
                         const float ds = pr * (sum_over_g(dpp) + tD[kk]);

@@ -145,24 +145,28 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                     const int kk = w * C::RW + 16 * u + r;  // this lane's row, and its key, in the block
                     float part = 0.f;
 #pragma unroll
-                    for (int ks = 0; ks < C::KS; ++ks) {
-                        const bf16x8 kv = ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g));
+                    for (int ks = 0; ks < C::KS; ++ks)
+                        part += dot_bf16x8(qf[u][ks], ld_bf16x8(tK + Swz<D>::off(kk, 32 * ks + 8 * g)));
+                    bf16x4 vv[C::DB];  // read now, used after the softmax update
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) part = fmaf((float)qf[u][ks][e], (float)kv[e], part);
-                    }
+                    for (int db = 0; db < C::DB; ++db)
+                        vv[db] = __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(tV + Swz<D>::off(kk, 16 * db + 4 * g)));
                     const float sc = sum_over_g(part);
-                    const float m_new = fmaxf(m_run[u], sc);
+                    const bool grew = sc > m_run[u];
+                    const float m_new = grew ? sc : m_run[u];
                     const float alpha = exp2_fast((m_run[u] - m_new) * c2);  // 0 while m was -inf
                     const float pr = exp2_fast((sc - m_new) * c2);
                     l_run[u] = fmaf(l_run[u], alpha, g == 0 ? pr : 0.f);  // one lane of the row counts p
                     m_run[u] = m_new;
+                    // O is rescaled only where some row's maximum grew (a wave-uniform branch)
+                    if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {
 #pragma unroll
-                    for (int db = 0; db < C::DB; ++db) {
-                        const bf16x4 vv =
-                            __builtin_bit_cast(bf16x4, *reinterpret_cast<const uint2*>(tV + Swz<D>::off(kk, 16 * db + 4 * g)));
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) oacc[u][db][t] = fmaf(oacc[u][db][t], alpha, pr * (float)vv[t]);
+                        for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
                     }
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) oacc[u][db][t] = fmaf(pr, (float)vv[db][t], oacc[u][db][t]);
                 }
                 cur = nxt;
                 return true;

@@ -52,6 +52,19 @@ __device__ inline uint2 pack_bf16x4_bits(f32x4 v) {
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// sum_e a[e] b[e] over 8 bf16 pairs in fp32: four v_dot2_f32_bf16 on two
+// independent accumulators (a dependency chain of two, not eight).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ inline float dot_bf16x8(bf16x8 a, bf16x8 b) {
+    const bf16x2 a0{a[0], a[1]}, a1{a[2], a[3]}, a2{a[4], a[5]}, a3{a[6], a[7]};
+    const bf16x2 b0{b[0], b[1]}, b1{b[2], b[3]}, b2{b[4], b[5]}, b3{b[6], b[7]};
+    float x = __builtin_amdgcn_fdot2_f32_bf16(a0, b0, 0.f, false);
+    float y = __builtin_amdgcn_fdot2_f32_bf16(a1, b1, 0.f, false);
+    x = __builtin_amdgcn_fdot2_f32_bf16(a2, b2, x, false);
+    y = __builtin_amdgcn_fdot2_f32_bf16(a3, b3, y, false);
+    return x + y;
+}
+
 // Max / sum over the four lanes that share r = lane % 16, with the gfx950
 // row-swap permutes (16-lane rows 0<->1, 2<->3, then the two 32-lane halves).
 __device__ inline float max_over_g(float x) {
