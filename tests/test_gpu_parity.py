@@ -33,6 +33,7 @@ LAYOUT_CASES = [
     (F, 65536, 64, 256, 32),
     # a distinct summary subblock per head: one layout per subblock
     (P, 256, 16, 32, 8), (P, 256, 64, 128, 32), (P, 240, 16, 20, 6), (P, 512, 64, 256, 32), (P, 192, 32, 48, 10),
+    (P, 1024, 64, 128, 2),
     (P, 16384, 64, 128, 32),
 ]
 
@@ -111,6 +112,9 @@ SMALL_CASES = [
     (P, MG, 512, 64, 48, 10, 64, torch.bfloat16, 1, 4),
     (P, IL, 256, 32, 64, 16, 128, torch.float32, 1, 4),
     (P, A1, 256, 32, 64, 16, 64, torch.bfloat16, 1, 3),
+    # the largest number of subblocks (64, l = 128, c = 2), and eight with l <= 64
+    (P, MG, 1024, 64, 128, 2, 32, torch.bfloat16, 1, 64),
+    (P, A2, 512, 16, 64, 8, 32, torch.bfloat16, 1, 8),
 ]
 
 
