@@ -112,6 +112,7 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     sa::summary_words(p.l, p.c, p.l - p.c, &a.sum_lo, &a.sum_hi);
     a.sub = p.sub;
     a.claim_mode = sa::CLAIM_QUEUES;
+    a.pairs = 0;
     a.dl = sa::make_divl(p.l);
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;

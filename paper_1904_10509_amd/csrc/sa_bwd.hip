@@ -16,6 +16,9 @@
 //             time from a queue and walks its column view: S and dP
 //             recomputed, dV += P^T dO and dK += dS^T Q held in registers for
 //             the whole column.
+// In the fixed pattern with B = 64 a key block that is half summary keys is
+// split into its two halves, and summary halves one l-block apart are walked
+// as pairs (see split_column, pair_partner).
 // Column lengths can vary with a short period (in the fixed pattern only the
 // key blocks holding summary columns are long), and a hardware placement of
 // one workgroup per column can then pile the long columns onto a few compute
@@ -74,11 +77,12 @@ __device__ inline int64_t queue_heads(int64_t bh_count, int x) {
     return bh_count > x ? (bh_count - 1 - x) / kQueues + 1 : 0;
 }
 
-// Items of the dK / dV schedule: key block kb whole (half 0), or one 32-key
-// half of a 64-wide block (half 1: keys 0..31, half 2: keys 32..63); -1 is
-// an empty slot.
-constexpr int kItemShift = 29;
-__device__ inline int32_t item_code(int kb, int half) { return kb | (half << kItemShift); }
+// Items of the dK / dV schedule: key block kb whole (kind 0), one 32-key
+// half of a 64-wide block (kind 1: keys 0..31, kind 2: keys 32..63), or a
+// pair of such halves (kind 3: keys 0..31, kind 4: keys 32..63, of kb and of
+// kb + l / 64); -1 is an empty slot.  kb < 2^27 (n < 2^31, B >= 16).
+constexpr int kItemShift = 28;
+__device__ inline int32_t item_code(int kb, int kind) { return kb | (kind << kItemShift); }
 
 // In the fixed pattern with B = 64, a key block half of whose keys (the
 // upper or the lower 32) are summary keys and the other half not is split
@@ -94,6 +98,22 @@ __device__ inline int split_column(const AttnArgs& a, int g, int kb) {
     if (mp.part == PART_A1) return 0;
     const uint64_t bits = summary_bits(mp, mod_l(a.dl, 64 * kb));
     return bits == 0xFFFFFFFF00000000ull ? 1 : (bits == 0x00000000FFFFFFFFull ? 2 : 0);
+}
+
+// When l is a multiple of 64 the summary halves of split blocks recur every
+// l / 64 blocks at the same place, and two of them, one l-block apart, can be
+// walked as one item (a.pairs, chosen by the launcher): a split block of an
+// even l-block takes the summary half of the block l / 64 further along.  The
+// column of the first holds the second's (summary keys meet every later
+// query), and each staged Q / dO tile then serves 64 keys, where a single
+// half uses it for 32.  Returns the partner block of split block kb's summary
+// half, kb when that half is walked alone, or -1 when it is the second half
+// of kb - l / 64's pair.
+__device__ inline int pair_partner(const AttnArgs& a, int kb) {
+    if (!a.pairs || a.l % 64 != 0) return kb;
+    const int step = a.l / 64;
+    if ((kb / step) & 1) return -1;
+    return kb + step < a.nq ? kb + step : kb;
 }
 
 // Workgroup g < n_layouts of the pre kernel: layout g's items (2 nq slots)
@@ -112,8 +132,9 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
     __syncthreads();
     for (int kb = tid; kb < a.nq; kb += blockDim.x) {
-        atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
-        if (split_column(a, g, kb)) atomicAdd(&cls_pos[lower_cls], 1);
+        const int split = split_column(a, g, kb);
+        if (split == 0 || pair_partner(a, kb) >= 0) atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+        if (split) atomicAdd(&cls_pos[lower_cls], 1);
     }
     __syncthreads();
     if (tid == 0) {
@@ -128,10 +149,15 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     __syncthreads();
     for (int kb = tid; kb < a.nq; kb += blockDim.x) {
         const int split = split_column(a, g, kb);
-        // the summary half takes the column's class, the other half the short one
-        ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] =
-            item_code(kb, split == 0 ? 0 : (split == 1 ? 2 : 1));
-        if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, split == 1 ? 1 : 2);
+        // the summary half (alone or with its partner) takes the column's
+        // class, the other half the short one
+        const int sum_half = split == 1 ? 2 : 1, partner = split ? pair_partner(a, kb) : kb;
+        if (split == 0)
+            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
+        else if (partner >= 0)
+            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] =
+                item_code(kb, partner == kb ? sum_half : sum_half + 2);
+        if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 3 - sum_half);
     }
     for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
     if (tid == 0) items_out[g] = items;
@@ -594,17 +620,25 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             continue;
         }
         const int kb = code & ((1 << kItemShift) - 1);
-        const int half = kHalves ? code >> kItemShift : 0;
+        const int kind = kHalves ? code >> kItemShift : 0;
+        // In a pair waves 0, 1 take the summary half of kb, waves 2, 3 that of
+        // kb + l / 64, each for all queries of a block; a single half is shared
+        // by all four waves (two key groups times two query halves).
+        const bool pair = kind >= 3;
+        const int half = pair ? kind - 2 : kind;  // 32-key half walked; 0: the whole block
+        const bool single = half != 0 && !pair;
+        const int kb_w = pair && w >= 2 ? kb + a.l / 64 : kb;  // this wave's key block
         const MaskParams mp = head_mask_params(a, PAT, MODE, h);
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
         // that the waves share the summary columns of the fixed pattern (which
         // sit at the end of a block) and with them the softmax work.  In a
-        // half item the wave takes key group w mod 2 of the half, for the
-        // queries of one 32-query half (w / 2) of every block.
+        // single half the wave takes key group w mod 2 of the half, for the
+        // queries of one 32-query half (w / 2) of every block; in a pair, key
+        // group w mod 2 of its block's half, for every query.
         auto kgrp = [&](int kbw) { return half == 0 ? C::NW * kbw + w : 2 * (half - 1) + (w & 1); };
-        auto key_of = [&](int kbw) { return kb * BLK + 16 * kgrp(kbw) + r; };
+        auto key_of = [&](int kbw) { return kb_w * BLK + 16 * kgrp(kbw) + r; };
 
         // this lane's keys j = key_of(kbw) as B operands (d = 32 ks + 8g + t)
         bf16x8 kf[C::KBW][C::KS], vf[C::KBW][C::KS];
@@ -620,7 +654,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             cl[kbw] = col_lane(j, a.dl, a.c, mp.w);
         }
         // summary keys of this key block (fixed pattern), bit = key offset in the block
-        const uint64_t key_summary = PAT == FIXED ? summary_bits(mp, mod_l(a.dl, kb * BLK)) & kTileBits : 0ull;
+        const uint64_t key_summary = PAT == FIXED ? summary_bits(mp, mod_l(a.dl, kb_w * BLK)) & kTileBits : 0ull;
         f32x4 dvacc[C::KBW][C::DB], dkacc[C::KBW][C::DB];
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw)
@@ -633,7 +667,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
         const int e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
         int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
-        if (half != 0 && ((key_summary >> (32 * (half - 1))) & 0xFFFFFFFFull) == 0ull) {
+        if (single && ((key_summary >> (32 * (half - 1))) & 0xFFFFFFFFull) == 0ull) {
             // the non-summary half is attended only inside its own l-block:
             // the column's first entries (the query blocks ascend)
             int near = 0;
@@ -668,7 +702,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
             const bool masked =
-                !block_full32(PAT, mp.part, a.dl, a.c, mp.w, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+                pair || !block_full32(PAT, mp.part, a.dl, a.c, mp.w, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
             wait_loads_upto<0>();
             __syncthreads();  // block sidx is in LDS everywhere; the other stage is free
             if (sidx + 1 < len) load_block(qb_next, st ^ 1);
@@ -730,7 +764,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 }
                 if constexpr (!decltype(full)::value) {
                     const int i0_mod = mod_l(a.dl, i0);
-                    const bool far = far_block(PAT, a.dl, i0, kb * BLK, BLK);
+                    const bool far = far_block(PAT, a.dl, i0, kb_w * BLK, BLK);
                     if (PAT == FIXED && far && mp.part != PART_A1) {
                         // a summary key is attended by every row, any other key by none
 #pragma unroll
@@ -759,8 +793,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                 }
 
-                if (half != 0) {
-                    // a half item: this wave takes one 32-query half of the block
+                if (single) {
+                    // a single half: this wave takes one 32-query half of the block
 #pragma unroll
                     for (int qc = 0; qc < C::QC; ++qc)
                         if (qc != (w >> 1)) cls[0][qc] = CHUNK_NONE;
@@ -861,7 +895,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         });
 
         if constexpr (kHalves) {
-            if (half != 0) {
+            if (single) {
                 // the two query halves of each key group are summed through LDS
                 // (the ring is idle once every wave has passed the last step)
                 static_assert(sizeof(sQ) >= 2 * 2 * C::DB * 64 * sizeof(f32x4), "reduction fits the Q ring");
@@ -888,7 +922,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key_of(kbw)
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
-            if (half != 0 && w >= 2) break;  // written by the wave of the other query half
+            if (single && w >= 2) break;  // written by the wave of the other query half
             const int j = key_of(kbw);
             uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
@@ -1073,20 +1107,11 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     float* nlse2 = ws.nlse2;
     const int64_t pre_groups = (rows + 255) / 256 > layout_count(a.mode, a.sub) ? (rows + 255) / 256
                                                                                  : layout_count(a.mode, a.sub);
-    hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, a,
-                       (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items, ws.order);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     AttnArgs ak = a;
     return with_pattern_mode(a.pattern, a.mode, [&](auto pat, auto mode) {
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
-        with_full_body<PAT>(a, [&](auto fb) {
-            hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value>), grid,
-                               dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx,
-                               (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)dout,
-                               nlse2, ndelta, (uint16_t*)dq);
-            return hipSuccess;
-        });
         const int64_t slots = resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>>(DkvCfg<D, BLK, PAT>::NT);
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
@@ -1098,6 +1123,25 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         const int64_t bh_count = (int64_t)a.batch * a.heads;
         ak.claim_mode = (PAT == STRIDED || a.nq <= 8) ? CLAIM_ROUND_ROBIN
                         : (bh_count * 4 <= (int64_t)qgrid ? CLAIM_SERPENTINE : CLAIM_QUEUES);
+        // Summary halves in pairs (fixed, B = 64, l a multiple of 64: n / l of
+        // them per (batch, head)) only where each workgroup of a head gets at
+        // least 2.5 of them on average: a pair's column takes one workgroup
+        // about 1.45 times as long as a single half's, so with fewer the
+        // longest pair sets the kernel's time (fixed, n = 12,288, l = 128,
+        // 16 heads: 7% slower), with more the saved staging and steps win
+        // (n = 65,536, l = 256, 8 heads: 3% faster).
+        const int64_t per_head = (int64_t)qgrid / bh_count;
+        ak.pairs = PAT == FIXED && BLK == 64 && a.l % 64 == 0 && 2 * ((int64_t)a.n / a.l) >= 5 * per_head;
+        hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, ak,
+                           (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items,
+                           ws.order);
+        with_full_body<PAT>(a, [&](auto fb) {
+            hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value>), grid,
+                               dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx,
+                               (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)dout,
+                               nlse2, ndelta, (uint16_t*)dq);
+            return hipSuccess;
+        });
         hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE>), dim3(qgrid), dim3(DkvCfg<D, BLK, PAT>::NT), 0,
                            stream, ak, a.col_ptr, a.row_idx, (const uint16_t*)q, (const uint16_t*)k,
                            (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta, (uint16_t*)dk, (uint16_t*)dv,

@@ -65,6 +65,7 @@ struct AttnArgs {
     uint64_t sum_lo, sum_hi;  // summary positions below 128 (fixed masks, l <= 64, subblock 0)
     int32_t sub;           // fixed: 0 = one summary window for all heads, else floor(l / c) subblocks
     int32_t claim_mode;    // dK / dV work order, one of CLAIM_* (set by the backward launcher)
+    int32_t pairs;         // dK / dV: summary halves walked in pairs (set by the backward launcher)
     DivL dl;               // division by l
     const int32_t* row_ptr;
     const int32_t* col_idx;

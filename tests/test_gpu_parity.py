@@ -135,9 +135,14 @@ def test_parity_dkdv_work_orders():
     least four workgroups per (batch, head)) and atomic queues (fixed with
     more (batch, head) pairs than a quarter of the resident workgroups).  The
     last needs many heads: 16 x 16 here.  Each order must cover every column
-    exactly once, so all must match the oracle."""
+    exactly once, so all must match the oracle.  With many heads the summary
+    halves of the fixed pattern are also walked in pairs (at least 2.5 of them
+    per workgroup of a head): under the queues (16 x 16 heads, shared and
+    distinct subblocks) and under the serpentine order (2 x 96 heads, l = 64)."""
     dev = device()
-    for pattern, n, B, l, c, batch, heads in [(F, 1024, 64, 128, 32, 16, 16),   # queues
+    for pattern, n, B, l, c, batch, heads in [(F, 1024, 64, 128, 32, 16, 16),   # queues, pairs
+                                               (P, 1024, 64, 128, 32, 16, 16),  # queues, pairs of either half
+                                               (F, 1024, 64, 64, 32, 2, 96),    # serpentine, pairs
                                                (F, 1024, 64, 128, 32, 1, 3),    # serpentine
                                                (S, 1024, 64, 128, 0, 2, 5),     # round-robin
                                                (F, 512, 64, 128, 32, 2, 2)]:    # 8 key blocks: round-robin
