@@ -1,10 +1,16 @@
 // B x D bf16 tiles in LDS, filled straight from global memory.
 //
 // A tile is stored unpadded, row-major, with its 16-byte chunks permuted per
-// row (chunk c of row R sits at position c ^ perm(R)).  The permutation puts
-// the 16 rows that one 16-lane group reads at the same column into 16
-// distinct 16-byte slots of every 256-byte bank window, for both the row
-// reads (ds_read_b128) and the transposing reads (ds_read_b64_tr_b16).
+// row (chunk c of row R sits at position c ^ perm(R)).  perm is a linear map
+// over GF(2) of the low four bits of R, chosen (by exhaustive search over
+// such maps) so that no two lanes served together touch one bank twice, for
+// the row reads (ds_read_b128: 16 rows at one 16-byte column, taken 8 or 16
+// lanes at a time) and for the transposing reads (ds_read_b64_tr_b16: four
+// rows of 32 bytes per 16 lanes, taken 16 or 32 lanes at a time), whether a
+// cycle serves 128 or 256 bytes.  The plain forms perm(R) = R / rows-per-256
+// bytes left the transposing reads two-way conflicted.  perm depending on
+// R mod 16 alone keeps it unchanged under row offsets that are multiples of
+// 16, which the readers below rely on.
 //
 // Filling uses global_load_lds_dwordx4: lane L of a wave writes bytes
 // [16 L, 16 L + 16) of a 1 KiB LDS window (base in M0), from any global
@@ -32,9 +38,14 @@ namespace sa {
 
 template <int D>
 struct Swz {
-    static constexpr int CPR = D / 8;                            // 16-byte chunks per row
-    static constexpr int RPW = (2 * D >= 256) ? 1 : 256 / (2 * D);  // rows per 256-byte window
-    __device__ static int perm(int row) { return (row / RPW) % CPR; }
+    static constexpr int CPR = D / 8;  // 16-byte chunks per row
+    static_assert(D == 32 || D == 64 || D == 128, "head sizes 32, 64, 128");
+    __device__ static int perm(int row) {
+        const int b0 = row & 1, b1 = (row >> 1) & 1, b2 = (row >> 2) & 1, b3 = (row >> 3) & 1;
+        if constexpr (D == 32) return b2 | ((b1 ^ b2 ^ b3) << 1);
+        else if constexpr (D == 64) return b2 | (b1 << 1) | ((b0 ^ b2 ^ b3) << 2);
+        else return b2 | (b1 << 1) | (b0 << 2) | ((b2 ^ b3) << 3);
+    }
     // element offset of (row, col); col .. col+7 must stay inside one 8-element chunk
     __device__ static int off(int row, int col) {
         return row * D + ((((col >> 3) ^ perm(row))) << 3) + (col & 7);
