@@ -701,8 +701,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const int qb = qb_next;
             qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
             const int i0 = qb * BLK;
+            // a pair's keys are summary keys, attended by every query of a block
+            // away from both key blocks' l-blocks
             const bool masked =
-                pair || !block_full32(PAT, mp.part, a.dl, a.c, mp.w, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
+                pair ? !far_block(PAT, a.dl, i0, (kb + a.l / 64) * BLK, BLK)
+                     : !block_full32(PAT, mp.part, a.dl, a.c, mp.w, i0, i0 + BLK - 1, kb * BLK, kb * BLK + BLK - 1);
             wait_loads_upto<0>();
             __syncthreads();  // block sidx is in LDS everywhere; the other stage is free
             if (sidx + 1 < len) load_block(qb_next, st ^ 1);
@@ -742,11 +745,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     return;
                 }
             }
-            // The step body exists twice: for blocks attended everywhere (every
-            // chunk class a compile-time ALL unless a half item leaves a query
-            // half to the other waves, no mask) and for the others, in both
-            // patterns.
-            auto compute = [&](auto full) {
+            // The step body exists for blocks attended everywhere (every chunk
+            // class a compile-time ALL, no mask; with one_half, a single half
+            // leaves one query half to the other waves) and for the others, in
+            // both patterns.
+            auto compute = [&](auto full, auto one_half) {
 
                 // -LSE log2 e and -D of queries i0 + 16 qblk + 4g + t
                 auto row_stat = [&](const float* tile, int qblk) {
@@ -793,7 +796,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                 }
 
-                if (single) {
+                if (decltype(one_half)::value || (!decltype(full)::value && single)) {
                     // a single half: this wave takes one 32-query half of the block
 #pragma unroll
                     for (int qc = 0; qc < C::QC; ++qc)
@@ -890,8 +893,16 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                 }
             };
-            if (masked) compute(std::false_type{});
-            else compute(std::true_type{});
+            // unmasked steps of whole blocks and pairs run without a runtime
+            // chunk class (straight-line code over both query chunks)
+            if (masked) {
+                compute(std::false_type{}, std::false_type{});
+            } else if constexpr (kHalves) {
+                if (single) compute(std::true_type{}, std::true_type{});
+                else compute(std::true_type{}, std::false_type{});
+            } else {
+                compute(std::true_type{}, std::false_type{});
+            }
         });
 
         if constexpr (kHalves) {
