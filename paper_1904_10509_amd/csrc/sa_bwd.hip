@@ -807,6 +807,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 // and its operands are neither read nor multiplied (wave-uniform
                 // branches)
                 constexpr int HQ = C::QB >= 2 ? 2 : 1;  // 16-query blocks per 32-query chunk
+                // unmasked steps: ask the scheduler to interleave the exponentials
+                // with the matrix products (its strategy for attention-like loops)
+                if constexpr (decltype(full)::value && !decltype(one_half)::value) __builtin_amdgcn_iglp_opt(2);
                 bool qc_live[C::QC];
 #pragma unroll
                 for (int qc = 0; qc < C::QC; ++qc) {
