@@ -18,3 +18,13 @@ def orc():
     from oracle import oracle
     oracle.lib()
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Max-abs error of every parity check of the session (tests/gpu_util.py)."""
+    mod = sys.modules.get("gpu_util")
+    if mod is None or not getattr(mod, "RESULTS", None):
+        return
+    terminalreporter.section("parity: max-abs error per tensor (bound: tol + half an ulp of the output type)")
+    for label, md, tol, margin in mod.RESULTS:
+        terminalreporter.write_line(f"{label:78s} max-abs {md:.3e}  tol {tol:g}  margin {margin:.3e}")
