@@ -28,7 +28,10 @@
  * Conventions for every entry point:
  *   - All functions are extern "C"; no C++ or PyTorch type crosses the ABI.
  *   - Device pointers point to memory allocated by the caller; the library
- *     allocates no device memory and keeps no mutable global state.
+ *     allocates no device memory.  Its one piece of global state is a cache,
+ *     per kernel and device, of how many workgroups of the dK / dV kernel the
+ *     device holds at once (set on first use with atomic stores; any thread
+ *     computes the same value), so calls from several host threads are safe.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Device work is enqueued asynchronously; nothing synchronizes.  The
  *     device work of a call is kernel launches only (no memset, no
@@ -194,7 +197,6 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
                     void* workspace, size_t workspace_bytes, void* stream);
 
-/* Static English description of a status code. */
 /*
  * Bytes of device workspace that sparse_attn_decode needs (host only): the
  * partial softmax states of the key ranges a decoding step is split into,
@@ -275,6 +277,7 @@ int sparse_attn_bwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32
                                const void* v, const void* o, const void* dout, const float* lse, float softmax_scale,
                                void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Static English description of a status code (never NULL). */
 const char* sparse_attn_status_string(int status);
 
 #ifdef __cplusplus

@@ -1,0 +1,13 @@
+// bf16 backward kernels (sa_bwd_kernels.h) instantiated for d = 128: one
+// translation unit per head size, so that they compile in parallel.
+#include "sa_bwd_kernels.h"
+
+namespace sa {
+
+hipError_t bwd_bf16_d128(const AttnArgs& a, const void* q, const void* k, const void* v, const void* o,
+                        const void* dout, const float* lse, void* dq, void* dk, void* dv, const BwdWorkspace& ws,
+                        hipStream_t stream) {
+    return launch_bwd_bf16_d<128>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+}
+
+}  // namespace sa

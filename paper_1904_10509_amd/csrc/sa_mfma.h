@@ -45,6 +45,20 @@ __device__ inline bf16x8 pack_bf16x8(f32x4 lo, f32x4 hi) {
     return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
 
+// The same two results as a high and a low operand: hi = bf16(x) and
+// lo = bf16(x - hi), so that hi + lo carries x to about 2^-16 of itself
+// where hi alone carries it to 2^-8.
+__device__ inline void split_bf16x8(f32x4 a, f32x4 b, bf16x8& hi, bf16x8& lo) {
+    hi = pack_bf16x8(a, b);
+    f32x4 ra, rb;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        ra[t] = a[t] - (float)hi[t];
+        rb[t] = b[t] - (float)hi[4 + t];
+    }
+    lo = pack_bf16x8(ra, rb);
+}
+
 __device__ inline uint2 pack_bf16x4_bits(f32x4 v) {
     bf16x4 a = __builtin_convertvector(v, bf16x4);
     return __builtin_bit_cast(uint2, a);
