@@ -104,11 +104,38 @@ def _stream(stream, device):
 
 
 def _strides(*tensors):
-    st = tensors[0].stride()
+    """Element strides of [batch, heads, n, d] tensors that agree with the
+    first in shape, element type, device and strides (d contiguous); raises
+    ValueError otherwise, before anything reaches the library."""
+    ref = tensors[0]
+    if ref.dim() != 4:
+        raise ValueError("tensors must be [batch, heads, n, d]")
+    st = ref.stride()
     for t in tensors:
-        if t.dim() != 4 or t.stride() != st or t.stride(3) != 1:
-            raise ValueError("tensors must be [batch, heads, n, d] with d contiguous and identical strides")
+        if t.dim() != 4 or t.shape != ref.shape:
+            raise ValueError(f"tensor of shape {tuple(t.shape)} where {tuple(ref.shape)} is expected")
+        if t.dtype != ref.dtype:
+            raise ValueError(f"tensor of type {t.dtype} where {ref.dtype} is expected")
+        if t.device != ref.device or t.device.type != "cuda":
+            raise ValueError("every tensor must be on the same GPU")
+        if t.stride() != st or t.stride(3) != 1:
+            raise ValueError("tensors must have d contiguous and identical strides")
     return (ctypes.c_int64 * 3)(st[0], st[1], st[2])
+
+
+def _check_lse(lse, q):
+    b, h, n, _ = q.shape
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (b, h, n) or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 [batch, heads, n] tensor")
+    if lse.device != q.device:
+        raise ValueError("lse must be on q's device")
+
+
+def _check_layout(layout, q):
+    if q.shape[2] != layout.n:
+        raise ValueError("sequence length differs from the layout's")
+    if layout.row_ptr.device != q.device:
+        raise ValueError("the layout must be on q's device")
 
 
 def _dtype_code(t):
@@ -250,12 +277,12 @@ def _scale(softmax_scale, d):
 def forward(q, k, v, layout: Layout, softmax_scale=None, out=None, lse=None, stream=None):
     """O and LSE of sparse attention over ``layout``; q, k, v are [b, h, n, d] on the GPU."""
     b, h, n, d = q.shape
-    if n != layout.n:
-        raise ValueError("sequence length differs from the layout's")
     strides = _strides(q, k, v)
+    _check_layout(layout, q)
     o = torch.empty_like(q) if out is None else out
     _strides(q, o)
     lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if lse is None else lse
+    _check_lse(lse, q)
     sparse_attn_fwd(*layout.pattern_args, *layout.row_args, b, h, d, _dtype_code(q), q, k, v, strides,
                     _scale(softmax_scale, d), o, lse, stream)
     return o, lse
@@ -266,12 +293,16 @@ def backward(q, k, v, o, dout, lse, layout: Layout, softmax_scale=None, grads=No
     """dq, dk, dv of sparse attention given the forward's o and lse."""
     b, h, n, d = q.shape
     strides = _strides(q, k, v, o, dout)
+    _check_layout(layout, q)
+    _check_lse(lse, q)
     dq, dk, dv = grads if grads is not None else (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
     _strides(q, dq, dk, dv)
     dtype = _dtype_code(q)
     need = sparse_attn_bwd_workspace_size(*layout.pattern_args, b, h, d, dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    elif workspace.device != q.device:
+        raise ValueError("workspace must be on q's device")
     sparse_attn_bwd(*layout.pattern_args, *layout.row_args, *layout.col_args, b, h, d, dtype, q, k, v, o,
                     dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
                     workspace.numel() * workspace.element_size(), stream)
@@ -466,7 +497,10 @@ class SparseAttention(torch.autograd.Function):
     @staticmethod
     def backward(ctx, dout):
         q, k, v, o, lse = ctx.saved_tensors
-        dq, dk, dv = backward(q, k, v, o, dout.contiguous(), lse, ctx.layout, ctx.softmax_scale)
+        # the entry point takes one set of strides for all tensors: q's
+        if dout.stride() != q.stride():
+            dout = torch.empty_like(q).copy_(dout)
+        dq, dk, dv = backward(q, k, v, o, dout, lse, ctx.layout, ctx.softmax_scale)
         return dq, dk, dv, None, None
 
 

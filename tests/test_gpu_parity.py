@@ -1,9 +1,9 @@
 """GPU parity: the HIP path through the C ABI against the fp64 oracle.
 
 Layouts must match bitwise.  Outputs and gradients must match the fp64
-oracle on the same inputs within the tolerance of the element type, 1e-5 for
-fp32 and 2e-2 for bf16 (LSE: 1e-5 / 1e-3), on |gpu - oracle| / max(1, |oracle|):
-the max-abs error for values up to 1, relative above.
+oracle on the same inputs elementwise within the tolerance of the element
+type plus half an ulp of the stored output (tests/gpu_util.py): 1e-5 for fp32
+and 2e-2 for bf16 on O, dQ, dK, dV, and 1e-5 / 1e-3 on the fp32 LSE.
 """
 import numpy as np
 import pytest
@@ -13,7 +13,7 @@ from oracle import oracle as orc_mod
 from paper_1904_10509_amd import sparse_attn as sa
 from paper_1904_10509_amd.inputs import WORKLOADS, make_inputs, workload_inputs
 
-from gpu_util import LSE_TOL, TOL, device, max_err, oracle_inputs, run_gpu, to64
+from gpu_util import check, check_all, check_lse, device, oracle_inputs, run_gpu, to64
 
 pytestmark = pytest.mark.gpu
 
@@ -115,6 +115,17 @@ SMALL_CASES = [
     # the largest number of subblocks (64, l = 128, c = 2), and eight with l <= 64
     (P, MG, 1024, 64, 128, 2, 32, torch.bfloat16, 1, 64),
     (P, A2, 512, 16, 64, 8, 32, torch.bfloat16, 1, 8),
+    # few summary keys per row (c = 1, 2), A2 alone, many heads: the summary
+    # columns sum hundreds of large weights, so the dV / dK products take P and
+    # dS in two bf16 parts (shared window and a subblock per head; B = 64 with
+    # half items, B = 32 without)
+    (F, A2, 512, 64, 64, 1, 64, torch.bfloat16, 1, 32),
+    (F, A2, 512, 64, 64, 2, 64, torch.bfloat16, 1, 64),
+    (P, A2, 512, 64, 64, 1, 64, torch.bfloat16, 1, 64),
+    (P, A2, 512, 64, 64, 2, 64, torch.bfloat16, 1, 32),
+    (F, A2, 512, 32, 64, 1, 32, torch.bfloat16, 2, 32),
+    (F, MG, 512, 64, 64, 1, 64, torch.bfloat16, 1, 32),
+    (F, IL, 512, 64, 64, 2, 128, torch.bfloat16, 1, 32),
 ]
 
 
@@ -124,9 +135,8 @@ def test_parity_small(pattern, mode, n, B, l, c, d, dtype, batch, heads):
     scale = d ** -0.5
     got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=mode, scale=scale)
     ref = orc_mod.backward(*oracle_inputs(x), pattern=pattern, mode=mode, l=l, c=c, scale=scale)
-    for name in ("o", "dq", "dk", "dv"):
-        assert max_err(got[name], ref[name]) <= TOL[dtype], (name, max_err(got[name], ref[name]))
-    assert max_err(got["lse"], ref["lse"]) <= LSE_TOL[dtype], max_err(got["lse"], ref["lse"])
+    label = f"p{pattern} m{mode} n{n} B{B} l{l} c{c} d{d} {str(dtype)[6:]} {batch}x{heads}"
+    check_all(label, got, ref, dtype, names=("o", "lse", "dq", "dk", "dv"))
 
 
 def test_parity_dkdv_work_orders():
@@ -149,8 +159,7 @@ def test_parity_dkdv_work_orders():
         x = make_inputs(batch, heads, n, 32, torch.bfloat16, seed=batch * heads + n)
         got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=MG, scale=32 ** -0.5, dev=dev)
         ref = orc_mod.backward(*oracle_inputs(x), pattern=pattern, mode=MG, l=l, c=c, scale=32 ** -0.5)
-        for name in ("o", "dq", "dk", "dv"):
-            assert max_err(got[name], ref[name]) <= 2e-2, (pattern, batch, heads, name, max_err(got[name], ref[name]))
+        check_all(f"work order p{pattern} n{n} l{l} {batch}x{heads}", got, ref, torch.bfloat16)
 
 
 def test_workload_fp32_full():
@@ -160,8 +169,7 @@ def test_workload_fp32_full():
         got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=mode, scale=w.scale)
         ref = orc_mod.backward(*oracle_inputs(x), pattern=w.pattern, mode=mode, l=w.stride, c=w.summary,
                                scale=w.scale)
-        for name in ("o", "lse", "dq", "dk", "dv"):
-            assert max_err(got[name], ref[name]) <= 1e-5, (mode, name, max_err(got[name], ref[name]))
+        check_all(f"{w.name} mode {mode}", got, ref, torch.float32, names=("o", "lse", "dq", "dk", "dv"))
 
 
 def test_workload_interleaved_full():
@@ -170,9 +178,7 @@ def test_workload_interleaved_full():
     got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=w.mode, scale=w.scale)
     ref = orc_mod.backward(*oracle_inputs(x), pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary,
                            scale=w.scale)
-    for name in ("o", "dq", "dk", "dv"):
-        assert max_err(got[name], ref[name]) <= 2e-2, (name, max_err(got[name], ref[name]))
-    assert max_err(got["lse"], ref["lse"]) <= 1e-3
+    check_all(w.name, got, ref, torch.bfloat16, names=("o", "lse", "dq", "dk", "dv"))
     empty = np.isneginf(ref["lse"])
     assert empty.sum() == w.batch * (w.heads // 2) * (w.stride - w.summary)  # head 1, first block
     assert np.all(got["o"][np.broadcast_to(empty[..., None], got["o"].shape)] == 0)
@@ -206,16 +212,47 @@ def test_workload_sampled(name):
     dk, dv = orc_mod.backward_cols(*xi, cols, **kw)
     r = (rows[:, 0], rows[:, 1], rows[:, 2])
     cc = (cols[:, 0], cols[:, 1], cols[:, 2])
-    assert max_err(got["o"][r], o) <= 2e-2
-    assert max_err(got["lse"][r], lse) <= 1e-3
-    assert max_err(got["dq"][r], dq) <= 2e-2
-    assert max_err(got["dk"][cc], dk) <= 2e-2
-    assert max_err(got["dv"][cc], dv) <= 2e-2
-    # properties at full size: rows of P sum to one (checked through V = 1 below on a
-    # smaller case), finite outputs, gradient of a shift of all keys vanishes
+    bf = torch.bfloat16
+    check(f"{name} o rows", got["o"][r], o, bf)
+    check_lse(f"{name} lse rows", got["lse"][r], lse, bf)
+    check(f"{name} dq rows", got["dq"][r], dq, bf)
+    check(f"{name} dk cols", got["dk"][cc], dk, bf)
+    check(f"{name} dv cols", got["dv"][cc], dv, bf)
     for key in ("o", "dq", "dk", "dv", "lse"):
         assert np.all(np.isfinite(got[key])), key
-    assert np.abs(got["dk"].sum(axis=2)).max() <= 2e-2 * np.sqrt(w.n)
+
+
+# Full size, element by element: every (batch, head) slice of the strided text
+# workload (n = 12,288, 2 x 8 heads), and two whole slices of the fixed audio
+# workload (n = 65,536, all 65,536 rows and columns of heads 0 and 5), in the
+# launch configuration the benchmark times (all heads in one call).
+def test_workload_strided_n12288_full():
+    w = WORKLOADS["strided_n12288_l128_merged"]
+    x = workload_inputs(w)
+    got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=w.mode, scale=w.scale)
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary,
+                           scale=w.scale)
+    check_all(f"{w.name} full", got, ref, torch.bfloat16, names=("o", "lse", "dq", "dk", "dv"))
+
+
+@pytest.mark.parametrize("name", ["fixed_n65536_l256_c32_merged", "fixed_per_head_n65536_l256_c32_merged"])
+def test_workload_fixed_n65536_two_slices_full(name):
+    w = WORKLOADS[name]
+    x = workload_inputs(w)
+    got = run_gpu(x, n=w.n, block=w.block, l=w.stride, c=w.summary, pattern=w.pattern, mode=w.mode, scale=w.scale)
+    xi = oracle_inputs(x)
+    kw = dict(pattern=w.pattern, mode=w.mode, l=w.stride, c=w.summary, scale=w.scale)
+    if w.pattern == P:
+        # head h's window is subblock h mod (l / c), so the oracle sees heads 0
+        # and 1 as such (the upper and the lower half of a key block)
+        ref = orc_mod.backward(*[a[:1, 0:2] for a in xi], **kw)
+        check_all(f"{name} heads 0, 1 full", {k_: v_[:1, 0:2] for k_, v_ in got.items()}, ref, torch.bfloat16,
+                  names=("o", "lse", "dq", "dk", "dv"))
+        return
+    for h in (0, 5):
+        ref = orc_mod.backward(*[a[:1, h:h + 1] for a in xi], **kw)
+        check_all(f"{name} head {h} full", {k_: v_[:1, h:h + 1] for k_, v_ in got.items()}, ref, torch.bfloat16,
+                  names=("o", "lse", "dq", "dk", "dv"))
 
 
 def test_ones_value_gives_ones_output():
@@ -226,7 +263,8 @@ def test_ones_value_gives_ones_output():
         x["v"] = torch.ones_like(x["v"])
         got = run_gpu(x, n=n, block=B, l=l, c=c, pattern=pattern, mode=mode, scale=d ** -0.5, backward=False, dev=dev)
         nonempty = np.isfinite(got["lse"])
-        assert np.abs(got["o"][nonempty] - 1.0).max() <= 2e-2
+        check(f"V = 1 p{pattern} m{mode}", got["o"][nonempty], np.ones(int(nonempty.sum()) * d).reshape(-1, d),
+              torch.bfloat16)
         assert np.all(got["o"][~nonempty] == 0)
 
 
@@ -271,9 +309,64 @@ def test_autograd_wrapper():
     o = sa.SparseAttention.apply(q, k, v, lay, None)
     (o.float() * x["dout"].to(dev).float()).sum().backward()
     ref = orc_mod.backward(*oracle_inputs(x), pattern=S, mode=MG, l=32, c=0, scale=d ** -0.5)
-    assert max_err(q.grad.float().cpu().numpy(), ref["dq"]) <= 2e-2
-    assert max_err(k.grad.float().cpu().numpy(), ref["dk"]) <= 2e-2
-    assert max_err(v.grad.float().cpu().numpy(), ref["dv"]) <= 2e-2
+    check("autograd o", to64(o), ref["o"], torch.bfloat16)
+    check("autograd dq", to64(q.grad), ref["dq"], torch.bfloat16)
+    check("autograd dk", to64(k.grad), ref["dk"], torch.bfloat16)
+    check("autograd dv", to64(v.grad), ref["dv"], torch.bfloat16)
+
+
+def test_autograd_wrapper_transposed_views():
+    """q, k, v as [b, n, h, d].transpose(1, 2) views (not contiguous): the
+    wrapper hands the incoming gradient over with q's strides."""
+    dev = device()
+    b, n, h, d = 1, 256, 2, 64
+    x = make_inputs(b, h, n, d, torch.bfloat16, seed=23)
+    lay = sa.build_layout(n, 32, 32, 8, F, IL, device=dev)
+    leaves = [x[n_].transpose(1, 2).contiguous().to(dev).requires_grad_(True) for n_ in ("q", "k", "v")]
+    q, k, v = (t.transpose(1, 2) for t in leaves)  # [b, h, n, d] views of [b, n, h, d] storage
+    assert not q.is_contiguous()
+    o = sa.SparseAttention.apply(q, k, v, lay, None)
+    (o.float() * x["dout"].to(dev).float()).sum().backward()
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=F, mode=IL, l=32, c=8, scale=d ** -0.5)
+    check("autograd views o", to64(o), ref["o"], torch.bfloat16)
+    for name, t in (("dq", leaves[0]), ("dk", leaves[1]), ("dv", leaves[2])):
+        check(f"autograd views {name}", to64(t.grad.transpose(1, 2)), ref[name], torch.bfloat16)
+
+
+def test_binding_rejects_mismatched_tensors():
+    """Shapes, dtypes, devices and the sequence length are checked before the
+    C ABI is called: a smaller or differently typed tensor never reaches a
+    kernel."""
+    dev = device()
+    n, d = 256, 64
+    x = make_inputs(2, 2, n, d, torch.bfloat16, seed=4)
+    q, k, v, dout = (x[n_].to(dev) for n_ in ("q", "k", "v", "dout"))
+    lay = sa.build_layout(n, 64, 64, 0, S, MG, device=dev)
+    o, lse = sa.forward(q, k, v, lay)
+    bad = [
+        lambda: sa.forward(q, k[:1].contiguous(), v, lay),                    # batch
+        lambda: sa.forward(q, k, v[:, :, : n - 64].contiguous(), lay),        # sequence
+        lambda: sa.forward(q, k.float(), v, lay),                             # dtype
+        lambda: sa.forward(q, k.cpu(), v, lay),                               # device
+        lambda: sa.forward(q[:, :, :128].contiguous(), k[:, :, :128].contiguous(),
+                           v[:, :, :128].contiguous(), lay),                  # n against the layout
+        lambda: sa.forward(q, k, v, lay, out=torch.empty_like(q[:1])),
+        lambda: sa.forward(q, k, v, lay, lse=torch.empty(2, 2, n - 1, device=dev)),
+        lambda: sa.backward(q, k, v, o, dout[:1].contiguous(), lse, lay),
+        lambda: sa.backward(q, k, v, o.float(), dout, lse, lay),
+        lambda: sa.backward(q, k, v, o, dout, lse[:, :, 1:], lay),
+        lambda: sa.backward(q, k, v, o, dout, lse.to(torch.bfloat16), lay),
+        lambda: sa.backward(q[:, :, :128].contiguous(), k[:, :, :128].contiguous(), v[:, :, :128].contiguous(),
+                            o[:, :, :128].contiguous(), dout[:, :, :128].contiguous(),
+                            lse[:, :, :128].contiguous(), lay),
+        lambda: sa.backward(q, k, v, o, dout, lse, lay, grads=(torch.empty_like(q), torch.empty_like(k[:1]),
+                                                               torch.empty_like(v))),
+    ]
+    for i, f in enumerate(bad):
+        with pytest.raises(ValueError):
+            f()
+            print("not rejected:", i)
+    torch.cuda.synchronize()
 
 
 # ---------------------------------------------------------------------------
@@ -326,8 +419,9 @@ def test_workload_n1048576_sampled():
     o_ref, lse_ref = orc_mod.forward_rows(*xi[:3], rows, **kw)
     dq_ref = orc_mod.backward_rows(*xi, rows, **kw)
     dk_ref, dv_ref = orc_mod.backward_cols(*xi, cols, **kw)
-    assert max_err(gather(o, rows), o_ref) <= 2e-2
-    assert max_err(gather(lse, rows), lse_ref) <= 1e-3
-    assert max_err(gather(dq, rows), dq_ref) <= 2e-2
-    assert max_err(gather(dk, cols), dk_ref) <= 2e-2
-    assert max_err(gather(dv, cols), dv_ref) <= 2e-2
+    bf = torch.bfloat16
+    check("n1048576 o rows", gather(o, rows), o_ref, bf)
+    check_lse("n1048576 lse rows", gather(lse, rows), lse_ref, bf)
+    check("n1048576 dq rows", gather(dq, rows), dq_ref, bf)
+    check("n1048576 dk cols", gather(dk, cols), dk_ref, bf)
+    check("n1048576 dv cols", gather(dv, cols), dv_ref, bf)
