@@ -198,6 +198,31 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * sparse_attn_bwd without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * sparse_attn_bwd less the workspace; the library uses a fixed device array
+ * of sparse_attn_bwd_noalloc_max_workspace bytes (64 MiB) instead, one per
+ * device, held until the process ends, and allocates nothing (no hipMalloc,
+ * no allocating library call).  A call whose workspace size
+ * (sparse_attn_bwd_workspace_size) exceeds it returns SA_ERR_BUFFER_TOO_SMALL
+ * without enqueueing anything (n = 65,536 with 8 heads needs 4 MiB, n =
+ * 1,048,576 with 4 heads 32 MiB).  `stream` must belong to the current
+ * device (SA_ERR_INVALID otherwise).  Every call on one device shares that
+ * device's array: calls that overlap on one device race and must be ordered
+ * by the caller (one stream, or events).  The array keeps the last call's
+ * contents; nothing in it needs to start at zero.
+ */
+int sparse_attn_bwd_noalloc_max_workspace(size_t* bytes);
+
+int sparse_attn_bwd_noalloc(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                            int32_t head_mode, const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                            const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                            int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                            const void* o, const void* dout, const float* lse, const int64_t* strides,
+                            float softmax_scale, void* dq, void* dk, void* dv, void* stream);
+
+/*
  * Bytes of device workspace that sparse_attn_decode needs (host only): the
  * partial softmax states of the key ranges a decoding step is split into,
  * (d_head + 2) fp32 values per range and (batch, head).  Pattern arguments

@@ -2,6 +2,8 @@
 // status codes.  Nothing is enqueued unless every argument is valid.
 #include <math.h>
 
+#include <mutex>
+
 #include "sparse_attn.h"
 #include "sa_internal.h"
 #include "sa_mask.h"
@@ -216,6 +218,68 @@ ClassLayout class_layout(const TransposedPlan& p, char* ws) {
     return c;
 }
 
+// Arguments of a backward call, shared by sparse_attn_bwd and
+// sparse_attn_bwd_noalloc: everything but the workspace.  Fills the kernel
+// arguments and the workspace size the call needs.
+int check_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int32_t pattern, int32_t head_mode,
+              const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind, const int32_t* col_ptr,
+              const int32_t* row_idx, const uint8_t* kind_t, int32_t batch, int32_t heads, int32_t d_head,
+              int32_t dtype, const void* q, const void* k, const void* v, const void* o, const void* dout,
+              const float* lse, const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
+              sa::AttnArgs* a, size_t* need) {
+    PatternArgs p;
+    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    if (st != SA_OK) return st;
+    st = check_tensor_args(p, batch, heads, d_head, dtype, strides);
+    if (st != SA_OK) return st;
+    if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
+    if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return SA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        return SA_ERR_INVALID;
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
+    *need = sa::bwd_workspace_bytes(batch, heads, n, p.nq, p.n_layouts);
+    *a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx, kind, col_ptr, row_idx,
+                   kind_t);
+    return SA_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Scratch of sparse_attn_bwd_noalloc: a fixed device array in place of the
+// caller's workspace, one copy per device, held until the process ends.  In
+// host code `scratch` names a host-side stand-in, not device memory, so its
+// device address is looked up once per device (with that device current)
+// and only that address is ever passed on.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device, guarded by g_scratch_mutex
+
+// Device address of the scratch array on the device of `stream`, which must
+// be the current device.
+int scratch_address(hipStream_t stream, void** out) {
+    int dev = -1, stream_dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
+    if (hipStreamGetDevice(stream, &stream_dev) != hipSuccess) return SA_ERR_HIP;
+    if (stream_dev != dev) return SA_ERR_INVALID;
+    if (dev < 0 || dev >= kMaxDevices) return SA_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return SA_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return SA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -309,24 +373,45 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     const void* v, const void* o, const void* dout, const float* lse,
                     const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
                     void* workspace, size_t workspace_bytes, void* stream) {
-    PatternArgs p;
-    int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
+    sa::AttnArgs a;
+    size_t need = 0;
+    const int st = check_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind, col_ptr,
+                             row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse, strides,
+                             softmax_scale, dq, dk, dv, &a, &need);
     if (st != SA_OK) return st;
-    st = check_tensor_args(p, batch, heads, d_head, dtype, strides);
-    if (st != SA_OK) return st;
-    if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
-    if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return SA_ERR_INVALID;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
-        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
-        return SA_ERR_INVALID;
-    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
-    const size_t need = sa::bwd_workspace_bytes(batch, heads, n, p.nq, p.n_layouts);
     if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
     if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;
-    sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,
-                               kind, col_ptr, row_idx, kind_t);
     hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
                                   static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+int sparse_attn_bwd_noalloc_max_workspace(size_t* bytes) {
+    if (!bytes) return SA_ERR_INVALID;
+    *bytes = kScratchBytes;
+    return SA_OK;
+}
+
+int sparse_attn_bwd_noalloc(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                            int32_t head_mode, const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                            const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                            int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                            const void* o, const void* dout, const float* lse, const int64_t* strides,
+                            float softmax_scale, void* dq, void* dk, void* dv, void* stream) {
+    sa::AttnArgs a;
+    size_t need = 0;
+    int st = check_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind, col_ptr, row_idx,
+                       kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse, strides, softmax_scale, dq, dk,
+                       dv, &a, &need);
+    if (st != SA_OK) return st;
+    if (need > kScratchBytes) return SA_ERR_BUFFER_TOO_SMALL;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* ws = nullptr;
+    st = scratch_address(s, &ws);
+    if (st != SA_OK) return st;
+    // the workspace's contents on entry are ignored: the pre kernel writes the
+    // row statistics and empties the work counters before anything reads them
+    hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

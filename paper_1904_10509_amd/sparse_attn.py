@@ -36,6 +36,8 @@ EXPORTED = (
     "sparse_attn_transposed_workspace_size",
     "sparse_attn_fwd_transposed",
     "sparse_attn_bwd_transposed",
+    "sparse_attn_bwd_noalloc_max_workspace",
+    "sparse_attn_bwd_noalloc",
     "sparse_attn_status_string",
 )
 
@@ -72,6 +74,8 @@ def lib():
         L.sparse_attn_fwd_transposed.argtypes = _TR + [_vp] * 3 + [_i32] * 4 + [_vp] * 3 + [_f32] + [_vp] * 3 + [_sz, _vp]
         L.sparse_attn_bwd_transposed.argtypes = (_TR + [_vp] * 6 + [_i32] * 4 + [_vp] * 6 + [_f32] + [_vp] * 4
                                                  + [_sz, _vp])
+        L.sparse_attn_bwd_noalloc_max_workspace.argtypes = [_vp]
+        L.sparse_attn_bwd_noalloc.argtypes = (_PAT + [_vp] * 6 + [_i32] * 4 + [_vp] * 7 + [_f32] + [_vp] * 4)
         L.sparse_attn_status_string.argtypes = [ctypes.c_int]
         L.sparse_attn_status_string.restype = ctypes.c_char_p
         for name in EXPORTED[:-1]:
@@ -201,6 +205,23 @@ def sparse_attn_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, 
                                _ptr(dout), _ptr(lse), strides, softmax_scale, _ptr(dq), _ptr(dk),
                                _ptr(dv), _ptr(workspace), workspace_bytes, _stream(stream, q.device))
     _check("sparse_attn_bwd", st)
+
+
+def sparse_attn_bwd_noalloc_max_workspace():
+    out = ctypes.c_size_t(0)
+    _check("sparse_attn_bwd_noalloc_max_workspace", lib().sparse_attn_bwd_noalloc_max_workspace(ctypes.byref(out)))
+    return out.value
+
+
+def sparse_attn_bwd_noalloc(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,
+                            col_ptr, row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse,
+                            strides, softmax_scale, dq, dk, dv, stream=None):
+    st = lib().sparse_attn_bwd_noalloc(n, block, stride_l, summary_c, pattern, head_mode, _ptr(row_ptr),
+                                       _ptr(col_idx), _ptr(kind), _ptr(col_ptr), _ptr(row_idx), _ptr(kind_t),
+                                       batch, heads, d_head, dtype, _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                       _ptr(dout), _ptr(lse), strides, softmax_scale, _ptr(dq), _ptr(dk),
+                                       _ptr(dv), _stream(stream, q.device))
+    _check("sparse_attn_bwd_noalloc", st)
 
 
 def sparse_attn_decode_workspace_size(pos, stride_l, summary_c, pattern, head_mode, batch, heads, d_head, dtype):

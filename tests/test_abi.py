@@ -279,3 +279,18 @@ def test_transposed_binding_rejects_strided_views():
     with pytest.raises(ValueError, match="strided A1"):
         sa.forward_merged_transposed(q, q, q, sa.Layout(64, 16, 16, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, [1],
                                                         *([torch.zeros(1)] * 6)), 16)
+
+
+def test_noalloc_rejects_workspace_beyond_scratch(L):
+    """The allocation-free backward refuses a call whose workspace would exceed
+    its fixed scratch (here 16 heads x 2^20 rows, 8 bytes of row statistics
+    each: 128 MiB), before touching any memory or the device."""
+    n, heads, d = 1 << 20, 16, 64
+    need = sa.sparse_attn_bwd_workspace_size(n, 64, 1024, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, 1, heads, d,
+                                             sa.SA_BF16)
+    assert need > sa.sparse_attn_bwd_noalloc_max_workspace()
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: the size check comes first
+    strides = (ctypes.c_int64 * 3)(heads * n * d, n * d, d)
+    st = L.sparse_attn_bwd_noalloc(n, 64, 1024, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, *([fake] * 6), 1, heads, d,
+                                   sa.SA_BF16, *([fake] * 6), strides, ctypes.c_float(0.125), *([fake] * 3), None)
+    assert st == sa.SA_ERR_BUFFER_TOO_SMALL
