@@ -116,6 +116,12 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.claim_mode = sa::CLAIM_QUEUES;
     a.pairs = 0;
     a.dl = sa::make_divl(p.l);
+    a.walk = sa::WALK_LAYOUT;
+    a.qshift = 0;
+    a.epilogue = sa::EPI_STORE;
+    a.lse_sb = (int64_t)heads * p.n;  // LSE and row statistics: [batch, heads, n]
+    a.lse_sh = p.n;
+    a.lse_ss = 1;
     a.row_ptr = row_ptr;
     a.col_idx = col_idx;
     a.kind = kind;
@@ -123,6 +129,46 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.row_idx = row_idx;
     a.kind_t = kind_t;
     return a;
+}
+
+// Strided pattern, merged heads or A2 alone, bf16: A2 by residue classes
+// (Sec. 5.5, a stride becomes a local window once positions are reordered by
+// their residue mod l).  With l dividing n, position i = m l + r (class r,
+// step m) meets j = m' l + r of its own class only, and A2 \ A1 of the merged
+// set is {m' <= m - 2}: dense causal attention inside each class, with the
+// queries' causal limit moved back by two steps (A2 alone: by none).  The
+// classes are strided views of the [b, h, n, d] tensors, so the block kernels
+// walk them unchanged: batch = the b h pairs (stride of one head), heads = the
+// l classes (stride of one row), sequence stride l rows, every block kb <= qb
+// present (no layout), LSE and row statistics read back in row order.  The
+// merged set's band A1 runs first over the caller's layout (only its band
+// blocks: with B dividing l, A2 \ A1 never meets them), and the class kernels
+// then combine their part into its O and LSE (forward) or add it to its
+// gradients (backward).  Returns false where the block path stays: fp32,
+// l not dividing n, n / l not a multiple of 16, batch and head strides that do
+// not merge, or sizes the class grid cannot hold.
+bool class_plan(const PatternArgs& p, int32_t batch, int32_t heads, int32_t d, int32_t dtype, const int64_t* strides,
+                float scale, sa::AttnArgs* cls) {
+    if (p.pattern != sa::STRIDED || dtype != SA_BF16) return false;
+    if (p.mode != SA_MODE_MERGED && p.mode != SA_MODE_A2) return false;
+    if (p.n % p.l != 0 || (p.mode == SA_MODE_MERGED && p.l % p.block != 0)) return false;
+    const int64_t M = p.n / p.l;  // positions per class
+    const int32_t cb = (M % 64 == 0 && M >= 256) ? 64 : (M % 32 == 0 ? 32 : (M % 16 == 0 ? 16 : 0));
+    if (cb == 0 || M / cb > 65535) return false;
+    if (batch > 1 && strides[0] != (int64_t)heads * strides[1]) return false;  // (b, h) as one index
+    if ((int64_t)batch * heads > 65535) return false;                            // grid dimension
+    const int64_t cls_strides[3] = {strides[1], strides[2], (int64_t)p.l * strides[2]};
+    PatternArgs c;
+    if (check_pattern(M, cb, (int32_t)M, 0, SA_STRIDED, SA_MODE_A1, &c) != SA_OK) return false;
+    if (check_tensor_args(c, batch * heads, p.l, d, dtype, cls_strides) != SA_OK) return false;
+    *cls = make_args(c, batch * heads, p.l, d, cls_strides, scale, nullptr, nullptr, nullptr, nullptr, nullptr,
+                     nullptr);
+    cls->walk = sa::WALK_DENSE;
+    cls->qshift = p.mode == SA_MODE_MERGED ? 2 : 0;
+    cls->lse_sb = p.n;  // row i = m l + r of pair bh sits at bh n + r + m l
+    cls->lse_sh = 1;
+    cls->lse_ss = p.l;
+    return true;
 }
 
 // Pattern arguments of a decoding step (no block size: S_pos is enumerated).
@@ -226,7 +272,7 @@ int check_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int
               const int32_t* row_idx, const uint8_t* kind_t, int32_t batch, int32_t heads, int32_t d_head,
               int32_t dtype, const void* q, const void* k, const void* v, const void* o, const void* dout,
               const float* lse, const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
-              sa::AttnArgs* a, size_t* need) {
+              sa::AttnArgs* a, size_t* need, bool* by_classes, sa::AttnArgs* cls) {
     PatternArgs p;
     int st = check_pattern(n, block, stride_l, summary_c, pattern, head_mode, &p);
     if (st != SA_OK) return st;
@@ -241,7 +287,28 @@ int check_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int
     *need = sa::bwd_workspace_bytes(batch, heads, n, p.nq, p.n_layouts);
     *a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx, kind, col_ptr, row_idx,
                    kind_t);
+    *by_classes = class_plan(p, batch, heads, d_head, dtype, strides, softmax_scale, cls);
     return SA_OK;
+}
+
+// The launches of a validated backward call (see class_plan): the band's
+// backward, then the classes' dQ and dK / dV added to it; A2 alone: the row
+// statistics, then the classes' dQ and dK / dV.
+hipError_t launch_bwd(sa::AttnArgs a, bool by_classes, sa::AttnArgs cls, int dtype, const void* q, const void* k,
+                      const void* v, const void* o, const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                      void* ws, hipStream_t s) {
+    if (!by_classes) return sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
+    hipError_t e;
+    if (a.mode == sa::MODE_MERGED) {
+        a.walk = sa::WALK_BAND;
+        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
+        cls.epilogue = sa::EPI_ADD;
+    } else {
+        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_PRE);
+    }
+    if (e == hipSuccess)
+        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DQ | sa::BWD_DKDV);
+    return e;
 }
 
 }  // namespace
@@ -348,7 +415,19 @@ int sparse_attn_fwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
     if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
     sa::AttnArgs a = make_args(p, batch, heads, d_head, strides, softmax_scale, row_ptr, col_idx,
                                kind, nullptr, nullptr, nullptr);
-    hipError_t e = sa::fwd_launch(a, dtype, q, k, v, o, lse, static_cast<hipStream_t>(stream));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    sa::AttnArgs cls;
+    if (class_plan(p, batch, heads, d_head, dtype, strides, softmax_scale, &cls)) {
+        hipError_t e = hipSuccess;
+        if (p.mode == SA_MODE_MERGED) {  // the band first, then the classes merged into it
+            a.walk = sa::WALK_BAND;
+            e = sa::fwd_launch(a, dtype, q, k, v, o, lse, s);
+            cls.epilogue = sa::EPI_MERGE;
+        }
+        if (e == hipSuccess) e = sa::fwd_launch(cls, dtype, q, k, v, o, lse, s);
+        return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+    }
+    hipError_t e = sa::fwd_launch(a, dtype, q, k, v, o, lse, s);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
@@ -373,16 +452,17 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     const void* v, const void* o, const void* dout, const float* lse,
                     const int64_t* strides, float softmax_scale, void* dq, void* dk, void* dv,
                     void* workspace, size_t workspace_bytes, void* stream) {
-    sa::AttnArgs a;
+    sa::AttnArgs a, cls;
     size_t need = 0;
+    bool by_classes = false;
     const int st = check_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind, col_ptr,
                              row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse, strides,
-                             softmax_scale, dq, dk, dv, &a, &need);
+                             softmax_scale, dq, dk, dv, &a, &need, &by_classes, &cls);
     if (st != SA_OK) return st;
     if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
     if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;
-    hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
-                                  static_cast<hipStream_t>(stream));
+    hipError_t e = launch_bwd(a, by_classes, cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
+                              static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
@@ -398,11 +478,12 @@ int sparse_attn_bwd_noalloc(int64_t n, int32_t block, int32_t stride_l, int32_t 
                             int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
                             const void* o, const void* dout, const float* lse, const int64_t* strides,
                             float softmax_scale, void* dq, void* dk, void* dv, void* stream) {
-    sa::AttnArgs a;
+    sa::AttnArgs a, cls;
     size_t need = 0;
+    bool by_classes = false;
     int st = check_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind, col_ptr, row_idx,
                        kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse, strides, softmax_scale, dq, dk,
-                       dv, &a, &need);
+                       dv, &a, &need, &by_classes, &cls);
     if (st != SA_OK) return st;
     if (need > kScratchBytes) return SA_ERR_BUFFER_TOO_SMALL;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -411,7 +492,7 @@ int sparse_attn_bwd_noalloc(int64_t n, int32_t block, int32_t stride_l, int32_t 
     if (st != SA_OK) return st;
     // the workspace's contents on entry are ignored: the pre kernel writes the
     // row statistics and empties the work counters before anything reads them
-    hipError_t e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
+    hipError_t e = launch_bwd(a, by_classes, cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

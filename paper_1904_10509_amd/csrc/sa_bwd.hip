@@ -129,13 +129,13 @@ size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, 
 
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                      void* dv, void* workspace, hipStream_t stream) {
+                      void* dv, void* workspace, hipStream_t stream, int parts) {
     const BwdWorkspace ws = bwd_workspace(workspace, (int64_t)a.batch * a.heads * a.n, layout_count(a.mode, a.sub));
     if (dtype == 1) {
         switch (a.d) {
-        case 32: return bwd_bf16_d32(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-        case 64: return bwd_bf16_d64(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-        default: return bwd_bf16_d128(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+        case 32: return bwd_bf16_d32(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
+        case 64: return bwd_bf16_d64(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
+        default: return bwd_bf16_d128(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
         }
     }
     switch (a.d) {

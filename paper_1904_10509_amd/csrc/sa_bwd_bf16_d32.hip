@@ -6,8 +6,8 @@ namespace sa {
 
 hipError_t bwd_bf16_d32(const AttnArgs& a, const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv, const BwdWorkspace& ws,
-                        hipStream_t stream) {
-    return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+                        hipStream_t stream, int parts) {
+    return launch_bwd_bf16_d<32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
 }
 
 }  // namespace sa

@@ -66,13 +66,13 @@ struct BwdWorkspace {
 // bf16 backward of one head size (one translation unit each, sa_bwd_bf16_d*.hip).
 hipError_t bwd_bf16_d32(const AttnArgs& a, const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv, const BwdWorkspace& ws,
-                        hipStream_t stream);
+                        hipStream_t stream, int parts);
 hipError_t bwd_bf16_d64(const AttnArgs& a, const void* q, const void* k, const void* v, const void* o,
                         const void* dout, const float* lse, void* dq, void* dk, void* dv, const BwdWorkspace& ws,
-                        hipStream_t stream);
+                        hipStream_t stream, int parts);
 hipError_t bwd_bf16_d128(const AttnArgs& a, const void* q, const void* k, const void* v, const void* o,
                          const void* dout, const float* lse, void* dq, void* dk, void* dv, const BwdWorkspace& ws,
-                         hipStream_t stream);
+                         hipStream_t stream, int parts);
 
 namespace {
 
@@ -263,8 +263,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     const int lay = head_layout(a, h);
     const MaskParams mp = head_mask_params(a, PAT, MODE, h);
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-    const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
     const int row0 = qb * BLK + w * C::RW;
+    const int qs0 = qb * BLK - a.qshift;  // first query row of the block as the masks see it
     const float c2 = a.scale_log2;
     constexpr uint64_t kTileBits = BLK == 64 ? ~0ull : (1ull << BLK) - 1;
 
@@ -283,16 +283,21 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             qf[u][ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
             of[u][ks] = ld_bf16x8(dout + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
         }
-        nl2[u] = nlse2[rowbase + i];
-        const float nd = ndelta[rowbase + i];
+        nl2[u] = nlse2[stat_index(a, b, h, i)];
+        const float nd = ndelta[stat_index(a, b, h, i)];
         nd4[u] = f32x4{nd, nd, nd, nd};
-        rl[u] = row_lane(i, a.dl);
+        rl[u] = row_lane(i - a.qshift, a.dl);
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) dqacc[u][db] = zero4();
     }
 
-    const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
+    int e0 = 0, e1 = qb + 1;  // WALK_DENSE: key blocks 0 .. qb
+    if (a.walk != WALK_DENSE) {
+        const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
+        e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]);
+        e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
+        if (a.walk == WALK_BAND) e0 = max(e0, e1 - (a.l / BLK + 1));
+    }
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
     // A step stages one block, or two summary halves (see RowStepper) as one tile
@@ -324,7 +329,8 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     auto walk = [&](auto pass) {
     constexpr bool kSumD = decltype(pass)::value == 0;  // the walk that sums D
     // two-stage ring; the next step's blocks are read one step ahead
-    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK),
+                             a.walk == WALK_DENSE};
     RowStep cur = steps.next();
     if (cur.a >= 0) load_step(cur, 0);
     two_stage_while([&](auto stage) {
@@ -335,7 +341,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         const int j0 = kb * BLK;
         // a pair of summary halves is attended everywhere
         const bool masked =
-            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qs0, qs0 + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // this step is in LDS everywhere; the other stage is free
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
@@ -344,7 +350,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         if constexpr (PAT == STRIDED) {
             // a single diagonal (see the forward): per row one score, one dS and
             // dQ += dS k as a rank-1 step in registers
-            if (diag_far && far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+            if (diag_far && far_block(PAT, a.dl, qs0, j0, BLK)) {
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) {
                     const int kk = w * C::RW + 16 * u + r;  // this lane's row, and its key, in the block
@@ -385,7 +391,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             if constexpr (!decltype(full)::value) {
                 const int j0_mod = mod_l(a.dl, j0);
                 const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-                const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+                const bool far = far_block(PAT, a.dl, qs0, j0, BLK);
                 if (PAT == FIXED && far && mp.part != PART_A1) {
                     // every row attends exactly the summary keys: one mask for the wave
                     const uint64_t sb = sum & kTileBits;
@@ -535,7 +541,7 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
         for (int u = 0; u < C::QBW; ++u) {
             const float nd = -sum_over_g(dsum[u]);
             nd4[u] = f32x4{nd, nd, nd, nd};
-            if (g == 0) ndelta[rowbase + row0 + 16 * u + r] = nd;
+            if (g == 0) ndelta[stat_index(a, b, h, row0 + 16 * u + r)] = nd;
         }
         __syncthreads();  // every wave is done with the ring before it is refilled
     }
@@ -546,8 +552,12 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     for (int u = 0; u < C::QBW; ++u) {
         uint16_t* drow = dq + base + (int64_t)(row0 + 16 * u + r) * a.ss;
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
-            *reinterpret_cast<uint2*>(drow + db * 16 + 4 * g) = pack_bf16x4_bits(dqacc[u][db] * a.scale);
+        for (int db = 0; db < C::DB; ++db) {
+            uint2* dst = reinterpret_cast<uint2*>(drow + db * 16 + 4 * g);
+            f32x4 x = dqacc[u][db] * a.scale;
+            if (a.epilogue == EPI_ADD) x += bf16x4_to_f32x4(*dst);
+            *dst = pack_bf16x4_bits(x);
+        }
     }
 }
 
@@ -614,8 +624,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     uint64_t per_layout = 0;  // item slots taken per (batch, head): the largest item count of a layout
     if (tid == 0) {
         const int n_layouts = layout_count(a.mode, a.sub);
-        for (int gl = 0; gl < n_layouts; ++gl)
-            per_layout = (uint64_t)items[gl] > per_layout ? (uint64_t)items[gl] : per_layout;
+        // walks of the band or of every block take the key blocks whole, in
+        // order (the longest columns first when dense); no item order is built
+        if (a.walk != WALK_LAYOUT) per_layout = (uint64_t)a.nq;
+        else
+            for (int gl = 0; gl < n_layouts; ++gl)
+                per_layout = (uint64_t)items[gl] > per_layout ? (uint64_t)items[gl] : per_layout;
         unsigned xcc;
         asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcc));
         qx = (int)(xcc % kQueues);
@@ -681,7 +695,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
         const int h = bh % a.heads, b = bh / a.heads;
         const int lay = head_layout(a, h);
-        const int32_t code = __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
+        const int32_t code = a.walk != WALK_LAYOUT ? item_code(rank, 0)
+                                                   : __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
         if (code < 0) {  // an empty slot (a layout with fewer items than another)
             if (tid == 0) sItem[(it + 1) & 1] = next;
             __syncthreads();
@@ -698,7 +713,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         const int kb_w = pair && w >= 2 ? kb + a.l / 64 : kb;  // this wave's key block
         const MaskParams mp = head_mask_params(a, PAT, MODE, h);
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-        const int64_t rowbase = ((int64_t)b * a.heads + h) * a.n;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
         // that the waves share the summary columns of the fixed pattern (which
         // sit at the end of a block) and with them the softmax work.  In a
@@ -732,9 +746,13 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 dkacc[kbw][db] = zero4();
             }
 
-        const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
-        const int e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
-        int len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
+        int e0 = 0, len = a.nq - kb;  // WALK_DENSE: query blocks kb .. nq - 1
+        if (a.walk != WALK_DENSE) {
+            const int64_t cp = (int64_t)lay * (a.nq + 1) + kb;
+            e0 = __builtin_amdgcn_readfirstlane(col_ptr[cp]);
+            len = __builtin_amdgcn_readfirstlane(col_ptr[cp + 1]) - e0;
+            if (a.walk == WALK_BAND) len = min(len, a.l / BLK + 1);
+        }
         if (single && ((key_summary >> (32 * (half - 1))) & 0xFFFFFFFFull) == 0ull) {
             // the non-summary half is attended only inside its own l-block:
             // the column's first entries (the query blocks ascend)
@@ -749,26 +767,30 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         // The column is walked from its last query block down: the long
         // columns of a head, started together, then visit the same query
         // blocks at about the same time and share those Q / dO tiles in L2.
-        auto entry = [&](int sidx) { return e0 + len - 1 - sidx; };
+        auto query_block = [&](int sidx) {
+            return a.walk == WALK_DENSE ? kb + len - 1 - sidx
+                                        : __builtin_amdgcn_readfirstlane(row_idx[e0 + len - 1 - sidx]);
+        };
         auto load_block = [&](int qb, int stage) {
             const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
             ld.issue(q + qbase, sQ_base + stage * kTileBytes);
             ld.issue(dout + qbase, sdO_base + stage * kTileBytes);
-            if (w == 0) load_row_stats_async(nlse2 + rowbase + (int64_t)qb * BLK, BLK, sL_base + stage * 256u, lane);
+            const int64_t st0 = stat_index(a, b, h, (int64_t)qb * BLK);
+            if (w == 0) load_row_stats_async(nlse2 + st0, BLK, sL_base + stage * 256u, lane, (uint32_t)a.lse_ss);
             if (w == C::NW - 1)
-                load_row_stats_async(ndelta + rowbase + (int64_t)qb * BLK, BLK, sDl_base + stage * 256u, lane);
+                load_row_stats_async(ndelta + st0, BLK, sDl_base + stage * 256u, lane, (uint32_t)a.lse_ss);
         };
 
         wait_loads_upto<0>();  // register loads done before the ring starts
         // two-stage ring: the next block's index is read one step ahead (a
         // scalar load, off the vector-memory counter the ring waits on)
-        int qb_next = len > 0 ? __builtin_amdgcn_readfirstlane(row_idx[entry(0)]) : 0;
+        int qb_next = len > 0 ? query_block(0) : 0;
         if (len > 0) load_block(qb_next, 0);
         two_stage_loop(len, [&](auto stage, int sidx) {
             constexpr int st = decltype(stage)::value;
             const int qb = qb_next;
-            qb_next = sidx + 1 < len ? __builtin_amdgcn_readfirstlane(row_idx[entry(sidx + 1)]) : 0;
-            const int i0 = qb * BLK;
+            qb_next = sidx + 1 < len ? query_block(sidx + 1) : 0;
+            const int i0 = qb * BLK - a.qshift;  // first query row of the block as the masks see it
             // a pair's keys are summary keys, attended by every query of a block
             // away from both key blocks' l-blocks
             const bool masked =
@@ -1030,8 +1052,15 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
 #pragma unroll
             for (int db = 0; db < C::DB; ++db) {
-                *reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g) = pack_bf16x4_bits(dvacc[kbw][db]);
-                *reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g) = pack_bf16x4_bits(dkacc[kbw][db] * a.scale);
+                uint2* dvp = reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g);
+                uint2* dkp = reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g);
+                f32x4 xv = dvacc[kbw][db], xk = dkacc[kbw][db] * a.scale;
+                if (a.epilogue == EPI_ADD) {
+                    xv += bf16x4_to_f32x4(*dvp);
+                    xk += bf16x4_to_f32x4(*dkp);
+                }
+                *dvp = pack_bf16x4_bits(xv);
+                *dkp = pack_bf16x4_bits(xk);
             }
         }
         if (tid == 0) sItem[(it + 1) & 1] = next;
@@ -1114,7 +1143,7 @@ inline bool split_products(const AttnArgs& a) {
 template <int D, int BLK>
 hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                           void* dv, const BwdWorkspace& ws, hipStream_t stream) {
+                           void* dv, const BwdWorkspace& ws, hipStream_t stream, int parts) {
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     float* ndelta = ws.ndelta;
     float* nlse2 = ws.nlse2;
@@ -1148,10 +1177,11 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         // (n = 65,536, l = 256, 8 heads: 3% faster).
         const int64_t per_head = (int64_t)qgrid / bh_count;
         ak.pairs = PAT == FIXED && BLK == 64 && a.l % 64 == 0 && 2 * ((int64_t)a.n / a.l) >= 5 * per_head;
-        hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, ak,
-                           (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items,
-                           ws.order);
-        (void)with_full_body<PAT>(a, [&](auto fb) {
+        if (parts & BWD_PRE)
+            hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, ak,
+                               (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items,
+                               ws.order);
+        if (parts & BWD_DQ) (void)with_full_body<PAT>(a, [&](auto fb) {
             auto dq_kernel = [&](auto sp) {
                 hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value, decltype(sp)::value>),
                                    grid, dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx,
@@ -1172,7 +1202,8 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                                (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)dout, nlse2, ndelta,
                                (uint16_t*)dk, (uint16_t*)dv, ws.queue, ws.items, ws.order);
         };
-        if constexpr (PAT == FIXED) {
+        if (!(parts & BWD_DKDV)) {
+        } else if constexpr (PAT == FIXED) {
             if (split) dkdv(std::true_type{});
             else dkdv(std::false_type{});
         } else {
@@ -1185,11 +1216,11 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
 template <int D>
 hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, const void* v,
                              const void* o, const void* dout, const float* lse, void* dq,
-                             void* dk, void* dv, const BwdWorkspace& ws, hipStream_t stream) {
+                             void* dk, void* dv, const BwdWorkspace& ws, hipStream_t stream, int parts) {
     switch (a.block) {
-    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
-    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream);
+    case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
+    case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
+    default: return launch_bwd_bf16<D, 64>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
     }
 }
 

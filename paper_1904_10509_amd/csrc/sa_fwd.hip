@@ -65,6 +65,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const MaskParams mp = head_mask_params(a, PAT, MODE, h);
     const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
     const int row0 = qb * BLK + w * C::RW;  // first query row of this wave
+    const int qs0 = qb * BLK - a.qshift;    // first query row of the block as the masks see it
 
     bf16x8 qf[C::QBW][C::KS];
     f32x4 oacc[C::QBW][C::DB];
@@ -79,11 +80,16 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         for (int db = 0; db < C::DB; ++db) oacc[u][db] = zero4();
         m_run[u] = -INFINITY;
         l_run[u] = 0.f;
-        rl[u] = row_lane(row0 + 16 * u + r, a.dl);
+        rl[u] = row_lane(row0 + 16 * u + r - a.qshift, a.dl);
     }
 
-    const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    const int e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]), e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
+    int e0 = 0, e1 = qb + 1;  // WALK_DENSE: key blocks 0 .. qb
+    if (a.walk != WALK_DENSE) {
+        const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
+        e0 = __builtin_amdgcn_readfirstlane(row_ptr[rp]);
+        e1 = __builtin_amdgcn_readfirstlane(row_ptr[rp + 1]);
+        if (a.walk == WALK_BAND) e0 = max(e0, e1 - (a.l / BLK + 1));
+    }
     TileLoader<D, BLK, C::NW> ld;
     ld.init(a.ss, w, lane);
     // A step stages one block, or two summary halves (see RowStepper) as one tile
@@ -112,7 +118,8 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     const float c2 = a.scale_log2;
     // two-stage ring; the next step's blocks are read one step ahead (scalar
     // loads, off the vector-memory counter the ring waits on)
-    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK)};
+    RowStepper<kPairs> steps{col_idx, e0, e1, RowStepper<kPairs>::pair_bound(mp, a.dl, qb * BLK),
+                             a.walk == WALK_DENSE};
     // strided blocks away from the band are single diagonals (see the step)
     const bool diag_far = PAT == STRIDED && mp.part != PART_A1 && a.l % BLK == 0;
     RowStep cur = steps.next();
@@ -127,7 +134,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
         const int j0 = kb * BLK;
         // a pair of summary halves is attended everywhere
         const bool masked =
-            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qb * BLK, qb * BLK + BLK - 1, j0, j0 + BLK - 1);
+            cur.b < 0 && !block_full32(PAT, mp.part, a.dl, a.c, mp.w, qs0, qs0 + BLK - 1, j0, j0 + BLK - 1);
         wait_loads_upto<0>();
         __syncthreads();  // this step is in LDS everywhere; the other stage is free
         if (nxt.a >= 0) load_step(nxt, st ^ 1);
@@ -139,7 +146,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             // gains one score, so the online softmax takes a rank-1 step in
             // registers, q . k and O += p v, instead of a masked chunk of
             // products.
-            if (diag_far && far_block(PAT, a.dl, qb * BLK, j0, BLK)) {
+            if (diag_far && far_block(PAT, a.dl, qs0, j0, BLK)) {
 #pragma unroll
                 for (int u = 0; u < C::QBW; ++u) {
                     const int kk = w * C::RW + 16 * u + r;  // this lane's row, and its key, in the block
@@ -189,7 +196,7 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
             if constexpr (!decltype(full)::value) {
                 const int j0_mod = mod_l(a.dl, j0);
                 const uint64_t sum = PAT == FIXED ? summary_bits(mp, j0_mod) : 0ull;
-                const bool far = far_block(PAT, a.dl, qb * BLK, j0, BLK);
+                const bool far = far_block(PAT, a.dl, qs0, j0, BLK);
                 if (PAT == FIXED && far && mp.part != PART_A1) {
                     // every row attends exactly the summary keys: one mask for the wave
                     const uint64_t sb = sum & kTileBits;
@@ -343,15 +350,36 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     for (int u = 0; u < C::QBW; ++u) {
         const int i = row0 + 16 * u + r;
         const float l_tot = sum_over_g(l_run[u]);
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
         uint16_t* orow = o + base + (int64_t)i * a.ss;
+        float* lrow = lse + stat_index(a, b, h, i);
+        if (a.epilogue == EPI_MERGE) {
+            // O and LSE of another, disjoint part of the row's set are already
+            // there: with weights exp(LSE_part - LSE) the union's softmax is
+            // O = (w1 O1 + exp(m scale - mx) acc) / z, LSE = mx + log z
+            const float lse1 = *lrow;
+            const float lse2 = l_tot > 0.f ? m_run[u] * a.scale + __logf(l_tot) : -INFINITY;
+            const float mx = fmaxf(lse1, lse2);
+            const float w1 = lse1 == -INFINITY ? 0.f : __expf(lse1 - mx);
+            const float w2 = l_tot > 0.f ? __expf(m_run[u] * a.scale - mx) : 0.f;  // weight of acc
+            const float z = w1 + w2 * l_tot;
+            const float inv = z > 0.f ? 1.f / z : 0.f;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                uint2* dst = reinterpret_cast<uint2*>(orow + db * 16 + 4 * g);
+                const bf16x4 o1 = __builtin_bit_cast(bf16x4, *dst);
+                f32x4 x;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) x[t] = (w1 * (float)o1[t] + w2 * oacc[u][db][t]) * inv;
+                *dst = pack_bf16x4_bits(x);
+            }
+            if (g == 0) *lrow = z > 0.f ? mx + __logf(z) : -INFINITY;
+            continue;
+        }
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
         for (int db = 0; db < C::DB; ++db)
             *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pack_bf16x4_bits(oacc[u][db] * inv);
-        if (g == 0) {
-            const float val = l_tot > 0.f ? m_run[u] * a.scale + __logf(l_tot) : -INFINITY;
-            lse[((int64_t)b * a.heads + h) * a.n + i] = val;
-        }
+        if (g == 0) *lrow = l_tot > 0.f ? m_run[u] * a.scale + __logf(l_tot) : -INFINITY;
     }
 }
 
@@ -402,7 +430,7 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
     }
     float inv = l > 0.f ? 1.f / l : 0.f;
     for (int t = 0; t < D; ++t) o[base + (int64_t)i * a.ss + t] = acc[t] * inv;
-    lse[((int64_t)b * a.heads + h) * a.n + i] = l > 0.f ? m + logf(l) : -INFINITY;
+    lse[stat_index(a, b, h, i)] = l > 0.f ? m + logf(l) : -INFINITY;
 }
 
 template <int D, int BLK>

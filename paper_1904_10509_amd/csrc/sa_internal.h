@@ -52,6 +52,23 @@ inline hipError_t with_pattern_mode(int pattern, int mode, F&& f) {
 // Orders in which the dK / dV kernel takes its work.
 enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2 };
 
+// Which blocks a kernel walks:
+//   WALK_LAYOUT  the present blocks of the layout;
+//   WALK_BAND    of a strided layout with l a multiple of B, only the blocks of
+//                the band A1 = {i - l .. i}: the last l / B + 1 entries of a
+//                row, the first l / B + 1 of a column (they hold no other
+//                pair of the merged set);
+//   WALK_DENSE   every block kb <= qb, without a layout (dense causal).
+enum { WALK_LAYOUT = 0, WALK_BAND = 1, WALK_DENSE = 2 };
+
+// What a kernel does with its result:
+//   EPI_STORE  writes it;
+//   EPI_MERGE  (forward) combines it, by log-sum-exp, with the O and LSE
+//              already in the outputs (a softmax over a disjoint part of
+//              each row's set);
+//   EPI_ADD    (dQ, dK, dV) adds it to the gradient already in the output.
+enum { EPI_STORE = 0, EPI_MERGE = 1, EPI_ADD = 2 };
+
 // Everything a kernel needs to know about one call.
 struct AttnArgs {
     int32_t pattern, mode;
@@ -67,6 +84,10 @@ struct AttnArgs {
     int32_t claim_mode;    // dK / dV work order, one of CLAIM_* (set by the backward launcher)
     int32_t pairs;         // dK / dV: summary halves walked in pairs (set by the backward launcher)
     DivL dl;               // division by l
+    int32_t walk;          // WALK_*
+    int32_t qshift;        // masks see query i as i - qshift (a causal limit j <= i - qshift)
+    int32_t epilogue;      // EPI_*
+    int64_t lse_sb, lse_sh, lse_ss;  // element strides of LSE and the row statistics (batch, head, row)
     const int32_t* row_ptr;
     const int32_t* col_idx;
     const uint8_t* kind;
@@ -74,6 +95,11 @@ struct AttnArgs {
     const int32_t* row_idx;
     const uint8_t* kind_t;
 };
+
+// Index of row i of (batch b, head h) in LSE and the backward's row statistics.
+__host__ __device__ inline int64_t stat_index(const AttnArgs& a, int b, int h, int64_t i) {
+    return (int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh + i * a.lse_ss;
+}
 
 // Layout that head h reads.
 __host__ __device__ inline int head_layout(const AttnArgs& a, int h) { return layout_of_head(a.mode, a.sub, h); }
@@ -137,8 +163,13 @@ hipError_t merge_launch(int dtype, const void* o1, const float* lse1, const void
 hipError_t add_shifted_launch(int dtype, void* dst, const void* src, int64_t rows, int64_t n, int d, int64_t shift,
                               hipStream_t stream);
 
+// Launches of a backward call: the row statistics (pre), dQ, and dK / dV.
+enum { BWD_PRE = 1, BWD_DQ = 2, BWD_DKDV = 4, BWD_ALL = 7 };
+
+// Backward; `parts` selects launches of the bf16 path (the fp32 path always
+// runs all of them).
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
-                      void* dv, void* workspace, hipStream_t stream);
+                      void* dv, void* workspace, hipStream_t stream, int parts = BWD_ALL);
 
 }  // namespace sa

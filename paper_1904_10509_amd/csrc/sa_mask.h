@@ -32,7 +32,7 @@ __device__ inline uint64_t bit_range(int lo, int hi) {
 // Bits at positions m, m + l, m + 2l, ... below 64, from `period_bits`
 // (bits at 0, l, 2l, ... precomputed for the call).
 __device__ inline uint64_t periodic_from(uint64_t period_bits, int m) {
-    return m >= 64 ? 0ull : (period_bits << m);
+    return (unsigned)m >= 64u ? 0ull : (period_bits << m);  // m < 0 (never used) also gives 0
 }
 
 // Non-negative remainder.
@@ -152,6 +152,7 @@ struct RowStepper {
     const int32_t* col_idx;
     int e, e1;    // next entry, end of the row
     int far_end;  // pairs are formed below this key block; 0: no pairs
+    bool dense;   // no layout: entry e is key block e
     __device__ static int pair_bound(const MaskParams& p, const DivL& dl, int i0) {
         if (p.pattern != FIXED || p.part == PART_A1 || p.c != 32 || p.l % 64 != 0 || p.w % 32 != 0) return 0;
         return (i0 - mod_l(dl, i0)) / 64;
@@ -159,7 +160,7 @@ struct RowStepper {
     __device__ RowStep next() {
         RowStep s{-1, -1};
         if (e >= e1) return s;
-        s.a = __builtin_amdgcn_readfirstlane(col_idx[e]);
+        s.a = dense ? e : __builtin_amdgcn_readfirstlane(col_idx[e]);
         ++e;
         if constexpr (PAIRS) {
             if (e < e1) {

@@ -64,6 +64,12 @@ __device__ inline uint2 pack_bf16x4_bits(f32x4 v) {
     return __builtin_bit_cast(uint2, a);
 }
 
+// Four bf16 (8 bytes) to fp32, exactly.
+__device__ inline f32x4 bf16x4_to_f32x4(uint2 u) {
+    return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                 __uint_as_float(u.y & 0xffff0000u)};
+}
+
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // sum_e a[e] b[e] over 8 bf16 pairs in fp32: four v_dot2_f32_bf16 on two

@@ -126,11 +126,12 @@ struct TileLoader {
     }
 };
 
-// 64 consecutive fp32 values starting at src (one per lane, lanes past
-// n_valid repeat the last value) to LDS byte address dst: one direct-to-LDS load.
-__device__ inline void load_row_stats_async(const float* src, int n_valid, uint32_t dst, int lane) {
+// 64 fp32 values src[0], src[stride], ... (one per lane, lanes past n_valid
+// repeat the last value) to LDS byte address dst: one direct-to-LDS load.
+__device__ inline void load_row_stats_async(const float* src, int n_valid, uint32_t dst, int lane,
+                                            uint32_t stride = 1) {
     const uint32_t i = (uint32_t)(lane < n_valid ? lane : n_valid - 1);
-    dma_b32(uniform_ptr(src), 4u * i, dst);
+    dma_b32(uniform_ptr(src), 4u * i * stride, dst);
 }
 
 // s_waitcnt vmcnt(N): at most N of this wave's global loads (including the

@@ -115,6 +115,19 @@ SMALL_CASES = [
     # the largest number of subblocks (64, l = 128, c = 2), and eight with l <= 64
     (P, MG, 1024, 64, 128, 2, 32, torch.bfloat16, 1, 64),
     (P, A2, 512, 16, 64, 8, 32, torch.bfloat16, 1, 8),
+    # strided merged and A2 heads with l | n and n / l a multiple of 16 take
+    # A2 by residue classes (the band over the layout, then dense causal
+    # attention inside each class, merged in place): classes of 16, 32, 48,
+    # 96 and 256 positions (class blocks of 16, 32, 16, 32, 64), l / B of 1, 2,
+    # 4, A2 alone with l < B, d = 32 / 64 / 128, several (batch, head) pairs
+    (S, MG, 1024, 32, 64, 0, 64, torch.bfloat16, 2, 3),
+    (S, MG, 2048, 64, 64, 0, 128, torch.bfloat16, 1, 2),
+    (S, MG, 3072, 16, 32, 0, 32, torch.bfloat16, 1, 2),
+    (S, MG, 4096, 16, 16, 0, 64, torch.bfloat16, 1, 2),
+    (S, MG, 8192, 32, 128, 0, 64, torch.bfloat16, 1, 2),
+    (S, A2, 1536, 64, 32, 0, 64, torch.bfloat16, 2, 2),
+    (S, A2, 2048, 32, 8, 0, 32, torch.bfloat16, 1, 2),
+    (S, A2, 3072, 64, 32, 0, 128, torch.bfloat16, 1, 1),
     # few summary keys per row (c = 1, 2), A2 alone, many heads: the summary
     # columns sum hundreds of large weights, so the dV / dK products take P and
     # dS in two bf16 parts (shared window and a subblock per head; B = 64 with
@@ -313,6 +326,24 @@ def test_autograd_wrapper():
     check("autograd dq", to64(q.grad), ref["dq"], torch.bfloat16)
     check("autograd dk", to64(k.grad), ref["dk"], torch.bfloat16)
     check("autograd dv", to64(v.grad), ref["dv"], torch.bfloat16)
+
+
+def test_strided_classes_with_views():
+    """The strided merged path by residue classes on [b, n, h, d] storage seen
+    as [b, h, n, d] (batch 1: heads and rows in one stride pattern), against
+    the oracle."""
+    dev = device()
+    n, l, B, d, h = 2048, 64, 64, 64, 3
+    x = make_inputs(1, h, n, d, torch.bfloat16, seed=29)
+    lay = sa.build_layout(n, B, l, 0, S, MG, device=dev)
+    q, k, v, dout = (x[n_].transpose(1, 2).contiguous().to(dev).transpose(1, 2) for n_ in ("q", "k", "v", "dout"))
+    assert not q.is_contiguous()
+    o, lse = sa.forward(q, k, v, lay)
+    dq, dk, dv = sa.backward(q, k, v, o, dout, lse, lay)
+    torch.cuda.synchronize()
+    ref = orc_mod.backward(*oracle_inputs(x), pattern=S, mode=MG, l=l, c=0, scale=d ** -0.5)
+    got = {"o": to64(o), "lse": to64(lse), "dq": to64(dq), "dk": to64(dk), "dv": to64(dv)}
+    check_all("strided classes, [b, n, h, d] views", got, ref, torch.bfloat16, names=("o", "lse", "dq", "dk", "dv"))
 
 
 def test_autograd_wrapper_transposed_views():
