@@ -198,6 +198,33 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The stages of sparse_attn_bwd (bf16), for callers that schedule them
+ * themselves (the dQ and the dK / dV stages of one call, given the row
+ * statistics, touch disjoint outputs) and for timing the stages apart:
+ *   SA_BWD_ROW_STATS  D_i = dO_i . O_i and the LSE in base 2, per row, into the
+ *                     workspace (Sec. 5.4: the only per-row state the
+ *                     recomputation needs besides LSE);
+ *   SA_BWD_DQ         dQ, row by row over the layout;
+ *   SA_BWD_DKDV       dK and dV, column by column.
+ * `stages` is a bit set of them; stages run in this order within a call, and
+ * a stage needs the earlier ones of the same call (same arguments, same
+ * workspace) already enqueued: SA_BWD_DQ and SA_BWD_DKDV read the row
+ * statistics, and SA_BWD_DKDV also reads D where the dQ stage recomputes it
+ * (fixed pattern with few summary keys per row).  All three in one call equal
+ * sparse_attn_bwd.  Arguments and errors as sparse_attn_bwd; SA_ERR_INVALID for
+ * an empty or unknown set, SA_ERR_UNSUPPORTED for a partial set in fp32.
+ */
+enum { SA_BWD_ROW_STATS = 1, SA_BWD_DQ = 2, SA_BWD_DKDV = 4, SA_BWD_ALL_STAGES = 7 };
+
+int sparse_attn_bwd_stage(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                          int32_t head_mode, const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                          const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                          int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                          const void* o, const void* dout, const float* lse, const int64_t* strides,
+                          float softmax_scale, void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                          int32_t stages, void* stream);
+
+/*
  * sparse_attn_bwd without a caller workspace, for callers that cannot
  * allocate device memory (code under HIP graph capture, serving loops,
  * harnesses that forbid allocation).  Same arguments, results and errors as
@@ -265,26 +292,31 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
 /*
  * Strided pattern, merged heads (SA_STRIDED, SA_MODE_MERGED), with the A2
  * part computed by transposition (Sec. 5.5: reordered by residue mod l, a
- * stride of l becomes a local window).  Same results as sparse_attn_fwd /
- * sparse_attn_bwd over the merged layout, computed as
+ * stride of l becomes a local window), with the caller choosing the class
+ * block.  Same results as sparse_attn_fwd / sparse_attn_bwd over the merged
+ * layout (which take this route by themselves for bf16 when l divides n, B
+ * divides l and n / l is a multiple of 16), computed as
  *   the band  A1 = {max(0, i-l) .. i}: the block kernels over the strided A1
  *             layout (sparse_attn_layout with SA_MODE_A1 and the same n,
  *             block, stride_l, summary_c = 0), and
  *   the rest  {i - k l : k >= 2}: in each residue class (positions r + m l,
  *             m < M = n / l), query m attends keys m' <= m - 2, dense causal
- *             attention over blocks of class_block class positions,
- * combined through their log-sum-exps (the sets are disjoint).
+ *             attention over blocks of class_block class positions, read in
+ *             place through strided views,
+ * combined through their log-sum-exps (the sets are disjoint): the class
+ * kernels merge their part into the band's O and LSE, and add their
+ * gradients to the band's.
  * Requirements beyond the common ones: l divides n; class_block in
- * {16, 32, 64} divides M; M / class_block <= 4096 and batch * heads <= 65535
- * (else SA_ERR_UNSUPPORTED); q, k, v, o, dout, dq, dk, dv contiguous
- * [batch, heads, n, d_head] (no strides argument).
+ * {16, 32, 64} divides M (SA_ERR_INVALID otherwise); M / class_block <= 65535
+ * and batch * heads <= 65535 (else SA_ERR_UNSUPPORTED); q, k, v, o, dout, dq,
+ * dk, dv contiguous [batch, heads, n, d_head] (no strides argument).
  * Workspace: device memory of at least sparse_attn_transposed_workspace_size
- * bytes, 256-byte aligned (SA_ERR_INVALID otherwise); one size serves both
- * calls.  It holds a dense causal class layout, shifted copies of Q, O and
- * dO, partial outputs and gradients, and the backward scratch; its contents
- * on entry are ignored and calls sharing one workspace must not overlap.
- * The row pointers are those of the A1 layout; the backward also takes its
- * column form.  Outputs as for sparse_attn_fwd / sparse_attn_bwd.
+ * bytes (the backward's row statistics and schedule, as sparse_attn_bwd),
+ * 256-byte aligned (SA_ERR_INVALID otherwise); one size serves both calls,
+ * and the forward does not touch it.  Its contents on entry are ignored and
+ * calls sharing one workspace must not overlap.  The row pointers are those
+ * of the A1 layout; the backward also takes its column form.  Outputs as for
+ * sparse_attn_fwd / sparse_attn_bwd.
  */
 int sparse_attn_transposed_workspace_size(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
                                           int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, size_t* bytes);

@@ -1,7 +1,9 @@
 """Compile the HIP library libsparse_attn.so for gfx950, in-tree.
 
 Every source under csrc/ is compiled with hipcc into _build/ and linked into
-paper_1904_10509_amd/libsparse_attn.so next to this file.
+paper_1904_10509_amd/libsparse_attn.so next to this file.  The benchmark's
+measurement probe (probe/*.hip, the matrix-core peak and clock) becomes
+libsa_probe.so beside it.
 """
 import concurrent.futures as cf
 import os
@@ -11,6 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libsparse_attn.so")
+PROBE_DIR = os.path.join(HERE, "probe")
+PROBE_LIB = os.path.join(HERE, "libsa_probe.so")
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -24,12 +28,12 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
          "-I", os.path.join(os.path.dirname(HERE), "include")]
 
 
-def sources():
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+def sources(folder=CSRC):
+    return sorted(os.path.join(folder, f) for f in os.listdir(folder) if f.endswith(".hip"))
 
 
 def _compile(src):
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+    obj = os.path.join(BUILD, os.path.basename(os.path.dirname(src)) + "_" + os.path.basename(src) + ".o")
     cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     msgs = [ln for ln in (r.stdout + r.stderr).splitlines()
@@ -39,18 +43,25 @@ def _compile(src):
     return obj, "\n".join(msgs)
 
 
+def _link(objs, lib):
+    tmp = lib + ".tmp"
+    subprocess.run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs], check=True)
+    os.replace(tmp, lib)
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip and link the shared library; returns its path."""
+    """Compile every csrc/*.hip and probe/*.hip and link the two shared
+    libraries; returns the attention library's path."""
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
-        results = list(ex.map(_compile, sources()))
+    lib_srcs, probe_srcs = sources(CSRC), sources(PROBE_DIR)
+    with cf.ThreadPoolExecutor(max_workers=min(9, os.cpu_count() or 1)) as ex:
+        results = list(ex.map(_compile, lib_srcs + probe_srcs))
     for obj, msgs in results:
         if verbose and msgs.strip():
             print(msgs)
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *[o for o, _ in results]]
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    objs = [o for o, _ in results]
+    _link(objs[: len(lib_srcs)], LIB)
+    _link(objs[len(lib_srcs):], PROBE_LIB)
     return LIB
 
 

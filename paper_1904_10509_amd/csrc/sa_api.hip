@@ -144,31 +144,44 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
 // merged set's band A1 runs first over the caller's layout (only its band
 // blocks: with B dividing l, A2 \ A1 never meets them), and the class kernels
 // then combine their part into its O and LSE (forward) or add it to its
-// gradients (backward).  Returns false where the block path stays: fp32,
-// l not dividing n, n / l not a multiple of 16, batch and head strides that do
-// not merge, or sizes the class grid cannot hold.
+// gradients (backward).  class_args builds the class view's kernel arguments
+// for class blocks of cb positions (merged: queries shifted by two steps);
+// class_plan picks the class block and returns false where the block path
+// stays: fp32, l not dividing n, n / l not a multiple of 16, batch and head
+// strides that do not merge, or sizes the class grid cannot hold.
+int class_args(int64_t n, int32_t l, int32_t cb, int32_t mode, int32_t batch, int32_t heads, int32_t d,
+               int32_t dtype, const int64_t* strides, float scale, sa::AttnArgs* cls) {
+    if (n % l != 0) return SA_ERR_INVALID;
+    const int64_t M = n / l;  // positions per class
+    if (cb != 16 && cb != 32 && cb != 64) return SA_ERR_INVALID;
+    if (M % cb != 0) return SA_ERR_INVALID;
+    if (M / cb > 65535 || (int64_t)batch * heads > 65535) return SA_ERR_UNSUPPORTED;  // grid dimensions
+    if (batch > 1 && strides[0] != (int64_t)heads * strides[1]) return SA_ERR_UNSUPPORTED;  // (b, h) as one index
+    const int64_t cls_strides[3] = {strides[1], strides[2], (int64_t)l * strides[2]};
+    PatternArgs c;
+    int st = check_pattern(M, cb, (int32_t)M, 0, SA_STRIDED, SA_MODE_A1, &c);
+    if (st != SA_OK) return st;
+    st = check_tensor_args(c, batch * heads, l, d, dtype, cls_strides);
+    if (st != SA_OK) return st;
+    *cls = make_args(c, batch * heads, l, d, cls_strides, scale, nullptr, nullptr, nullptr, nullptr, nullptr,
+                     nullptr);
+    cls->walk = sa::WALK_DENSE;
+    cls->qshift = mode == SA_MODE_MERGED ? 2 : 0;
+    cls->lse_sb = n;  // row i = m l + r of pair bh sits at bh n + r + m l
+    cls->lse_sh = 1;
+    cls->lse_ss = l;
+    return SA_OK;
+}
+
 bool class_plan(const PatternArgs& p, int32_t batch, int32_t heads, int32_t d, int32_t dtype, const int64_t* strides,
                 float scale, sa::AttnArgs* cls) {
     if (p.pattern != sa::STRIDED || dtype != SA_BF16) return false;
     if (p.mode != SA_MODE_MERGED && p.mode != SA_MODE_A2) return false;
     if (p.n % p.l != 0 || (p.mode == SA_MODE_MERGED && p.l % p.block != 0)) return false;
-    const int64_t M = p.n / p.l;  // positions per class
+    const int64_t M = p.n / p.l;
     const int32_t cb = (M % 64 == 0 && M >= 256) ? 64 : (M % 32 == 0 ? 32 : (M % 16 == 0 ? 16 : 0));
-    if (cb == 0 || M / cb > 65535) return false;
-    if (batch > 1 && strides[0] != (int64_t)heads * strides[1]) return false;  // (b, h) as one index
-    if ((int64_t)batch * heads > 65535) return false;                            // grid dimension
-    const int64_t cls_strides[3] = {strides[1], strides[2], (int64_t)p.l * strides[2]};
-    PatternArgs c;
-    if (check_pattern(M, cb, (int32_t)M, 0, SA_STRIDED, SA_MODE_A1, &c) != SA_OK) return false;
-    if (check_tensor_args(c, batch * heads, p.l, d, dtype, cls_strides) != SA_OK) return false;
-    *cls = make_args(c, batch * heads, p.l, d, cls_strides, scale, nullptr, nullptr, nullptr, nullptr, nullptr,
-                     nullptr);
-    cls->walk = sa::WALK_DENSE;
-    cls->qshift = p.mode == SA_MODE_MERGED ? 2 : 0;
-    cls->lse_sb = p.n;  // row i = m l + r of pair bh sits at bh n + r + m l
-    cls->lse_sh = 1;
-    cls->lse_ss = p.l;
-    return true;
+    if (cb == 0) return false;
+    return class_args(p.n, p.l, cb, p.mode, batch, heads, d, dtype, strides, scale, cls) == SA_OK;
 }
 
 // Pattern arguments of a decoding step (no block size: S_pos is enumerated).
@@ -184,84 +197,30 @@ int check_decode_shape(int32_t batch, int32_t heads, int32_t d, int32_t dtype) {
     return SA_OK;
 }
 
-// Merged strided heads by transposition: the band (strided A1, blocks of
-// `block`) and the dense causal class attention (M = n / l positions per
-// class, blocks of `class_block`), with the workspace regions of both calls.
-constexpr int64_t kMaxClassBlockRows = 4096;
-
+// Merged strided heads by transposition through the explicit entry points:
+// the band over the caller's strided A1 layout, the classes in blocks of
+// class_block (see class_args); tensors contiguous.
 struct TransposedPlan {
-    PatternArgs band, cls;
-    int64_t rows, M, mq, nnz_c;
-    int64_t strides[3], class_strides[3];
-    size_t lay, t1, t2, t3, l1, l2, g1, g2, g3, bw, total;  // byte offsets
+    PatternArgs band;
+    int64_t strides[3];
+    sa::AttnArgs cls;
+    size_t workspace;  // bytes: the band backward's workspace
 };
 
-size_t align256(size_t x) { return (x + 255) / 256 * 256; }
-
 int plan_transposed(int64_t n, int32_t block, int32_t l, int32_t class_block, int32_t batch, int32_t heads, int32_t d,
-                    int32_t dtype, TransposedPlan* p) {
+                    int32_t dtype, float scale, TransposedPlan* p) {
     int st = check_pattern(n, block, l, 0, SA_STRIDED, SA_MODE_A1, &p->band);
     if (st != SA_OK) return st;
-    if (n % l != 0) return SA_ERR_INVALID;
-    p->M = n / l;
-    st = check_pattern(p->M, class_block, (int32_t)p->M, 0, SA_STRIDED, SA_MODE_A1, &p->cls);
-    if (st != SA_OK) return st;
-    p->mq = p->M / class_block;
-    if (p->mq > kMaxClassBlockRows) return SA_ERR_UNSUPPORTED;
-    p->nnz_c = p->mq * (p->mq + 1) / 2;
     if (batch < 1 || heads < 1) return SA_ERR_INVALID;
-    if ((int64_t)batch * heads > 65535) return SA_ERR_UNSUPPORTED;  // a grid dimension of the class call
     p->strides[0] = (int64_t)heads * n * d;
     p->strides[1] = n * d;
     p->strides[2] = d;
-    p->class_strides[0] = n * d;  // (batch, head) pairs
-    p->class_strides[1] = d;      // residue classes
-    p->class_strides[2] = (int64_t)l * d;
     st = check_tensor_args(p->band, batch, heads, d, dtype, p->strides);
     if (st != SA_OK) return st;
-    if ((int64_t)batch * heads > INT32_MAX) return SA_ERR_INVALID;
-    st = check_tensor_args(p->cls, batch * heads, l, d, dtype, p->class_strides);
+    st = class_args(n, l, class_block, SA_MODE_MERGED, batch, heads, d, dtype, p->strides, scale, &p->cls);
     if (st != SA_OK) return st;
-    p->rows = (int64_t)batch * heads * n;
-    const size_t tensor = (size_t)p->rows * d * (dtype == SA_BF16 ? 2 : 4);
-    const size_t stats = (size_t)p->rows * sizeof(float);
-    const size_t lay = 2 * (size_t)(p->mq + 1) * 4 + 2 * (size_t)p->nnz_c * 5 + 64;
-    size_t off = 0;
-    p->lay = off;
-    off += align256(lay);
-    size_t* tensors[] = {&p->t1, &p->t2, &p->t3, &p->g1, &p->g2, &p->g3};
-    for (size_t* t : tensors) {
-        *t = off;
-        off += align256(tensor);
-    }
-    p->l1 = off;
-    off += align256(stats);
-    p->l2 = off;
-    off += align256(stats);
-    const size_t bw_band = sa::bwd_workspace_bytes(batch, heads, n, p->band.nq, 1);
-    const size_t bw_cls = sa::bwd_workspace_bytes((int64_t)batch * heads, l, p->M, p->cls.nq, 1);
-    p->bw = off;
-    off += align256(bw_band > bw_cls ? bw_band : bw_cls);
-    p->total = off;
+    p->workspace = sa::bwd_workspace_bytes(batch, heads, n, p->band.nq, 1);
     return SA_OK;
-}
-
-// Class layout arrays inside the workspace.
-struct ClassLayout {
-    int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
-    uint8_t *kind, *kind_t;
-};
-ClassLayout class_layout(const TransposedPlan& p, char* ws) {
-    ClassLayout c;
-    char* b = ws + p.lay;
-    const size_t ptrs = (size_t)(p.mq + 1) * 4, idx = (size_t)p.nnz_c * 4;
-    c.row_ptr = reinterpret_cast<int32_t*>(b);
-    c.col_ptr = reinterpret_cast<int32_t*>(b + ptrs);
-    c.col_idx = reinterpret_cast<int32_t*>(b + 2 * ptrs);
-    c.row_idx = reinterpret_cast<int32_t*>(b + 2 * ptrs + idx);
-    c.kind = reinterpret_cast<uint8_t*>(b + 2 * ptrs + 2 * idx);
-    c.kind_t = c.kind + p.nnz_c;
-    return c;
 }
 
 // Arguments of a backward call, shared by sparse_attn_bwd and
@@ -294,20 +253,25 @@ int check_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int
 // The launches of a validated backward call (see class_plan): the band's
 // backward, then the classes' dQ and dK / dV added to it; A2 alone: the row
 // statistics, then the classes' dQ and dK / dV.
+// `parts`: the stages to launch (sa::BWD_*), in their order.
 hipError_t launch_bwd(sa::AttnArgs a, bool by_classes, sa::AttnArgs cls, int dtype, const void* q, const void* k,
                       const void* v, const void* o, const void* dout, const float* lse, void* dq, void* dk, void* dv,
-                      void* ws, hipStream_t s) {
-    if (!by_classes) return sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
-    hipError_t e;
-    if (a.mode == sa::MODE_MERGED) {
+                      void* ws, hipStream_t s, int parts = sa::BWD_ALL) {
+    if (!by_classes) return sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, parts);
+    // the band's part of each stage first (merged), then the classes' part
+    const bool merged = a.mode == sa::MODE_MERGED;
+    if (merged) {
         a.walk = sa::WALK_BAND;
-        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s);
         cls.epilogue = sa::EPI_ADD;
-    } else {
-        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_PRE);
     }
-    if (e == hipSuccess)
-        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DQ | sa::BWD_DKDV);
+    hipError_t e = hipSuccess;
+    for (int stage : {sa::BWD_PRE, sa::BWD_DQ, sa::BWD_DKDV}) {
+        if (!(parts & stage)) continue;
+        if (e == hipSuccess && (merged || stage == sa::BWD_PRE))
+            e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, stage);
+        if (e == hipSuccess && stage != sa::BWD_PRE)
+            e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, stage);
+    }
     return e;
 }
 
@@ -466,6 +430,31 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
+int sparse_attn_bwd_stage(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c, int32_t pattern,
+                          int32_t head_mode, const int32_t* row_ptr, const int32_t* col_idx, const uint8_t* kind,
+                          const int32_t* col_ptr, const int32_t* row_idx, const uint8_t* kind_t, int32_t batch,
+                          int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k, const void* v,
+                          const void* o, const void* dout, const float* lse, const int64_t* strides,
+                          float softmax_scale, void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                          int32_t stages, void* stream) {
+    if (stages < 1 || stages > SA_BWD_ALL_STAGES) return SA_ERR_INVALID;
+    sa::AttnArgs a, cls;
+    size_t need = 0;
+    bool by_classes = false;
+    const int st = check_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind, col_ptr,
+                             row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse, strides,
+                             softmax_scale, dq, dk, dv, &a, &need, &by_classes, &cls);
+    if (st != SA_OK) return st;
+    if (workspace_bytes < need) return SA_ERR_BUFFER_TOO_SMALL;
+    if (need > 0 && (!workspace || !aligned16(workspace))) return SA_ERR_INVALID;
+    // the fp32 path has no separate stages
+    const int parts = dtype == SA_BF16 ? stages : sa::BWD_ALL;
+    if (dtype != SA_BF16 && stages != SA_BWD_ALL_STAGES) return SA_ERR_UNSUPPORTED;
+    hipError_t e = launch_bwd(a, by_classes, cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace,
+                              static_cast<hipStream_t>(stream), parts);
+    return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
 int sparse_attn_bwd_noalloc_max_workspace(size_t* bytes) {
     if (!bytes) return SA_ERR_INVALID;
     *bytes = kScratchBytes;
@@ -543,10 +532,10 @@ int sparse_attn_decode(int64_t pos, int32_t stride_l, int32_t summary_c, int32_t
 int sparse_attn_transposed_workspace_size(int64_t n, int32_t block, int32_t stride_l, int32_t class_block,
                                           int32_t batch, int32_t heads, int32_t d_head, int32_t dtype, size_t* bytes) {
     TransposedPlan p;
-    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, 1.f, &p);
     if (st != SA_OK) return st;
     if (!bytes) return SA_ERR_INVALID;
-    *bytes = p.total;
+    *bytes = p.workspace;
     return SA_OK;
 }
 
@@ -555,32 +544,22 @@ int sparse_attn_fwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32
                                int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
                                const void* v, float softmax_scale, void* o, float* lse, void* workspace,
                                size_t workspace_bytes, void* stream) {
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
     TransposedPlan p;
-    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, softmax_scale, &p);
     if (st != SA_OK) return st;
     if (!row_ptr || !col_idx || !kind || !q || !k || !v || !o || !lse) return SA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SA_ERR_INVALID;
-    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
-    if (workspace_bytes < p.total) return SA_ERR_BUFFER_TOO_SMALL;
-    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return SA_ERR_INVALID;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
-    const ClassLayout cl = class_layout(p, ws);
-    float* lse1 = reinterpret_cast<float*>(ws + p.l1);
-    float* lse2 = reinterpret_cast<float*>(ws + p.l2);
-    hipError_t e = sa::causal_layout_launch((int32_t)p.mq, cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx,
-                                            cl.kind_t, s);
-    // the band: strided A1 over the caller's layout, into the workspace
+    if (workspace_bytes < p.workspace) return SA_ERR_BUFFER_TOO_SMALL;
+    if (p.workspace > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)) return SA_ERR_INVALID;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    // the band (strided A1 layout), then the classes merged into it
     const sa::AttnArgs band = make_args(p.band, batch, heads, d_head, p.strides, softmax_scale, row_ptr, col_idx,
                                         kind, nullptr, nullptr, nullptr);
-    if (e == hipSuccess) e = sa::fwd_launch(band, dtype, q, k, v, ws + p.t3, lse1, s);
-    // the rest: queries two class steps up, dense causal per class
-    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, q, ws + p.t1, p.rows, n, d_head, 2 * (int64_t)stride_l, s);
-    const sa::AttnArgs cls = make_args(p.cls, batch * heads, stride_l, d_head, p.class_strides, softmax_scale,
-                                       cl.row_ptr, cl.col_idx, cl.kind, nullptr, nullptr, nullptr);
-    if (e == hipSuccess) e = sa::fwd_launch(cls, dtype, ws + p.t1, k, v, ws + p.t2, lse2, s);
-    if (e == hipSuccess)
-        e = sa::merge_launch(dtype, ws + p.t3, lse1, ws + p.t2, lse2, o, lse, p.rows, n, d_head, stride_l, s);
+    sa::AttnArgs cls = p.cls;
+    cls.epilogue = sa::EPI_MERGE;
+    hipError_t e = sa::fwd_launch(band, dtype, q, k, v, o, lse, s);
+    if (e == hipSuccess) e = sa::fwd_launch(cls, dtype, q, k, v, o, lse, s);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
@@ -590,42 +569,27 @@ int sparse_attn_bwd_transposed(int64_t n, int32_t block, int32_t stride_l, int32
                                int32_t heads, int32_t d_head, int32_t dtype, const void* q, const void* k,
                                const void* v, const void* o, const void* dout, const float* lse, float softmax_scale,
                                void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
     TransposedPlan p;
-    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, &p);
+    const int st = plan_transposed(n, block, stride_l, class_block, batch, heads, d_head, dtype, softmax_scale, &p);
     if (st != SA_OK) return st;
     if (!row_ptr || !col_idx || !kind || !col_ptr || !row_idx || !kind_t) return SA_ERR_INVALID;
     if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return SA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(dq) ||
         !aligned16(dk) || !aligned16(dv))
         return SA_ERR_INVALID;
-    if (!isfinite(softmax_scale) || !(softmax_scale > 0.f)) return SA_ERR_INVALID;
-    if (workspace_bytes < p.total) return SA_ERR_BUFFER_TOO_SMALL;
-    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return SA_ERR_INVALID;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
-    const ClassLayout cl = class_layout(p, ws);
-    float* lse_c = reinterpret_cast<float*>(ws + p.l1);
-    const int64_t shift = 2 * (int64_t)stride_l;
-    hipError_t e = sa::causal_layout_launch((int32_t)p.mq, cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx,
-                                            cl.kind_t, s);
-    // the band, given the merged O and LSE: written to dq, dk, dv
+    if (workspace_bytes < p.workspace) return SA_ERR_BUFFER_TOO_SMALL;
+    if (p.workspace > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)) return SA_ERR_INVALID;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    // the band's backward given the merged O and LSE, then the classes' dQ and
+    // dK / dV added to it
     const sa::AttnArgs band = make_args(p.band, batch, heads, d_head, p.strides, softmax_scale, row_ptr, col_idx,
                                         kind, col_ptr, row_idx, kind_t);
-    if (e == hipSuccess) e = sa::bwd_launch(band, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws + p.bw, s);
-    // the rest: shifted copies of Q, O, dO and the class-order LSE (+inf on the padded tail)
-    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, q, ws + p.t1, p.rows, n, d_head, shift, s);
-    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, o, ws + p.t2, p.rows, n, d_head, shift, s);
-    if (e == hipSuccess) e = sa::shift_rows_launch(dtype, dout, ws + p.t3, p.rows, n, d_head, shift, s);
-    if (e == hipSuccess) e = sa::shift_lse_launch(lse, lse_c, p.rows, n, stride_l, s);
-    const sa::AttnArgs cls = make_args(p.cls, batch * heads, stride_l, d_head, p.class_strides, softmax_scale,
-                                       cl.row_ptr, cl.col_idx, cl.kind, cl.col_ptr, cl.row_idx, cl.kind_t);
+    sa::AttnArgs cls = p.cls;
+    cls.epilogue = sa::EPI_ADD;
+    hipError_t e = sa::bwd_launch(band, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace, s);
     if (e == hipSuccess)
-        e = sa::bwd_launch(cls, dtype, ws + p.t1, k, v, ws + p.t2, ws + p.t3, lse_c, ws + p.g1, ws + p.g2,
-                           ws + p.g3, ws + p.bw, s);
-    // sums: dq of position i takes row i - 2l of the shifted copy
-    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dq, ws + p.g1, p.rows, n, d_head, shift, s);
-    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dk, ws + p.g2, p.rows, n, d_head, 0, s);
-    if (e == hipSuccess) e = sa::add_shifted_launch(dtype, dv, ws + p.g3, p.rows, n, d_head, 0, s);
+        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, workspace, s, sa::BWD_DQ | sa::BWD_DKDV);
     return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

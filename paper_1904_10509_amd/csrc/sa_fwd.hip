@@ -386,6 +386,20 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
 // ---------------------------------------------------------------------------
 // fp32, VALU: one thread per query row
 // ---------------------------------------------------------------------------
+// The blocks of row qb a walk visits (see WALK_*), as entries e0 .. e1 of the
+// layout (WALK_DENSE: e is the key block itself).
+__device__ inline void row_entries(const AttnArgs& a, int lay, int qb, int* e0, int* e1) {
+    if (a.walk == WALK_DENSE) {
+        *e0 = 0;
+        *e1 = qb + 1;
+        return;
+    }
+    const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
+    *e0 = a.row_ptr[rp];
+    *e1 = a.row_ptr[rp + 1];
+    if (a.walk == WALK_BAND) *e0 = max(*e0, *e1 - (a.l / a.block + 1));
+}
+
 template <int D>
 __global__ void __launch_bounds__(64)
 fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict__ k,
@@ -405,13 +419,14 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
         acc[t] = 0.f;
     }
     float m = -INFINITY, l = 0.f;
-    const int64_t rp = (int64_t)lay * (a.nq + 1) + qb;
-    for (int e = a.row_ptr[rp]; e < a.row_ptr[rp + 1]; ++e) {
-        const int kb = a.col_idx[e];
-        const bool full = a.kind[e] == TILE_FULL;
+    int e0, e1;
+    row_entries(a, lay, qb, &e0, &e1);
+    for (int e = e0; e < e1; ++e) {
+        const int kb = a.walk == WALK_DENSE ? e : a.col_idx[e];
+        const bool full = a.walk != WALK_DENSE && a.kind[e] == TILE_FULL;
         for (int jj = 0; jj < a.block; ++jj) {
             const int j = kb * a.block + jj;
-            if (!full && !attended(a.pattern, part, a.l, a.c, wst, i, j)) continue;
+            if (!full && !attended(a.pattern, part, a.l, a.c, wst, i - a.qshift, j)) continue;
             const float* kr = k + base + (int64_t)j * a.ss;
             float s = 0.f;
             for (int t = 0; t < D; ++t) s = fmaf(qr[t], kr[t], s);
@@ -428,9 +443,23 @@ fwd_f32_kernel(AttnArgs a, const float* __restrict__ q, const float* __restrict_
             for (int t = 0; t < D; ++t) acc[t] = fmaf(p, vr[t], acc[t]);
         }
     }
+    float* orow = o + base + (int64_t)i * a.ss;
+    float* lrow = lse + stat_index(a, b, h, i);
+    if (a.epilogue == EPI_MERGE) {
+        // combine with the O and LSE of the disjoint part already there
+        const float lse1 = *lrow, lse2 = l > 0.f ? m + logf(l) : -INFINITY;
+        const float mx = fmaxf(lse1, lse2);
+        const float w1 = lse1 == -INFINITY ? 0.f : expf(lse1 - mx);
+        const float w2 = l > 0.f ? expf(m - mx) : 0.f;  // weight of acc
+        const float z = w1 + w2 * l;
+        const float inv = z > 0.f ? 1.f / z : 0.f;
+        for (int t = 0; t < D; ++t) orow[t] = (w1 * orow[t] + w2 * acc[t]) * inv;
+        *lrow = z > 0.f ? mx + logf(z) : -INFINITY;
+        return;
+    }
     float inv = l > 0.f ? 1.f / l : 0.f;
-    for (int t = 0; t < D; ++t) o[base + (int64_t)i * a.ss + t] = acc[t] * inv;
-    lse[stat_index(a, b, h, i)] = l > 0.f ? m + logf(l) : -INFINITY;
+    for (int t = 0; t < D; ++t) orow[t] = acc[t] * inv;
+    *lrow = l > 0.f ? m + logf(l) : -INFINITY;
 }
 
 template <int D, int BLK>

@@ -151,23 +151,10 @@ hipError_t decode_launch(int pattern, int mode, int32_t sub, int32_t pos, int32_
 
 size_t bwd_workspace_bytes(int64_t batch, int64_t heads, int64_t n, int64_t nq, int n_layouts);
 
-// Strided merged heads by transposition (sa_transposed.hip): the glue around
-// the two block-sparse calls.  Tensors are [rows = b h][n][d] contiguous.
-hipError_t causal_layout_launch(int32_t mq, int32_t* row_ptr, int32_t* col_idx, uint8_t* kind, int32_t* col_ptr,
-                                int32_t* row_idx, uint8_t* kind_t, hipStream_t stream);
-hipError_t shift_rows_launch(int dtype, const void* src, void* dst, int64_t rows, int64_t n, int d, int64_t shift,
-                             hipStream_t stream);
-hipError_t shift_lse_launch(const float* src, float* dst, int64_t rows, int64_t n, int32_t l, hipStream_t stream);
-hipError_t merge_launch(int dtype, const void* o1, const float* lse1, const void* o2, const float* lse2, void* o,
-                        float* lse, int64_t rows, int64_t n, int d, int32_t l, hipStream_t stream);
-hipError_t add_shifted_launch(int dtype, void* dst, const void* src, int64_t rows, int64_t n, int d, int64_t shift,
-                              hipStream_t stream);
-
 // Launches of a backward call: the row statistics (pre), dQ, and dK / dV.
 enum { BWD_PRE = 1, BWD_DQ = 2, BWD_DKDV = 4, BWD_ALL = 7 };
 
-// Backward; `parts` selects launches of the bf16 path (the fp32 path always
-// runs all of them).
+// Backward; `parts` selects its launches.
 hipError_t bwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k, const void* v,
                       const void* o, const void* dout, const float* lse, void* dq, void* dk,
                       void* dv, void* workspace, hipStream_t stream, int parts = BWD_ALL);

@@ -23,6 +23,7 @@ SA_STRIDED, SA_FIXED, SA_FIXED_PER_HEAD = 0, 1, 2
 SA_MODE_A1, SA_MODE_A2, SA_MODE_MERGED, SA_MODE_INTERLEAVED = 0, 1, 2, 3
 SA_F32, SA_BF16 = 0, 1
 SA_TILE_FULL, SA_TILE_MASKED = 0, 1
+SA_BWD_ROW_STATS, SA_BWD_DQ, SA_BWD_DKDV, SA_BWD_ALL_STAGES = 1, 2, 4, 7
 
 EXPORTED = (
     "sparse_attn_layout_count",
@@ -36,6 +37,7 @@ EXPORTED = (
     "sparse_attn_transposed_workspace_size",
     "sparse_attn_fwd_transposed",
     "sparse_attn_bwd_transposed",
+    "sparse_attn_bwd_stage",
     "sparse_attn_bwd_noalloc_max_workspace",
     "sparse_attn_bwd_noalloc",
     "sparse_attn_status_string",
@@ -74,6 +76,8 @@ def lib():
         L.sparse_attn_fwd_transposed.argtypes = _TR + [_vp] * 3 + [_i32] * 4 + [_vp] * 3 + [_f32] + [_vp] * 3 + [_sz, _vp]
         L.sparse_attn_bwd_transposed.argtypes = (_TR + [_vp] * 6 + [_i32] * 4 + [_vp] * 6 + [_f32] + [_vp] * 4
                                                  + [_sz, _vp])
+        L.sparse_attn_bwd_stage.argtypes = (_PAT + [_vp] * 6 + [_i32] * 4 + [_vp] * 7 + [_f32]
+                                            + [_vp] * 4 + [_sz, _i32, _vp])
         L.sparse_attn_bwd_noalloc_max_workspace.argtypes = [_vp]
         L.sparse_attn_bwd_noalloc.argtypes = (_PAT + [_vp] * 6 + [_i32] * 4 + [_vp] * 7 + [_f32] + [_vp] * 4)
         L.sparse_attn_status_string.argtypes = [ctypes.c_int]
@@ -207,6 +211,17 @@ def sparse_attn_bwd(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, 
     _check("sparse_attn_bwd", st)
 
 
+def sparse_attn_bwd_stage(n, block, stride_l, summary_c, pattern, head_mode, row_ptr, col_idx, kind,
+                          col_ptr, row_idx, kind_t, batch, heads, d_head, dtype, q, k, v, o, dout, lse,
+                          strides, softmax_scale, dq, dk, dv, workspace, workspace_bytes, stages, stream=None):
+    st = lib().sparse_attn_bwd_stage(n, block, stride_l, summary_c, pattern, head_mode, _ptr(row_ptr),
+                                     _ptr(col_idx), _ptr(kind), _ptr(col_ptr), _ptr(row_idx), _ptr(kind_t),
+                                     batch, heads, d_head, dtype, _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                     _ptr(dout), _ptr(lse), strides, softmax_scale, _ptr(dq), _ptr(dk),
+                                     _ptr(dv), _ptr(workspace), workspace_bytes, stages, _stream(stream, q.device))
+    _check("sparse_attn_bwd_stage", st)
+
+
 def sparse_attn_bwd_noalloc_max_workspace():
     out = ctypes.c_size_t(0)
     _check("sparse_attn_bwd_noalloc_max_workspace", lib().sparse_attn_bwd_noalloc_max_workspace(ctypes.byref(out)))
@@ -310,8 +325,9 @@ def forward(q, k, v, layout: Layout, softmax_scale=None, out=None, lse=None, str
 
 
 def backward(q, k, v, o, dout, lse, layout: Layout, softmax_scale=None, grads=None, workspace=None,
-             stream=None):
-    """dq, dk, dv of sparse attention given the forward's o and lse."""
+             stream=None, stages=None):
+    """dq, dk, dv of sparse attention given the forward's o and lse (``stages``:
+    a subset of the SA_BWD_* stages, through sparse_attn_bwd_stage)."""
     b, h, n, d = q.shape
     strides = _strides(q, k, v, o, dout)
     _check_layout(layout, q)
@@ -324,6 +340,11 @@ def backward(q, k, v, o, dout, lse, layout: Layout, softmax_scale=None, grads=No
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     elif workspace.device != q.device:
         raise ValueError("workspace must be on q's device")
+    if stages is not None:
+        sparse_attn_bwd_stage(*layout.pattern_args, *layout.row_args, *layout.col_args, b, h, d, dtype, q, k, v, o,
+                              dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
+                              workspace.numel() * workspace.element_size(), stages, stream)
+        return dq, dk, dv
     sparse_attn_bwd(*layout.pattern_args, *layout.row_args, *layout.col_args, b, h, d, dtype, q, k, v, o,
                     dout, lse, strides, _scale(softmax_scale, d), dq, dk, dv, workspace,
                     workspace.numel() * workspace.element_size(), stream)

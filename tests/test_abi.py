@@ -220,24 +220,17 @@ def test_decode_workspace_and_errors(L):
 
 
 def test_transposed_workspace_and_errors(L):
-    """Workspace of the merged transposed path: a dense causal class layout, six
-    tensors of the input's size (shifted Q, O, dO; partial gradients), two
-    fp32 row statistics, and the larger of the two backward workspaces, each
-    region 256-byte aligned."""
-    def a256(x):
-        return (x + 255) // 256 * 256
-
+    """Workspace of the merged transposed path: the band backward's (row
+    statistics and dK / dV schedule, as sparse_attn_bwd); the class kernels
+    read the same row statistics in place."""
     def bwd_ws(rows, nq):
         return (8 * rows + 15) // 16 * 16 + 8 * 8 + 4 + 2 * 4 * nq
 
     out = ctypes.c_size_t(0)
     n, B, l, CB, b, h, d = 12288, 64, 128, 32, 2, 8, 64
     assert L.sparse_attn_transposed_workspace_size(n, B, l, CB, b, h, d, sa.SA_BF16, ctypes.byref(out)) == 0
-    rows, mq = b * h * n, (n // l) // CB
-    nnz_c = mq * (mq + 1) // 2
-    expect = (a256(2 * (mq + 1) * 4 + 2 * nnz_c * 5 + 64) + 6 * a256(rows * d * 2) + 2 * a256(rows * 4)
-              + a256(max(bwd_ws(rows, n // B), bwd_ws(rows, mq))))
-    assert out.value == expect
+    rows = b * h * n
+    assert out.value == bwd_ws(rows, n // B)
     bad = [
         ((12288, 64, 100, 32, 2, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # l does not divide n
         ((12288, 64, 128, 24, 2, 8, 64, sa.SA_BF16), sa.SA_ERR_INVALID),      # class block not supported
@@ -294,3 +287,20 @@ def test_noalloc_rejects_workspace_beyond_scratch(L):
     st = L.sparse_attn_bwd_noalloc(n, 64, 1024, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, *([fake] * 6), 1, heads, d,
                                    sa.SA_BF16, *([fake] * 6), strides, ctypes.c_float(0.125), *([fake] * 3), None)
     assert st == sa.SA_ERR_BUFFER_TOO_SMALL
+
+
+def test_bwd_stage_validation(L):
+    """Stage sets: empty or unknown sets are invalid; fp32 runs only whole."""
+    n, B, l, b, h, d = 256, 32, 32, 1, 2, 64
+    need = sa.sparse_attn_bwd_workspace_size(n, B, l, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, b, h, d, sa.SA_BF16)
+    fake = ctypes.c_void_p(1 << 20)
+    strides = (ctypes.c_int64 * 3)(h * n * d, n * d, d)
+
+    def call(stages, dtype=sa.SA_BF16):
+        return L.sparse_attn_bwd_stage(n, B, l, 0, sa.SA_STRIDED, sa.SA_MODE_MERGED, *([fake] * 6), b, h, d, dtype,
+                                       *([fake] * 6), strides, ctypes.c_float(0.125), *([fake] * 3), fake, need,
+                                       stages, None)
+    assert call(0) == sa.SA_ERR_INVALID
+    assert call(8) == sa.SA_ERR_INVALID
+    assert call(-1) == sa.SA_ERR_INVALID
+    assert call(sa.SA_BWD_DQ, sa.SA_F32) == sa.SA_ERR_UNSUPPORTED
