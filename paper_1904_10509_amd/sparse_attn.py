@@ -16,7 +16,10 @@ from dataclasses import dataclass
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_attn.so")
+# SPARSE_ATTN_LIB names another build of the same sources to load instead (the
+# sanitizer test loads one whose host code is built with ASan and UBSan).
+LIB_PATH = os.environ.get("SPARSE_ATTN_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                              "libsparse_attn.so")
 
 SA_OK, SA_ERR_INVALID, SA_ERR_UNSUPPORTED, SA_ERR_BUFFER_TOO_SMALL, SA_ERR_HIP = 0, -1, -2, -3, -4
 SA_STRIDED, SA_FIXED, SA_FIXED_PER_HEAD = 0, 1, 2
