@@ -571,7 +571,11 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
 // each 16-key wave a single live 32-query chunk.
 template <int D, int BLK, int PAT>
 struct DkvCfg {
-    static constexpr int KW = 16;               // keys per wave
+    // keys per wave.  (32 keys per wave, two key groups sharing every Q / dO
+    // operand read, needs about 290 registers: at one wave per SIMD it made the
+    // fixed backward at n = 65,536 slower, 1.68 against 1.45 ms, and at two
+    // with spills 2.10 ms; the half and pair logic below handles both widths.)
+    static constexpr int KW = 16;
     static constexpr int KBW = KW / 16;         // 16-key blocks per wave
     static constexpr int NW = BLK / KW;         // waves
     static constexpr int NT = NW * 64;
@@ -580,7 +584,7 @@ struct DkvCfg {
     static constexpr int QC = (BLK + 31) / 32;  // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
-    static constexpr int WAVES_PER_EU = 3;
+    static constexpr int WAVES_PER_EU = KW == 32 ? 2 : 3;
 };
 
 // SPLIT: P and dS enter the dV and dK products as a high and a low bf16 part
@@ -598,7 +602,9 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                      const int32_t* __restrict__ order) {
     using C = DkvCfg<D, BLK, PAT>;
     constexpr bool kHalves = PAT == FIXED && BLK == 64;  // items may be 32-key halves
-    static_assert(!kHalves || (C::NW == 4 && C::KBW == 1 && C::QC == 2), "half items: 4 waves of 16 keys");
+    static_assert(!kHalves || (C::QC == 2 && ((C::NW == 4 && C::KBW == 1) || (C::NW == 2 && C::KBW == 2))),
+                  "half items: 4 waves of 16 keys or 2 of 32");
+    constexpr int kHalfWaves = C::NW >= 2 ? C::NW / 2 : 1;  // waves per 32-key half in a pair
     __shared__ __attribute__((aligned(16))) uint16_t sQ[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sdO[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) float sL[C::NS][64];
@@ -704,22 +710,28 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         }
         const int kb = code & ((1 << kItemShift) - 1);
         const int kind = kHalves ? code >> kItemShift : 0;
-        // In a pair waves 0, 1 take the summary half of kb, waves 2, 3 that of
-        // kb + l / 64, each for all queries of a block; a single half is shared
-        // by all four waves (two key groups times two query halves).
+        // In a pair the first half of the waves takes the summary half of kb,
+        // the second half that of kb + l / 64, each for all queries of a block;
+        // a single half is shared by all waves: with four waves of 16 keys, two
+        // key groups times two query halves; with two waves of 32 keys, both
+        // key groups times one query half each.
         const bool pair = kind >= 3;
         const int half = pair ? kind - 2 : kind;  // 32-key half walked; 0: the whole block
         const bool single = half != 0 && !pair;
-        const int kb_w = pair && w >= 2 ? kb + a.l / 64 : kb;  // this wave's key block
+        const int kb_w = pair && w >= kHalfWaves ? kb + a.l / 64 : kb;  // this wave's key block
+        const int qhalf = w / kHalfWaves;  // single half: the 32-query half of each block this wave takes
         const MaskParams mp = head_mask_params(a, PAT, MODE, h);
         const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
         // This wave's keys are the 16-key groups w, w + NW, ...: interleaved, so
         // that the waves share the summary columns of the fixed pattern (which
         // sit at the end of a block) and with them the softmax work.  In a
-        // single half the wave takes key group w mod 2 of the half, for the
-        // queries of one 32-query half (w / 2) of every block; in a pair, key
-        // group w mod 2 of its block's half, for every query.
-        auto kgrp = [&](int kbw) { return half == 0 ? C::NW * kbw + w : 2 * (half - 1) + (w & 1); };
+        // single half the wave takes key group w mod 2 of the half (both with
+        // 32 keys per wave), for the queries of one 32-query half (qhalf) of
+        // every block; in a pair, the same groups of its block's half, for
+        // every query.
+        auto kgrp = [&](int kbw) {
+            return half == 0 ? C::NW * kbw + w : 2 * (half - 1) + (C::KBW == 2 ? kbw : (w & 1));
+        };
         auto key_of = [&](int kbw) { return kb_w * BLK + 16 * kgrp(kbw) + r; };
 
         // this lane's keys j = key_of(kbw) as B operands (d = 32 ks + 8g + t)
@@ -889,8 +901,10 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 if (decltype(one_half)::value || (!decltype(full)::value && single)) {
                     // a single half: this wave takes one 32-query half of the block
 #pragma unroll
-                    for (int qc = 0; qc < C::QC; ++qc)
-                        if (qc != (w >> 1)) cls[0][qc] = CHUNK_NONE;
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
+#pragma unroll
+                        for (int qc = 0; qc < C::QC; ++qc)
+                            if (qc != qhalf) cls[kbw][qc] = CHUNK_NONE;
                 }
                 // A 32-query chunk enters the products only where some key of the
                 // wave is attended by one of its queries; elsewhere P and dS are zero
@@ -899,7 +913,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 constexpr int HQ = C::QB >= 2 ? 2 : 1;  // 16-query blocks per 32-query chunk
                 // unmasked steps: ask the scheduler to interleave the exponentials
                 // with the matrix products (its strategy for attention-like loops)
-                if constexpr (decltype(full)::value && !decltype(one_half)::value) __builtin_amdgcn_iglp_opt(2);
+                if constexpr (decltype(full)::value && !decltype(one_half)::value && C::KW == 16)
+                    __builtin_amdgcn_iglp_opt(2);
                 bool qc_live[C::QC];
 #pragma unroll
                 for (int qc = 0; qc < C::QC; ++qc) {
@@ -974,36 +989,42 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                         if (cls[kbw][qc] == CHUNK_ALL) chunk(std::false_type{});
                         else if (cls[kbw][qc] == CHUNK_PART) chunk(std::true_type{});
                     }
-                    bf16x8 oT[C::DB], qT[C::DB];
+                    // (SPLIT: every transposed operand is kept for the low parts,
+                    // issued after every high part so that no product waits on the
+                    // one just issued; otherwise each is read just before its use)
+                    constexpr int kKeep = SPLIT ? C::DB : 1;
+                    bf16x8 oT[kKeep], qT[kKeep];
 #pragma unroll
                     for (int db = 0; db < C::DB; ++db) {
+                        const int x = SPLIT ? db : 0;
                         if constexpr (BLK >= 32) {
-                            oT[db] = rd.tr(tO, qc * 32, qc * 32 + 16, db);
-                            qT[db] = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
+                            oT[x] = rd.tr(tO, qc * 32, qc * 32 + 16, db);
+                            qT[x] = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
                         } else {
-                            oT[db] = rd.tr_half(tO, 0, db);
-                            qT[db] = rd.tr_half(tQ, 0, db);
+                            oT[x] = rd.tr_half(tO, 0, db);
+                            qT[x] = rd.tr_half(tQ, 0, db);
                         }
 #pragma unroll
                         for (int kbw = 0; kbw < C::KBW; ++kbw) {
                             if (cls[kbw][qc] == CHUNK_NONE) continue;
-                            dvacc[kbw][db] = mfma_16x16x32(oT[db], pb[kbw], dvacc[kbw][db]);
-                            dkacc[kbw][db] = mfma_16x16x32(qT[db], sb[kbw], dkacc[kbw][db]);
+                            dvacc[kbw][db] = mfma_16x16x32(oT[x], pb[kbw], dvacc[kbw][db]);
+                            dkacc[kbw][db] = mfma_16x16x32(qT[x], sb[kbw], dkacc[kbw][db]);
                         }
                     }
                     if constexpr (SPLIT) {
-                        // the low parts, after every high part (no product waits on
-                        // the one just issued)
 #pragma unroll
                         for (int db = 0; db < C::DB; ++db) {
 #pragma unroll
                             for (int kbw = 0; kbw < C::KBW; ++kbw) {
                                 if (cls[kbw][qc] == CHUNK_NONE) continue;
-                                dvacc[kbw][db] = mfma_16x16x32(oT[db], pbl[kbw], dvacc[kbw][db]);
-                                dkacc[kbw][db] = mfma_16x16x32(qT[db], sbl[kbw], dkacc[kbw][db]);
+                                dvacc[kbw][db] = mfma_16x16x32(oT[db % kKeep], pbl[kbw], dvacc[kbw][db]);
+                                dkacc[kbw][db] = mfma_16x16x32(qT[db % kKeep], sbl[kbw], dkacc[kbw][db]);
                             }
                         }
                     }
+                    // with 32 keys per wave, chunks are kept apart: scheduled
+                    // together their live values outgrow two waves' registers
+                    if constexpr (C::KW == 32) __builtin_amdgcn_sched_barrier(0);
                 }
             };
             // unmasked steps of whole blocks and pairs run without a runtime
@@ -1022,31 +1043,36 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             if (single) {
                 // the two query halves of each key group are summed through LDS
                 // (the ring is idle once every wave has passed the last step)
-                static_assert(sizeof(sQ) >= 2 * 2 * C::DB * 64 * sizeof(f32x4), "reduction fits the Q ring");
+                static_assert(sizeof(sQ) >= (size_t)kHalfWaves * C::KBW * 2 * C::DB * 64 * sizeof(f32x4),
+                              "reduction fits the Q ring");
                 __syncthreads();
                 f32x4* red = reinterpret_cast<f32x4*>(&sQ[0][0]);
-                const int slot = (w & 1) * 2 * C::DB;
-                if (w >= 2) {
+                const int slot0 = (w % kHalfWaves) * C::KBW * 2 * C::DB;
+                if (qhalf == 1) {
 #pragma unroll
-                    for (int db = 0; db < C::DB; ++db) {
-                        red[(slot + db) * 64 + lane] = dvacc[0][db];
-                        red[(slot + C::DB + db) * 64 + lane] = dkacc[0][db];
-                    }
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
+#pragma unroll
+                        for (int db = 0; db < C::DB; ++db) {
+                            red[(slot0 + kbw * 2 * C::DB + db) * 64 + lane] = dvacc[kbw][db];
+                            red[(slot0 + kbw * 2 * C::DB + C::DB + db) * 64 + lane] = dkacc[kbw][db];
+                        }
                 }
                 __syncthreads();
-                if (w < 2) {
+                if (qhalf == 0) {
 #pragma unroll
-                    for (int db = 0; db < C::DB; ++db) {
-                        dvacc[0][db] += red[(slot + db) * 64 + lane];
-                        dkacc[0][db] += red[(slot + C::DB + db) * 64 + lane];
-                    }
+                    for (int kbw = 0; kbw < C::KBW; ++kbw)
+#pragma unroll
+                        for (int db = 0; db < C::DB; ++db) {
+                            dvacc[kbw][db] += red[(slot0 + kbw * 2 * C::DB + db) * 64 + lane];
+                            dkacc[kbw][db] += red[(slot0 + kbw * 2 * C::DB + C::DB + db) * 64 + lane];
+                        }
                 }
             }
         }
         // this lane holds dV^T / dK^T at d = 16 db + 4g + t for key key_of(kbw)
 #pragma unroll
         for (int kbw = 0; kbw < C::KBW; ++kbw) {
-            if (single && w >= 2) break;  // written by the wave of the other query half
+            if (single && qhalf == 1) break;  // written by the wave of the other query half
             const int j = key_of(kbw);
             uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
             uint16_t* dkrow = dk + base + (int64_t)j * a.ss;

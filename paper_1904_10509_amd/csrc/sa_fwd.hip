@@ -28,9 +28,12 @@ namespace {
 // Waves of 16 query rows: with four waves per 64-wide block the workgroup holds
 // more waves per SIMD (fewer registers each), and in the strided pattern a
 // block that holds one diagonal leaves each 16-row wave a single live chunk.
-template <int D, int BLK>
+template <int D, int BLK, int PAT>
 struct FwdCfg {
-    static constexpr int RW = 16;                   // query rows per wave
+    // query rows per wave.  (32 rows per wave in the fixed pattern, each K / V
+    // operand read feeding two row blocks at two waves per SIMD, made the
+    // forward at n = 65,536 slower: 0.83 against 0.77 ms.)
+    static constexpr int RW = 16;
     static constexpr int QBW = RW / 16;             // 16-row blocks per wave
     static constexpr int NW = BLK / RW;             // waves per workgroup
     static constexpr int NT = NW * 64;              // threads
@@ -39,17 +42,18 @@ struct FwdCfg {
     static constexpr int KC = (BLK + 31) / 32;      // 32-key chunks for P V
     static constexpr int DB = D / 16;               // 16-wide d blocks of O
     static constexpr int NS = 2;                    // K / V ring stages
+    static constexpr int WAVES_PER_EU = RW == 32 ? 2 : 3;
 };
 
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
 // over the XCDs) share a query block index across heads, so with heads a
 // multiple of 8 each head stays on one XCD and its keys stay in that L2.
 template <int D, int BLK, int PAT, int MODE, bool FULL_BODY>
-__global__ void __launch_bounds__((FwdCfg<D, BLK>::NT)) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ void __launch_bounds__((FwdCfg<D, BLK, PAT>::NT)) __attribute__((amdgpu_waves_per_eu(FwdCfg<D, BLK, PAT>::WAVES_PER_EU)))
 fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                 const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                 const uint16_t* __restrict__ v, uint16_t* __restrict__ o, float* __restrict__ lse) {
-    using C = FwdCfg<D, BLK>;
+    using C = FwdCfg<D, BLK, PAT>;
     // K and V tiles in a two-stage ring: the next key block is in flight
     // while one is computed; one barrier per key block
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
@@ -470,7 +474,7 @@ hipError_t launch_bf16(const AttnArgs& a, const void* q, const void* k, const vo
         constexpr int PAT = decltype(pat)::value, MODE = decltype(mode)::value;
         return with_full_body<PAT>(a, [&](auto fb) {
             hipLaunchKernelGGL((fwd_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value>), grid,
-                               dim3(FwdCfg<D, BLK>::NT), 0, stream, a, a.row_ptr, a.col_idx, (const uint16_t*)q,
+                               dim3(FwdCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx, (const uint16_t*)q,
                                (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse);
             return hipGetLastError();
         });

@@ -128,16 +128,19 @@ hipError_t fwd_launch(const AttnArgs& a, int dtype, const void* q, const void* k
 // Backward workspace: D and the base-2 LSE per row [b, h, n] (fp32), then
 // the work queues and the column order of the dK / dV kernel.
 // Whether the row-view kernels (forward, dQ) carry a second step body for
-// fully attended blocks: always in the fixed pattern; in the strided pattern
-// when those blocks (l / B - 1 per row) outnumber the diagonal-only blocks of
-// a middle row (about n / 2l), i.e. 2 l^2 > n B, as in the dense limit l >= n.
+// fully attended blocks: always in the fixed pattern and for walks of the band
+// or of every block (l / B - 1 of a band row's l / B + 1 blocks are full, and
+// all but the diagonal of a dense row); over a strided layout when those
+// blocks (l / B - 1 per row) outnumber the diagonal-only blocks of a middle
+// row (about n / 2l), i.e. 2 l^2 > n B, as in the dense limit l >= n.
 // Otherwise the second copy of the code costs more than it saves.
 template <int PAT, typename F>
 inline hipError_t with_full_body(const AttnArgs& a, F&& f) {
     if constexpr (PAT == FIXED) {
         return f(std::true_type{});
     } else {
-        if (2.0 * (double)a.l * (double)a.l > (double)a.n * (double)a.block) return f(std::true_type{});
+        if (a.walk != WALK_LAYOUT || 2.0 * (double)a.l * (double)a.l > (double)a.n * (double)a.block)
+            return f(std::true_type{});
         return f(std::false_type{});
     }
 }
