@@ -257,7 +257,9 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
     constexpr uint32_t kTileBytes = BLK * D * 2;
     const uint32_t sK_base = lds_addr(&sK[0][0]), sV_base = lds_addr(&sV[0][0]);
 
-    const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;
+    const GridItem gi = row_grid_item(a);  // longest rows first
+    const int h = __builtin_amdgcn_readfirstlane(gi.h), qb = __builtin_amdgcn_readfirstlane(gi.qb),
+              b = __builtin_amdgcn_readfirstlane(gi.b);
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = head_layout(a, h);
@@ -649,7 +651,15 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     //   CLAIM_SERPENTINE: workgroup w serves head w mod (batch heads) alone and
     //     takes that head's ranks in serpentine order over the J workgroups of
     //     the head (j, 2J - 1 - j, 2J + j, ...), which evens out the sums of
-    //     sorted column lengths, with no atomics.
+    //     sorted column lengths, with no atomics;
+    //   CLAIM_XCD_SERPENTINE: workgroup w (on XCD x = w mod 8, the j-th of
+    //     its J there) serves the heads bh = x (mod 8), head by head with
+    //     every column of a head, longest first, before the next: places
+    //     kJ + j for even k, kJ + J - 1 - j for odd k of that sequence.  The
+    //     J workgroups of an XCD thus walk the columns of J / nq heads at a
+    //     time, whose Q and dO stay in that XCD's L2 (the residue classes:
+    //     many short dense heads read at a stride of l rows).  Needs the grid
+    //     and batch x heads multiples of 8 (the launcher checks).
     // The atomics of all workgroups on one counter are serialised
     // device-wide; with many short columns a claim waits longer than a column
     // takes, hence the fixed orders.  Every mode yields queue-encoded slots.
@@ -665,6 +675,15 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             next_slot += gridDim.x;
             const uint64_t rank = s / (uint64_t)bh_count;
             return encode(rank, (int)(s - rank * (uint64_t)bh_count));
+        }
+        if (a.claim_mode == CLAIM_XCD_SERPENTINE) {
+            const uint64_t J = gridDim.x / kQueues, j = blockIdx.x / kQueues;
+            const int x = (int)(blockIdx.x % kQueues);
+            const uint64_t k = sweep++;
+            const uint64_t p = k * J + ((k & 1) ? J - 1 - j : j);
+            const uint64_t i = p / per_layout;  // the i-th head of this XCD
+            if (i >= (uint64_t)(bh_count / kQueues)) return kNoWork;
+            return encode(p - i * per_layout, x + kQueues * (int)i);
         }
         if (a.claim_mode == CLAIM_SERPENTINE) {
             const int bh = (int)(blockIdx.x % (uint64_t)bh_count);
@@ -1186,14 +1205,18 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
                   : resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE, false>>(DkvCfg<D, BLK, PAT>::NT);
         const unsigned qgrid =
             (unsigned)(slots > 0 && slots < items ? slots : (items < (1ll << 31) ? items : (1ll << 31) - 1));
-        // order of the dK / dV work (see the kernel): a fixed order where column
-        // lengths change smoothly (strided: a band and a stride's worth of rows
-        // per column) or columns are a few blocks long; serpentine per head
-        // where long summary columns alternate with short ones (fixed) and each
-        // head has a few workgroups; the queues otherwise
+        // order of the dK / dV work (see the kernel): head by head on each XCD
+        // for a walk of every block (the residue classes); a fixed order where
+        // column lengths change smoothly (strided: a band and a stride's worth
+        // of rows per column) or columns are a few blocks long; serpentine per
+        // head where long summary columns alternate with short ones (fixed) and
+        // each head has a few workgroups; the queues otherwise
         const int64_t bh_count = (int64_t)a.batch * a.heads;
-        ak.claim_mode = (PAT == STRIDED || a.nq <= 8) ? CLAIM_ROUND_ROBIN
-                        : (bh_count * 4 <= (int64_t)qgrid ? CLAIM_SERPENTINE : CLAIM_QUEUES);
+        ak.claim_mode = a.walk == WALK_DENSE && qgrid % kQueues == 0 && bh_count % kQueues == 0
+                            ? CLAIM_XCD_SERPENTINE
+                        : (PAT == STRIDED || a.nq <= 8)
+                            ? CLAIM_ROUND_ROBIN
+                            : (bh_count * 4 <= (int64_t)qgrid ? CLAIM_SERPENTINE : CLAIM_QUEUES);
         // Summary halves in pairs (fixed, B = 64, l a multiple of 64: n / l of
         // them per (batch, head)) only where each workgroup of a head gets at
         // least 2.5 of them on average: a pair's column takes one workgroup

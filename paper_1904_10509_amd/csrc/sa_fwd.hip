@@ -47,7 +47,8 @@ struct FwdCfg {
 
 // grid: (heads, nq, batch).  Consecutive workgroups (dispatched round-robin
 // over the XCDs) share a query block index across heads, so with heads a
-// multiple of 8 each head stays on one XCD and its keys stay in that L2.
+// multiple of 8 each head stays on one XCD and its keys stay in that L2; a
+// dense walk takes a head's query blocks together instead (row_grid_item).
 template <int D, int BLK, int PAT, int MODE, bool FULL_BODY>
 __global__ void __launch_bounds__((FwdCfg<D, BLK, PAT>::NT)) __attribute__((amdgpu_waves_per_eu(FwdCfg<D, BLK, PAT>::WAVES_PER_EU)))
 fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
@@ -62,7 +63,9 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
     constexpr uint64_t kTileBits = BLK == 64 ? ~0ull : (1ull << BLK) - 1;
     const uint32_t sK_base = lds_addr(&sK[0][0]), sV_base = lds_addr(&sV[0][0]);
 
-    const int h = blockIdx.x, qb = a.nq - 1 - (int)blockIdx.y, b = blockIdx.z;  // longest rows first
+    const GridItem gi = row_grid_item(a);  // longest rows first
+    const int h = __builtin_amdgcn_readfirstlane(gi.h), qb = __builtin_amdgcn_readfirstlane(gi.qb),
+              b = __builtin_amdgcn_readfirstlane(gi.b);
     const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int lay = head_layout(a, h);

@@ -50,7 +50,7 @@ inline hipError_t with_pattern_mode(int pattern, int mode, F&& f) {
 }
 
 // Orders in which the dK / dV kernel takes its work.
-enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2 };
+enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2, CLAIM_XCD_SERPENTINE = 3 };
 
 // Which blocks a kernel walks:
 //   WALK_LAYOUT  the present blocks of the layout;
@@ -95,6 +95,28 @@ struct AttnArgs {
     const int32_t* row_idx;
     const uint8_t* kind_t;
 };
+
+// The (head, query block, batch) of a row-view workgroup, on the grid
+// (heads, nq, batch).  The dispatcher hands consecutive workgroups to the 8
+// XCDs in turn, so workgroup L (x fastest) runs on XCD L mod 8.  A walk of
+// every block (the residue classes, each a short dense problem read at a
+// stride of l rows) gives the nq workgroups of one (batch, head) consecutive
+// places s = L / 8 on one XCD: its keys then stay in that XCD's L2 while all
+// its query blocks walk them, instead of leaving it between the query-block
+// generations of the plain order.  Needs batch x heads a multiple of 8;
+// otherwise, and for other walks, the plain order.  Longest rows first.
+struct GridItem {
+    int h, qb, b;
+};
+__device__ inline GridItem row_grid_item(const AttnArgs& a) {
+    if (a.walk == WALK_DENSE && ((int64_t)a.batch * a.heads) % 8 == 0) {
+        const uint64_t L = blockIdx.x + (uint64_t)gridDim.x * (blockIdx.y + (uint64_t)gridDim.y * blockIdx.z);
+        const uint64_t s = L / 8;
+        const uint64_t u = (s / (uint64_t)a.nq) * 8 + L % 8;  // (batch, head) unit
+        return {(int)(u % (uint64_t)a.heads), a.nq - 1 - (int)(s % (uint64_t)a.nq), (int)(u / (uint64_t)a.heads)};
+    }
+    return {(int)blockIdx.x, a.nq - 1 - (int)blockIdx.y, (int)blockIdx.z};
+}
 
 // Index of row i of (batch b, head h) in LSE and the backward's row statistics.
 __host__ __device__ inline int64_t stat_index(const AttnArgs& a, int b, int h, int64_t i) {
