@@ -187,32 +187,44 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     if (tid == 0) items_out[g] = items;
 }
 
+// Rows of the row-statistics kernel per 256-thread workgroup: one thread per
+// row in fp32; in bf16, D / 8 lanes per row, each reading 16 bytes, so that a
+// wave's load covers whole rows (64 / (D / 8) of them) contiguously.
+template <int D, typename T>
+constexpr int pre_rows_per_group() {
+    return sizeof(T) == 2 ? 256 / (D / 8) : 256;
+}
+
 template <int D, typename T>
 __global__ void __launch_bounds__(256)
 bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, const float* __restrict__ lse,
                float* __restrict__ ndelta, float* __restrict__ nlse2, unsigned long long* __restrict__ queue,
                int32_t* __restrict__ items, int32_t* __restrict__ order) {
     if (queue && (int)blockIdx.x < layout_count(a.mode, a.sub)) build_schedule(a, blockIdx.x, queue, items, order);
-    const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    constexpr int kLanes = sizeof(T) == 2 ? D / 8 : 1;  // lanes per row
+    const int64_t row = (int64_t)blockIdx.x * pre_rows_per_group<D, T>() + threadIdx.x / kLanes;
+    const int part = threadIdx.x % kLanes;  // 8-element part of the row (bf16)
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
+    // (kLanes divides 64, so the lanes of a row share their wave and its
+    // exit: every lane of a row reaches the reduction below)
     if (row >= rows) return;
     const int64_t bh = row / a.n, i = row % a.n;
     const int64_t off = (bh / a.heads) * a.sb + (bh % a.heads) * a.sh + i * a.ss;
     float acc = 0.f;
     if constexpr (sizeof(T) == 2) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(o + off + 8 * part);
+        const u32x4 y = *reinterpret_cast<const u32x4*>(dout + off + 8 * part);
 #pragma unroll
-        for (int t = 0; t < D; t += 8) {
-            const u32x4 x = *reinterpret_cast<const u32x4*>(o + off + t);
-            const u32x4 y = *reinterpret_cast<const u32x4*>(dout + off + t);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                acc = fmaf(__uint_as_float(x[e] << 16), __uint_as_float(y[e] << 16), acc);
-                acc = fmaf(__uint_as_float(x[e] & 0xffff0000u), __uint_as_float(y[e] & 0xffff0000u), acc);
-            }
+        for (int e = 0; e < 4; ++e) {
+            acc = fmaf(__uint_as_float(x[e] << 16), __uint_as_float(y[e] << 16), acc);
+            acc = fmaf(__uint_as_float(x[e] & 0xffff0000u), __uint_as_float(y[e] & 0xffff0000u), acc);
         }
+#pragma unroll
+        for (int m = 1; m < kLanes; m *= 2) acc += __shfl_xor(acc, m);
     } else {
         for (int t = 0; t < D; ++t) acc = fmaf(o[off + t], dout[off + t], acc);
     }
+    if (part != 0) return;
     ndelta[row] = -acc;
     nlse2[row] = -lse[row] * kLog2e;  // an empty row (LSE = -inf) gives +inf; its items are all masked
 }
@@ -1192,8 +1204,10 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
     float* ndelta = ws.ndelta;
     float* nlse2 = ws.nlse2;
-    const int64_t pre_groups = (rows + 255) / 256 > layout_count(a.mode, a.sub) ? (rows + 255) / 256
-                                                                                 : layout_count(a.mode, a.sub);
+    constexpr int kPreRows = pre_rows_per_group<D, uint16_t>();
+    const int64_t pre_groups = (rows + kPreRows - 1) / kPreRows > layout_count(a.mode, a.sub)
+                                   ? (rows + kPreRows - 1) / kPreRows
+                                   : layout_count(a.mode, a.sub);
     dim3 grid((unsigned)a.heads, (unsigned)a.nq, (unsigned)a.batch);
     const int64_t items = (int64_t)a.nq * a.batch * a.heads;
     AttnArgs ak = a;
