@@ -298,7 +298,7 @@ def decode_bench(args):
 
 
 def probe_lib():
-    """The measurement probe library (libsa_probe.so: the matrix-core peak and clock)."""
+    """The measurement probe library (libsa_probe.so: the matrix-core peak and clock, the LDS read rate)."""
     import ctypes
     path = os.path.join(ROOT, "paper_1904_10509_amd", "libsa_probe.so")
     if not os.path.exists(path):
@@ -308,7 +308,48 @@ def probe_lib():
     L.sa_probe_mfma_flop.argtypes = [ctypes.c_int, ctypes.c_int]
     L.sa_probe_mfma_launch.restype = ctypes.c_int
     L.sa_probe_mfma_launch.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    L.sa_probe_lds_bytes.restype = ctypes.c_double
+    L.sa_probe_lds_bytes.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    L.sa_probe_lds_launch.restype = ctypes.c_int
+    L.sa_probe_lds_launch.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
     return L
+
+
+def lds_read_rate(torch, dev, iters=4000, reps=5):
+    """LDS read rate per compute unit for ds_read_b128 and ds_read_b64_tr_b16
+    (2 workgroups of 4 waves per CU, 64 KiB of LDS each, 8 independent reads
+    per lane and iteration), with the shader clock during each."""
+    L = probe_lib()
+    props = torch.cuda.get_device_properties(dev)
+    cus = props.multi_processor_count
+    groups = cus * 8
+    sink = torch.empty(groups * 256, dtype=torch.int32, device=dev)
+    clocks = torch.zeros(2, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+    for kind, label in ((0, "ds_read_b128"), (1, "ds_read_b64_tr_b16")):
+        nbytes = L.sa_probe_lds_bytes(kind, groups, iters)
+        best_ms = None
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if L.sa_probe_lds_launch(kind, groups, iters, sink.data_ptr(), clocks.data_ptr(), stream.cuda_stream) != 0:
+                raise RuntimeError("probe launch failed")
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                ms = e0.elapsed_time(e1)
+                best_ms = ms if best_ms is None else min(best_ms, ms)
+        cyc, ticks = (int(x) for x in clocks.cpu())
+        ghz = cyc / (ticks / 100e6) / 1e9 if ticks > 0 else None
+        rate = nbytes / (best_ms * 1e-3)
+        out[label] = {"tb_per_s": rate / 1e12, "clock_ghz": ghz,
+                      "bytes_per_clk_per_cu": rate / cus / (ghz * 1e9) if ghz else None}
+    out["method"] = ("8 workgroups of 256 threads per CU launched (2 resident: 64 KiB of LDS each); every lane "
+                     "issues 8 independent reads per iteration at consecutive 16-byte slots; best of 5 launches by "
+                     "HIP events; clock from s_memtime over s_memrealtime across one wave's loop")
+    return out
 
 
 def mfma_peak(torch, dev, iters=4096, reps=5):
@@ -358,14 +399,16 @@ def main():
                     help="instead of the metric's line, time decoding steps (sparse_attn_decode) at the two "
                          "long-sequence shapes")
     ap.add_argument("--mfma-peak", action="store_true",
-                    help="instead of the metric's line, measure the achievable bf16 matrix-core rate and clock")
+                    help="instead of the metric's line, measure the achievable bf16 matrix-core rate and clock, "
+                         "and the LDS read rate per compute unit")
     args = ap.parse_args()
     if args.mfma_peak:
         import torch
         dev = torch.device("cuda:0")
         torch.cuda.set_device(dev)
         print(json.dumps({"metric": "achievable bf16 MFMA rate (v_mfma_f32_16x16x32_bf16)",
-                          "peak_datasheet_tflops": PEAK_BF16_TFLOPS, **mfma_peak(torch, dev)}), flush=True)
+                          "peak_datasheet_tflops": PEAK_BF16_TFLOPS, **mfma_peak(torch, dev),
+                          "lds_read": lds_read_rate(torch, dev)}), flush=True)
         return
     if args.decode:
         decode_bench(args)
