@@ -318,8 +318,8 @@ def probe_lib():
 
 def lds_read_rate(torch, dev, iters=4000, reps=5):
     """LDS read rate per compute unit for ds_read_b128 and ds_read_b64_tr_b16
-    (2 workgroups of 4 waves per CU, 64 KiB of LDS each, 8 independent reads
-    per lane and iteration), with the shader clock during each."""
+    (8 resident workgroups of 4 waves per CU, 16 KiB of LDS each, 8 independent
+    reads per lane and iteration), with the shader clock during each."""
     L = probe_lib()
     props = torch.cuda.get_device_properties(dev)
     cus = props.multi_processor_count
@@ -346,7 +346,7 @@ def lds_read_rate(torch, dev, iters=4000, reps=5):
         rate = nbytes / (best_ms * 1e-3)
         out[label] = {"tb_per_s": rate / 1e12, "clock_ghz": ghz,
                       "bytes_per_clk_per_cu": rate / cus / (ghz * 1e9) if ghz else None}
-    out["method"] = ("8 workgroups of 256 threads per CU launched (2 resident: 64 KiB of LDS each); every lane "
+    out["method"] = ("8 workgroups of 256 threads per CU, all resident (16 KiB of LDS each); every lane "
                      "issues 8 independent reads per iteration at consecutive 16-byte slots; best of 5 launches by "
                      "HIP events; clock from s_memtime over s_memrealtime across one wave's loop")
     return out

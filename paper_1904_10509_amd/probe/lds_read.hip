@@ -2,8 +2,10 @@
 // the LDS read rate per compute unit for the two read forms the attention
 // kernels use: ds_read_b128 (16 bytes a lane, the row operands) and
 // ds_read_b64_tr_b16 (8 bytes a lane, transposed, the operands whose
-// contraction runs over a tile's rows).  Each 256-thread workgroup fills 64 KiB
-// of LDS, then every lane issues 8 independent reads per iteration at
+// contraction runs over a tile's rows).  Each 256-thread workgroup fills 16 KiB
+// of LDS, small enough for eight workgroups (32 waves, the most a CU holds) to
+// be resident, since with fewer waves the rate measured is their latency, not
+// the LDS's; every lane issues 8 independent reads per iteration at
 // consecutive, conflict-free 16-byte slots and folds them into a checksum; one
 // wave reads the shader-cycle and real-time counters around its loop, as in
 // the matrix-core probe.  Built into libsa_probe.so; bench.py times the launch.
@@ -13,7 +15,7 @@
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWords = 16384;  // 64 KiB of LDS per workgroup
+constexpr int kWords = 4096;  // 16 KiB of LDS per workgroup
 constexpr int kReads = 8;      // independent reads per lane and iteration
 
 template <int KIND>
@@ -35,14 +37,14 @@ __global__ void __launch_bounds__(256) lds_read_kernel(int iters, uint32_t* __re
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int u = 0; u < kReads; ++u) {
-            // 16-byte slot (tid + 256 u + 64 it) mod 4096: a wave's lanes take
-            // consecutive slots; the highest word read is 4 * 4095 + 3 < kWords
-            const int slot = (tid + 256 * u + 64 * it) & 4095;
+            // 16-byte slot (tid + 256 u + 64 it) mod kWords / 4: a wave's lanes
+            // take consecutive slots; the highest word read is kWords - 1
+            const int slot = (tid + 256 * u + 64 * it) & (kWords / 4 - 1);
             if constexpr (KIND == 0) {
                 const u32x4 x = *reinterpret_cast<const u32x4*>(&buf[4 * slot]);
                 acc[u] ^= x[0] ^ x[1] ^ x[2] ^ x[3];
             } else {
-                // 8 bytes at word 2 * slot (at most 8191 + 1 < kWords)
+                // 8 bytes at word 2 * slot (at most kWords / 2 - 1)
                 const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) s16x4*)(&buf[2 * slot]));
                 acc[u] ^= (uint32_t)(uint16_t)v[0] ^ ((uint32_t)(uint16_t)v[1] << 16) ^ (uint32_t)(uint16_t)v[2] ^
