@@ -6,7 +6,8 @@ One step = forward and backward over each of the two measured workloads:
   fixed,   n = 65,536, l = 256, c = 32, B = 64, batch 1, 8 merged heads of 64
 Inputs are seeded N(0, 1) bf16 tensors already resident in device memory; the
 block layouts are built once before timing.  The backward runs as its three
-stages (row statistics, dQ, dK / dV: sparse_attn_bwd_stage).  The timed steps
+stages in two calls (sparse_attn_bwd_stage: row statistics with dQ, which the
+library runs as one launch, then dK / dV).  The timed steps
 record HIP events on the library's stream only around each dK / dV stage (an
 event costs the stream a few microseconds); after them, two untimed passes
 time each workload alone and split it into its forward and backward stages.
@@ -447,14 +448,17 @@ def main():
         runs.append(dict(w=w, x=x, lay=lay, q=q, k=k, v=v, dout=dout, o=o, lse=lse, grads=grads, ws=ws))
     torch.cuda.synchronize()
 
-    stages = (sa.SA_BWD_ROW_STATS, sa.SA_BWD_DQ, sa.SA_BWD_DKDV)
-
+    # the backward in two calls: the row statistics with dQ (the library runs
+    # them as one launch where it can), then dK / dV, the roofline's kernel
+    stage_calls = (("row_stats_and_dq", sa.SA_BWD_ROW_STATS | sa.SA_BWD_DQ), ("dkdv", sa.SA_BWD_DKDV))
+    stages = tuple(bits for _, bits in stage_calls)
     DKDV = len(stages) - 1  # index of the dK / dV stage
+    LAST = 1 + len(stages)  # index of the event after the last stage
 
     def step(events=None, marks="dkdv"):
-        """One step.  events[idx] holds five events of workload idx: before the
-        forward, after it, and after each backward stage.  marks = "dkdv"
-        records only the two around the dK / dV stage (the timed steps: each
+        """One step.  events[idx] holds the events of workload idx: before the
+        forward, after it, and after each backward call.  marks = "dkdv"
+        records only the two around the dK / dV call (the timed steps: each
         event costs the stream a few microseconds), "total" only the first
         and the last, "all" every one."""
         for idx, r in enumerate(runs):
@@ -474,7 +478,8 @@ def main():
                     ev[2 + si].record(stream)
 
     def new_events():
-        return [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in runs] for _ in range(args.steps)]
+        return [[[torch.cuda.Event(enable_timing=True) for _ in range(LAST + 1)] for _ in runs]
+                for _ in range(args.steps)]
 
     for _ in range(args.warmup):
         step()
@@ -506,9 +511,9 @@ def main():
     total_credited = total_element = 0.0
     for idx, r in enumerate(runs):
         w = r["w"]
-        total_ms = avg_ms(ev_total, idx, 0, 4)
-        fwd_ms, bwd_ms = avg_ms(ev_all, idx, 0, 1), avg_ms(ev_all, idx, 1, 4)
-        stage_ms = [avg_ms(ev_all, idx, 1, 2), avg_ms(ev_all, idx, 2, 3), avg_ms(ev_all, idx, 3, 4)]
+        total_ms = avg_ms(ev_total, idx, 0, LAST)
+        fwd_ms, bwd_ms = avg_ms(ev_all, idx, 0, 1), avg_ms(ev_all, idx, 1, LAST)
+        stage_ms = {name: avg_ms(ev_all, idx, 1 + si, 2 + si) for si, (name, _) in enumerate(stage_calls)}
         cred, cred_fwd = credited_flops(w, r["lay"].nnz)
         total_credited += cred
         pairs = attended_pairs(w)
@@ -518,7 +523,7 @@ def main():
             "n": w.n, "nnz_blocks": r["lay"].nnz, "credited_flop": cred, "element_level_flop": elem,
             "attended_pairs_per_head": pairs,
             "ms": total_ms, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
-            "bwd_stage_ms": {"row_stats": stage_ms[0], "dq": stage_ms[1], "dkdv": stage_ms[2]},
+            "bwd_stage_ms": stage_ms,
             "dkdv_ms_timed_steps": dkdv_ms_all[idx],
             "timing_note": ("ms: forward + backward from events at the workload's ends; fwd_ms, bwd_ms and "
                             "bwd_stage_ms from a pass with an event after every stage (a few us each); both "

@@ -210,9 +210,14 @@ int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_
  * a stage needs the earlier ones of the same call (same arguments, same
  * workspace) already enqueued: SA_BWD_DQ and SA_BWD_DKDV read the row
  * statistics, and SA_BWD_DKDV also reads D where the dQ stage recomputes it
- * (fixed pattern with few summary keys per row).  All three in one call equal
- * sparse_attn_bwd.  Arguments and errors as sparse_attn_bwd; SA_ERR_INVALID for
- * an empty or unknown set, SA_ERR_UNSUPPORTED for a partial set in fp32.
+ * (fixed pattern with few summary keys per row) and the work order the row
+ * statistics stage lays out (so each SA_BWD_DKDV needs its own earlier
+ * SA_BWD_ROW_STATS).  SA_BWD_ROW_STATS and SA_BWD_DQ in one call run as one
+ * launch where the dQ grid allows (its kernel then computes its rows'
+ * statistics itself); results are the same either way up to the summation
+ * order of D.  All three in one call equal sparse_attn_bwd.  Arguments and
+ * errors as sparse_attn_bwd; SA_ERR_INVALID for an empty or unknown set,
+ * SA_ERR_UNSUPPORTED for a partial set in fp32.
  */
 enum { SA_BWD_ROW_STATS = 1, SA_BWD_DQ = 2, SA_BWD_DKDV = 4, SA_BWD_ALL_STAGES = 7 };
 

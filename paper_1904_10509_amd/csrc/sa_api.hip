@@ -115,6 +115,7 @@ sa::AttnArgs make_args(const PatternArgs& p, int32_t batch, int32_t heads, int32
     a.sub = p.sub;
     a.claim_mode = sa::CLAIM_QUEUES;
     a.pairs = 0;
+    a.row_stats = 0;
     a.dl = sa::make_divl(p.l);
     a.walk = sa::WALK_LAYOUT;
     a.qshift = 0;
@@ -258,20 +259,23 @@ hipError_t launch_bwd(sa::AttnArgs a, bool by_classes, sa::AttnArgs cls, int dty
                       const void* v, const void* o, const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* ws, hipStream_t s, int parts = sa::BWD_ALL) {
     if (!by_classes) return sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, parts);
-    // the band's part of each stage first (merged), then the classes' part
+    // the band's part of each stage first (merged), then the classes' part;
+    // the row statistics, in row order, go with the band's dQ (merged) or run
+    // alone (A2: no band)
     const bool merged = a.mode == sa::MODE_MERGED;
     if (merged) {
         a.walk = sa::WALK_BAND;
         cls.epilogue = sa::EPI_ADD;
     }
     hipError_t e = hipSuccess;
-    for (int stage : {sa::BWD_PRE, sa::BWD_DQ, sa::BWD_DKDV}) {
-        if (!(parts & stage)) continue;
-        if (e == hipSuccess && (merged || stage == sa::BWD_PRE))
-            e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, stage);
-        if (e == hipSuccess && stage != sa::BWD_PRE)
-            e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, stage);
-    }
+    const int band_first = merged ? parts & (sa::BWD_PRE | sa::BWD_DQ) : parts & sa::BWD_PRE;
+    if (band_first) e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, band_first);
+    if (e == hipSuccess && (parts & sa::BWD_DQ))
+        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DQ);
+    if (e == hipSuccess && merged && (parts & sa::BWD_DKDV))
+        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DKDV);
+    if (e == hipSuccess && (parts & sa::BWD_DKDV))
+        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DKDV);
     return e;
 }
 

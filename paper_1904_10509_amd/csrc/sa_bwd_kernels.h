@@ -188,11 +188,13 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
 }
 
 // Rows of the row-statistics kernel per 256-thread workgroup: one thread per
-// row in fp32; in bf16, D / 8 lanes per row, each reading 16 bytes, so that a
-// wave's load covers whole rows (64 / (D / 8) of them) contiguously.
+// row in fp32; in bf16 four lanes per row, lane g reading the 16-byte chunks
+// 8 g + 32 ks (ks = 0 .. D/32 - 1), the chunks the dQ kernel's lane g holds, so
+// that D sums in the dQ kernel's order (see bwd_dq_bf16_kernel's row_stats):
+// the same bits whichever kernel computes it.
 template <int D, typename T>
 constexpr int pre_rows_per_group() {
-    return sizeof(T) == 2 ? 256 / (D / 8) : 256;
+    return sizeof(T) == 2 ? 64 : 256;
 }
 
 template <int D, typename T>
@@ -201,30 +203,26 @@ bwd_pre_kernel(AttnArgs a, const T* __restrict__ o, const T* __restrict__ dout, 
                float* __restrict__ ndelta, float* __restrict__ nlse2, unsigned long long* __restrict__ queue,
                int32_t* __restrict__ items, int32_t* __restrict__ order) {
     if (queue && (int)blockIdx.x < layout_count(a.mode, a.sub)) build_schedule(a, blockIdx.x, queue, items, order);
-    constexpr int kLanes = sizeof(T) == 2 ? D / 8 : 1;  // lanes per row
+    constexpr int kLanes = sizeof(T) == 2 ? 4 : 1;  // lanes per row
     const int64_t row = (int64_t)blockIdx.x * pre_rows_per_group<D, T>() + threadIdx.x / kLanes;
-    const int part = threadIdx.x % kLanes;  // 8-element part of the row (bf16)
+    const int g = threadIdx.x % kLanes;
     const int64_t rows = (int64_t)a.batch * a.heads * a.n;
-    // (kLanes divides 64, so the lanes of a row share their wave and its
-    // exit: every lane of a row reaches the reduction below)
+    // (the four lanes of a row share their wave and its exit, so every lane
+    // of a row reaches the reduction below)
     if (row >= rows) return;
     const int64_t bh = row / a.n, i = row % a.n;
     const int64_t off = (bh / a.heads) * a.sb + (bh % a.heads) * a.sh + i * a.ss;
     float acc = 0.f;
     if constexpr (sizeof(T) == 2) {
-        const u32x4 x = *reinterpret_cast<const u32x4*>(o + off + 8 * part);
-        const u32x4 y = *reinterpret_cast<const u32x4*>(dout + off + 8 * part);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc = fmaf(__uint_as_float(x[e] << 16), __uint_as_float(y[e] << 16), acc);
-            acc = fmaf(__uint_as_float(x[e] & 0xffff0000u), __uint_as_float(y[e] & 0xffff0000u), acc);
-        }
-#pragma unroll
-        for (int m = 1; m < kLanes; m *= 2) acc += __shfl_xor(acc, m);
+        for (int ks = 0; ks < D / 32; ++ks)
+            acc += dot_bf16x8(ld_bf16x8(dout + off + ks * 32 + 8 * g), ld_bf16x8(o + off + ks * 32 + 8 * g));
+        acc += __shfl_xor(acc, 1);  // (g0 + g1) and (g2 + g3), then their sum
+        acc += __shfl_xor(acc, 2);
     } else {
         for (int t = 0; t < D; ++t) acc = fmaf(o[off + t], dout[off + t], acc);
     }
-    if (part != 0) return;
+    if (g != 0) return;
     ndelta[row] = -acc;
     nlse2[row] = -lse[row] * kLog2e;  // an empty row (LSE = -inf) gives +inf; its items are all masked
 }
@@ -255,15 +253,27 @@ struct DqCfg {
 // the exact O rather than for the O rounded to bf16 that the pre kernel
 // reads, and stores it for the dK / dV kernel; the second forms dS from it
 // and takes dS into the dQ product in a high and a low bf16 part.
+//
+// a.row_stats: the kernel does the pre kernel's work for its own rows, D_i =
+// dO_i . O_i and the LSE in base 2 (it holds dO_i already), and writes both for
+// the dK / dV kernel; its first layout_count workgroups build the dK / dV
+// schedule.  The launcher sets it when the grid covers every row and at least
+// that many workgroups, and then launches no pre kernel.
 template <int D, int BLK, int PAT, int MODE, bool FULL_BODY, bool SPLIT>
 __global__ void __launch_bounds__((DqCfg<D, BLK, PAT>::NT))
     __attribute__((amdgpu_waves_per_eu(DqCfg<D, BLK, PAT>::WAVES_PER_EU)))
 bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
                    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                    const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
-                   const float* __restrict__ nlse2, float* __restrict__ ndelta,
-                   uint16_t* __restrict__ dq) {
+                   float* __restrict__ nlse2, float* __restrict__ ndelta,
+                   uint16_t* __restrict__ dq, const uint16_t* __restrict__ o, const float* __restrict__ lse,
+                   unsigned long long* __restrict__ queue, int32_t* __restrict__ items,
+                   int32_t* __restrict__ order) {
     using C = DqCfg<D, BLK, PAT>;
+    if (a.row_stats && queue) {  // uniform over the workgroup
+        const int64_t wg = blockIdx.x + (int64_t)gridDim.x * (blockIdx.y + (int64_t)gridDim.y * blockIdx.z);
+        if (wg < layout_count(a.mode, a.sub)) build_schedule(a, (int)wg, queue, items, order);
+    }
     __shared__ __attribute__((aligned(16))) uint16_t sK[C::NS][BLK * D];
     __shared__ __attribute__((aligned(16))) uint16_t sV[C::NS][BLK * D];
     constexpr uint32_t kTileBytes = BLK * D * 2;
@@ -297,8 +307,25 @@ bwd_dq_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_
             qf[u][ks] = ld_bf16x8(q + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
             of[u][ks] = ld_bf16x8(dout + base + (int64_t)i * a.ss + ks * 32 + 8 * g);
         }
-        nl2[u] = nlse2[stat_index(a, b, h, i)];
-        const float nd = ndelta[stat_index(a, b, h, i)];
+        const int64_t si = stat_index(a, b, h, i);
+        float nd;
+        if (a.row_stats) {
+            // D_i over the lanes of row i (each holds 8 g .. 8 g + 7 of every
+            // 32-wide chunk), and -LSE_i log2 e, as the pre kernel writes them
+            float part = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks)
+                part += dot_bf16x8(of[u][ks], ld_bf16x8(o + base + (int64_t)i * a.ss + ks * 32 + 8 * g));
+            nd = -sum_over_g(part);
+            nl2[u] = -lse[si] * kLog2e;  // an empty row (LSE = -inf) gives +inf; its items are all masked
+            if (g == 0) {
+                ndelta[si] = nd;
+                nlse2[si] = nl2[u];
+            }
+        } else {
+            nl2[u] = nlse2[si];
+            nd = ndelta[si];
+        }
         nd4[u] = f32x4{nd, nd, nd, nd};
         rl[u] = row_lane(i - a.qshift, a.dl);
 #pragma unroll
@@ -1240,16 +1267,22 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         // (n = 65,536, l = 256, 8 heads: 3% faster).
         const int64_t per_head = (int64_t)qgrid / bh_count;
         ak.pairs = PAT == FIXED && BLK == 64 && a.l % 64 == 0 && 2 * ((int64_t)a.n / a.l) >= 5 * per_head;
-        if (parts & BWD_PRE)
+        // The row statistics go into the dQ kernel when both are asked for and
+        // its grid (every row) holds a workgroup per layout for the schedule.
+        AttnArgs aq = ak;
+        aq.row_stats = (parts & BWD_PRE) && (parts & BWD_DQ) &&
+                       (int64_t)a.heads * a.nq * a.batch >= layout_count(a.mode, a.sub);
+        if ((parts & BWD_PRE) && !aq.row_stats)
             hipLaunchKernelGGL((bwd_pre_kernel<D, uint16_t>), dim3((unsigned)pre_groups), dim3(256), 0, stream, ak,
                                (const uint16_t*)o, (const uint16_t*)dout, lse, ndelta, nlse2, ws.queue, ws.items,
                                ws.order);
         if (parts & BWD_DQ) (void)with_full_body<PAT>(a, [&](auto fb) {
             auto dq_kernel = [&](auto sp) {
                 hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, BLK, PAT, MODE, decltype(fb)::value, decltype(sp)::value>),
-                                   grid, dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, a, a.row_ptr, a.col_idx,
+                                   grid, dim3(DqCfg<D, BLK, PAT>::NT), 0, stream, aq, a.row_ptr, a.col_idx,
                                    (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)dout,
-                                   nlse2, ndelta, (uint16_t*)dq);
+                                   nlse2, ndelta, (uint16_t*)dq, (const uint16_t*)o, lse, ws.queue, ws.items,
+                                   ws.order);
             };
             if constexpr (PAT == FIXED) {
                 if (split) dq_kernel(std::true_type{});

@@ -83,6 +83,7 @@ struct AttnArgs {
     int32_t sub;           // fixed: 0 = one summary window for all heads, else floor(l / c) subblocks
     int32_t claim_mode;    // dK / dV work order, one of CLAIM_* (set by the backward launcher)
     int32_t pairs;         // dK / dV: summary halves walked in pairs (set by the backward launcher)
+    int32_t row_stats;     // dQ: compute the row statistics itself, in place of the pre kernel (set by the launcher)
     DivL dl;               // division by l
     int32_t walk;          // WALK_*
     int32_t qshift;        // masks see query i as i - qshift (a causal limit j <= i - qshift)
