@@ -5,12 +5,14 @@ One step = forward and backward over each of the two measured workloads:
   strided, n = 12,288, l = 128, B = 64, batch 2, 8 merged heads of 64
   fixed,   n = 65,536, l = 256, c = 32, B = 64, batch 1, 8 merged heads of 64
 Inputs are seeded N(0, 1) bf16 tensors already resident in device memory; the
-block layouts are built once before timing.  The backward runs as its three
-stages in two calls (sparse_attn_bwd_stage: row statistics with dQ, which the
-library runs as one launch, then dK / dV).  The timed steps
-record HIP events on the library's stream only around each dK / dV stage (an
-event costs the stream a few microseconds); after them, two untimed passes
-time each workload alone and split it into its forward and backward stages.
+block layouts are built once before timing.  The fixed workload (the one with
+the most attended pairs) runs its backward in two calls of
+sparse_attn_bwd_stage, the row statistics with dQ (one launch in the library)
+and then dK / dV, and the timed steps record HIP events on the library's
+stream only around that dK / dV call (an event costs the stream a few
+microseconds); the strided workload's backward is one call.  After the timed
+steps, two untimed passes time each workload alone and split it into its
+forward and backward calls.
 
 The metric credits every present B x B block 14 B^2 d FLOPs per (batch,
 head): 4 B^2 d forward (QK^T, PV) and 10 B^2 d backward (QK^T recomputed,
@@ -448,19 +450,25 @@ def main():
         runs.append(dict(w=w, x=x, lay=lay, q=q, k=k, v=v, dout=dout, o=o, lse=lse, grads=grads, ws=ws))
     torch.cuda.synchronize()
 
-    # the backward in two calls: the row statistics with dQ (the library runs
-    # them as one launch where it can), then dK / dV, the roofline's kernel
-    stage_calls = (("row_stats_and_dq", sa.SA_BWD_ROW_STATS | sa.SA_BWD_DQ), ("dkdv", sa.SA_BWD_DKDV))
-    stages = tuple(bits for _, bits in stage_calls)
-    DKDV = len(stages) - 1  # index of the dK / dV stage
-    LAST = 1 + len(stages)  # index of the event after the last stage
+    # The roofline's kernel is the dK / dV stage of the workload with the most
+    # attended pairs; that workload's backward runs as two calls, the row
+    # statistics with dQ (one launch in the library) and then dK / dV, with
+    # events around the second.  Every other workload's backward is one call
+    # (the strided one then runs its short residue classes' dQ and dK / dV as
+    # one launch).
+    dom = max(range(len(runs)), key=lambda i: (attended_pairs(runs[i]["w"]) or 0) * runs[i]["w"].batch
+              * runs[i]["w"].heads)
+    split_calls = (("row_stats_and_dq", sa.SA_BWD_ROW_STATS | sa.SA_BWD_DQ), ("dkdv", sa.SA_BWD_DKDV))
+    whole_call = (("backward", sa.SA_BWD_ALL_STAGES),)
+    calls = [split_calls if i == dom else whole_call for i in range(len(runs))]
+    LAST = 1 + len(split_calls)  # events per workload: before the forward, after it, after each call
 
     def step(events=None, marks="dkdv"):
         """One step.  events[idx] holds the events of workload idx: before the
         forward, after it, and after each backward call.  marks = "dkdv"
-        records only the two around the dK / dV call (the timed steps: each
-        event costs the stream a few microseconds), "total" only the first
-        and the last, "all" every one."""
+        records only the two around the dominant workload's dK / dV call (the
+        timed steps: each event costs the stream a few microseconds), "total"
+        only the first and the last, "all" every one."""
         for idx, r in enumerate(runs):
             ev = events[idx] if events is not None else None
             if ev is not None and marks != "dkdv":
@@ -468,14 +476,16 @@ def main():
             sa.forward(r["q"], r["k"], r["v"], r["lay"], r["w"].scale, out=r["o"], lse=r["lse"])
             if ev is not None and marks == "all":
                 ev[1].record(stream)
-            for si, st in enumerate(stages):
-                if ev is not None and marks == "dkdv" and si == DKDV:
+            n_calls = len(calls[idx])
+            for si, (name, st) in enumerate(calls[idx]):
+                if ev is not None and marks == "dkdv" and name == "dkdv":
                     ev[1 + si].record(stream)
                 sa.backward(r["q"], r["k"], r["v"], r["o"], r["dout"], r["lse"], r["lay"], r["w"].scale,
                             grads=r["grads"], workspace=r["ws"], stages=st)
-                if ev is not None and (marks == "all" or (marks == "dkdv" and si == DKDV)
-                                       or (marks == "total" and si == len(stages) - 1)):
+                if ev is not None and (marks == "all" or (marks == "dkdv" and name == "dkdv")):
                     ev[2 + si].record(stream)
+                if ev is not None and marks == "total" and si == n_calls - 1:
+                    ev[LAST].record(stream)
 
     def new_events():
         return [[[torch.cuda.Event(enable_timing=True) for _ in range(LAST + 1)] for _ in runs]
@@ -497,7 +507,7 @@ def main():
     def avg_ms(evs, idx, a, b):
         return sum(evs[s_][idx][a].elapsed_time(evs[s_][idx][b]) for s_ in range(args.steps)) / args.steps
 
-    dkdv_ms_all = [avg_ms(ev, idx, 1 + DKDV, 2 + DKDV) for idx in range(len(runs))]
+    dkdv_ms = avg_ms(ev, dom, len(split_calls), 1 + len(split_calls))
     # after the timed steps, untimed: each workload's own time (events at its
     # ends only), then its split into forward and backward stages (every event)
     ev_total, ev_all = new_events(), new_events()
@@ -512,8 +522,9 @@ def main():
     for idx, r in enumerate(runs):
         w = r["w"]
         total_ms = avg_ms(ev_total, idx, 0, LAST)
-        fwd_ms, bwd_ms = avg_ms(ev_all, idx, 0, 1), avg_ms(ev_all, idx, 1, LAST)
-        stage_ms = {name: avg_ms(ev_all, idx, 1 + si, 2 + si) for si, (name, _) in enumerate(stage_calls)}
+        n_calls = len(calls[idx])
+        fwd_ms, bwd_ms = avg_ms(ev_all, idx, 0, 1), avg_ms(ev_all, idx, 1, 1 + n_calls)
+        stage_ms = {name: avg_ms(ev_all, idx, 1 + si, 2 + si) for si, (name, _) in enumerate(calls[idx])}
         cred, cred_fwd = credited_flops(w, r["lay"].nnz)
         total_credited += cred
         pairs = attended_pairs(w)
@@ -524,7 +535,7 @@ def main():
             "attended_pairs_per_head": pairs,
             "ms": total_ms, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
             "bwd_stage_ms": stage_ms,
-            "dkdv_ms_timed_steps": dkdv_ms_all[idx],
+            "dkdv_ms_timed_steps": dkdv_ms if idx == dom else None,
             "timing_note": ("ms: forward + backward from events at the workload's ends; fwd_ms, bwd_ms and "
                             "bwd_stage_ms from a pass with an event after every stage (a few us each); both "
                             "passes run after the timed steps"),
@@ -542,17 +553,17 @@ def main():
     value = total_credited / (ms_per_step * 1e-3) / 1e12
 
     # roofline of the dominant kernel: the dK / dV stage (one bwd_dkdv_bf16_kernel
-    # launch) of the workload where it takes longest, priced at its element-level
-    # work, 8 d FLOPs per attended pair (S, dP, dV, dK)
-    dom = max(range(len(runs)), key=lambda i: dkdv_ms_all[i])
+    # launch) of the workload with the most attended pairs, priced at its
+    # element-level work, 8 d FLOPs per attended pair (S, dP, dV, dK), over its
+    # event-timed duration in the timed steps
     dw = runs[dom]["w"]
     dkdv_flop = 8.0 * dw.d_head * attended_pairs(dw) * dw.batch * dw.heads
-    achieved = dkdv_flop / (dkdv_ms_all[dom] * 1e-3) / 1e12
+    achieved = dkdv_flop / (dkdv_ms * 1e-3) / 1e12
     roofline = {
         "kernel": f"bwd_dkdv_bf16_kernel (dK/dV stage of sparse_attn_bwd) on {dw.name}",
         "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
         "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(dw.name),
-        "avg_ms": dkdv_ms_all[dom], "flop_per_launch": dkdv_flop,
+        "avg_ms": dkdv_ms, "flop_per_launch": dkdv_flop,
         "flop_basis": "8 d per attended pair (S, dP, dV, dK) x pairs per head x batch x heads",
         "algorithmic_bytes": algorithmic_dkdv_bytes(dw),
     }

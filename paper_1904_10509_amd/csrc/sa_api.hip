@@ -259,23 +259,21 @@ hipError_t launch_bwd(sa::AttnArgs a, bool by_classes, sa::AttnArgs cls, int dty
                       const void* v, const void* o, const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* ws, hipStream_t s, int parts = sa::BWD_ALL) {
     if (!by_classes) return sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, parts);
-    // the band's part of each stage first (merged), then the classes' part;
-    // the row statistics, in row order, go with the band's dQ (merged) or run
-    // alone (A2: no band)
+    // the band's stages first (merged; the row statistics, in row order, go
+    // with the band's dQ), or the row statistics alone (A2: no band)
     const bool merged = a.mode == sa::MODE_MERGED;
     if (merged) {
         a.walk = sa::WALK_BAND;
         cls.epilogue = sa::EPI_ADD;
     }
     hipError_t e = hipSuccess;
-    const int band_first = merged ? parts & (sa::BWD_PRE | sa::BWD_DQ) : parts & sa::BWD_PRE;
-    if (band_first) e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, band_first);
-    if (e == hipSuccess && (parts & sa::BWD_DQ))
-        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DQ);
-    if (e == hipSuccess && merged && (parts & sa::BWD_DKDV))
-        e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DKDV);
-    if (e == hipSuccess && (parts & sa::BWD_DKDV))
-        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, sa::BWD_DKDV);
+    // the classes' dQ and dK / dV last and together (short classes run them
+    // as one launch)
+    const int band = merged ? parts : parts & sa::BWD_PRE;
+    if (band) e = sa::bwd_launch(a, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, band);
+    const int classes = parts & (sa::BWD_DQ | sa::BWD_DKDV);
+    if (e == hipSuccess && classes)
+        e = sa::bwd_launch(cls, dtype, q, k, v, o, dout, lse, dq, dk, dv, ws, s, classes);
     return e;
 }
 

@@ -1309,10 +1309,222 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
     });
 }
 
+// ---------------------------------------------------------------------------
+// bf16, matrix cores: the whole backward of one short residue class
+// ---------------------------------------------------------------------------
+// In the class view of a strided call each (batch x head, class) unit is
+// dense causal attention over M positions with the causal limit moved back
+// a.qshift steps.  Where M <= 128 (a multiple of 32), one workgroup of M / 16
+// waves takes a unit whole: its Q, K, V, dO and row statistics go into LDS
+// once, and
+//   phase 1: wave w takes keys 16 w .. 16 w + 15 and walks the 32-query chunks
+//     that attend them, forming S and dP once per pair: dV and dK accumulate
+//     in registers, dS (bf16, the values the dK product takes) goes to LDS
+//     transposed, dS^T[key][query];
+//   phase 2: wave w takes queries 16 w .. 16 w + 15: dQ^T = K^T dS^T over the
+//     keys they attend, both operands read back from LDS.
+// The separate dQ and dK / dV kernels form S and dP twice and read the four
+// tensors twice.  No atomics: every output row has one writer.
+template <int D, int M>
+struct ClassBwdCfg {
+    static constexpr int NW = M / 16;       // waves
+    static constexpr int NT = NW * 64;
+    static constexpr int KS = D / 32;
+    static constexpr int DB = D / 16;
+    static constexpr int MP = M + 8;         // row stride of dS^T in LDS (elements, rows 16-byte aligned)
+    static constexpr int MS = (M + 63) / 64 * 64;  // row statistics, whole 64-row loads
+    static_assert(M % 32 == 0 && M <= 128, "classes of 32, 64, 96 or 128 positions");
+};
+
+template <int D, int M>
+__global__ void __launch_bounds__((ClassBwdCfg<D, M>::NT))
+bwd_class_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                      const uint16_t* __restrict__ v, const uint16_t* __restrict__ dout,
+                      const float* __restrict__ nlse2, const float* __restrict__ ndelta,
+                      uint16_t* __restrict__ dq, uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+    using C = ClassBwdCfg<D, M>;
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[M * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sK[M * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sV[M * D];
+    __shared__ __attribute__((aligned(16))) uint16_t sO[M * D];       // dO
+    __shared__ __attribute__((aligned(16))) uint16_t sST[M * C::MP];  // dS^T
+    __shared__ __attribute__((aligned(16))) float sL[C::MS];          // -LSE log2 e
+    __shared__ __attribute__((aligned(16))) float sD[C::MS];          // -D
+
+    const int h = blockIdx.x, b = blockIdx.z;  // class, batch x head
+    const int tid = threadIdx.x, lane = tid % 64, g = lane / 16, r = lane % 16;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
+    const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
+    const int shift = a.qshift;
+    const float c2 = a.scale_log2;
+
+    // The unit's four tensors, M x D each in the swizzled tile layout, by
+    // direct-to-LDS loads: wave w takes the 1 KiB windows w, w + NW, ...
+    // (D / 32 per tensor); the launcher keeps (M - 1) ss + D inside 32-bit
+    // byte offsets.  Waves 0 and 1 load the row statistics, 64 rows a load.
+    constexpr int kWin = M * D / 512;
+    static_assert(kWin % C::NW == 0, "every wave issues the same number of loads");
+#pragma unroll
+    for (int kk = 0; kk < kWin / C::NW; ++kk) {
+        const int win = w + C::NW * kk;
+        const int oe = 512 * win + 8 * lane;  // element offset of this lane's slot
+        const int row = oe / D, chunk = ((oe % D) / 8) ^ Swz<D>::perm(row);
+        const uint32_t off = (uint32_t)(((int64_t)row * a.ss + 8 * chunk) * 2);
+        dma_b128(uniform_ptr(q + base), off, lds_addr(sQ) + 1024 * win);
+        dma_b128(uniform_ptr(k + base), off, lds_addr(sK) + 1024 * win);
+        dma_b128(uniform_ptr(v + base), off, lds_addr(sV) + 1024 * win);
+        dma_b128(uniform_ptr(dout + base), off, lds_addr(sO) + 1024 * win);
+    }
+    if (64 * w < M) {
+        const int m0 = 64 * w, nv = M - m0 < 64 ? M - m0 : 64;
+        const int64_t st0 = stat_index(a, b, h, m0);
+        load_row_stats_async(nlse2 + st0, nv, lds_addr(sL) + 4 * m0, lane, (uint32_t)a.lse_ss);
+        load_row_stats_async(ndelta + st0, nv, lds_addr(sD) + 4 * m0, lane, (uint32_t)a.lse_ss);
+    }
+    // dS^T starts at zero: pairs no chunk visits stay zero for phase 2
+    for (int i = tid; i < M * C::MP / 8; i += C::NT) reinterpret_cast<u32x4*>(sST)[i] = u32x4{0u, 0u, 0u, 0u};
+    wait_loads_upto<0>();
+    __syncthreads();
+
+    TileReader<D> rd;
+    rd.init(g, r);
+
+    // phase 1: this lane's key j; S^T blocks s[t] = q_(16 qblk + 4 g + t) . k_j
+    const int j = 16 * w + r;
+    bf16x8 kf[C::KS], vf[C::KS];
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+        kf[ks] = rd.row(sK, 16 * w, ks);
+        vf[ks] = rd.row(sV, 16 * w, ks);
+    }
+    f32x4 dvacc[C::DB], dkacc[C::DB];
+#pragma unroll
+    for (int db = 0; db < C::DB; ++db) {
+        dvacc[db] = zero4();
+        dkacc[db] = zero4();
+    }
+    // the first 32-query chunk holding a query i >= 16 w + shift (one that
+    // attends a key of this wave)
+    for (int qc = (16 * w + shift) / 32; qc < M / 32; ++qc) {
+        f32x4 p[2], ds[2];
+#pragma unroll
+        for (int hq = 0; hq < 2; ++hq) {
+            const int qblk = 2 * qc + hq;
+            bf16x8 qa[C::KS], oa[C::KS];
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) {
+                qa[ks] = rd.row(sQ, 16 * qblk, ks);
+                oa[ks] = rd.row(sO, 16 * qblk, ks);
+            }
+            f32x4 sacc = zero4(), dpacc = *reinterpret_cast<const f32x4*>(&sD[16 * qblk + 4 * g]);
+#pragma unroll
+            for (int ks = 0; ks < C::KS; ++ks) {
+                sacc = mfma_16x16x32(qa[ks], kf[ks], sacc);
+                dpacc = mfma_16x16x32(oa[ks], vf[ks], dpacc);
+            }
+            const f32x4 nl = *reinterpret_cast<const f32x4*>(&sL[16 * qblk + 4 * g]);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int i = 16 * qblk + 4 * g + t;  // query; pair (i, j) attended when j <= i - shift
+                const float pv = j <= i - shift ? exp2_fast(fmaf(sacc[t], c2, nl[t])) : 0.f;
+                p[hq][t] = pv;
+                ds[hq][t] = pv * dpacc[t];
+            }
+        }
+        const bf16x8 pb = pack_bf16x8(p[0], p[1]), sb = pack_bf16x8(ds[0], ds[1]);
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {
+            dvacc[db] = mfma_16x16x32(rd.tr(sO, 32 * qc, 32 * qc + 16, db), pb, dvacc[db]);
+            dkacc[db] = mfma_16x16x32(rd.tr(sQ, 32 * qc, 32 * qc + 16, db), sb, dkacc[db]);
+        }
+        // dS^T row j, queries 32 qc + 16 hq + 4 g .. +3
+        *reinterpret_cast<uint2*>(&sST[j * C::MP + 32 * qc + 4 * g]) = pack_bf16x4_bits(ds[0]);
+        *reinterpret_cast<uint2*>(&sST[j * C::MP + 32 * qc + 16 + 4 * g]) = pack_bf16x4_bits(ds[1]);
+    }
+    // this lane holds dV^T / dK^T at d = 16 db + 4 g + t for key j
+    {
+        uint16_t* dvrow = dv + base + (int64_t)j * a.ss;
+        uint16_t* dkrow = dk + base + (int64_t)j * a.ss;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {
+            uint2* dvp = reinterpret_cast<uint2*>(dvrow + db * 16 + 4 * g);
+            uint2* dkp = reinterpret_cast<uint2*>(dkrow + db * 16 + 4 * g);
+            f32x4 xv = dvacc[db], xk = dkacc[db] * a.scale;
+            if (a.epilogue == EPI_ADD) {
+                xv += bf16x4_to_f32x4(*dvp);
+                xk += bf16x4_to_f32x4(*dkp);
+            }
+            *dvp = pack_bf16x4_bits(xv);
+            *dkp = pack_bf16x4_bits(xk);
+        }
+    }
+    __syncthreads();  // dS^T complete
+
+    // phase 2: queries q0 + r; dQ^T = K^T dS^T over the 32-key chunks up to the
+    // last key the wave's queries attend (q0 + 15 - shift)
+    const int q0 = 16 * w, last = q0 + 15 - shift;
+    f32x4 dqacc[C::DB];
+#pragma unroll
+    for (int db = 0; db < C::DB; ++db) dqacc[db] = zero4();
+    for (int kc = 0; last >= 0 && kc <= last / 32; ++kc) {
+        // dS^T rows 32 kc + 4 g + u and 32 kc + 16 + 4 g + u of query column
+        // q0 + r (transposing reads), the key order of rd.tr below
+        const uint16_t* t = &sST[(32 * kc + 4 * g + r / 4) * C::MP + q0 + 4 * (r & 3)];
+        const u32x2 lo = ld_tr16(t), hi = ld_tr16(t + 16 * C::MP);
+        const bf16x8 dsb = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+            dqacc[db] = mfma_16x16x32(rd.tr(sK, 32 * kc, 32 * kc + 16, db), dsb, dqacc[db]);
+    }
+    uint16_t* drow = dq + base + (int64_t)(q0 + r) * a.ss;
+#pragma unroll
+    for (int db = 0; db < C::DB; ++db) {
+        uint2* dst = reinterpret_cast<uint2*>(drow + db * 16 + 4 * g);
+        f32x4 x = dqacc[db] * a.scale;
+        if (a.epilogue == EPI_ADD) x += bf16x4_to_f32x4(*dst);
+        *dst = pack_bf16x4_bits(x);
+    }
+}
+
+// Whether a call's dQ and dK / dV can run as one bwd_class_bf16_kernel per
+// unit: the class view (a dense walk of a strided A1 view) with M a multiple
+// of 32 up to 128 whose tensors fit LDS, and row offsets inside 32 bits.
+template <int D>
+inline bool class_bwd_fits(const AttnArgs& a) {
+    if (a.walk != WALK_DENSE || a.pattern != STRIDED || a.mode != MODE_A1) return false;
+    const int M = a.n;
+    if (M % 32 != 0 || M > 128 || (D == 128 && M > 96)) return false;  // 4 M D + M (M + 8) bf16 within 160 KiB
+    return ((int64_t)(M - 1) * a.ss + D) * 2 < ((int64_t)1 << 32) && a.lse_ss * 64 < ((int64_t)1 << 30);
+}
+
+template <int D, int M>
+hipError_t launch_class_bwd(const AttnArgs& a, const void* q, const void* k, const void* v, const void* dout,
+                            void* dq, void* dk, void* dv, const BwdWorkspace& ws, hipStream_t stream) {
+    hipLaunchKernelGGL((bwd_class_bf16_kernel<D, M>), dim3((unsigned)a.heads, 1, (unsigned)a.batch),
+                       dim3(ClassBwdCfg<D, M>::NT), 0, stream, a, (const uint16_t*)q, (const uint16_t*)k,
+                       (const uint16_t*)v, (const uint16_t*)dout, ws.nlse2, ws.ndelta, (uint16_t*)dq,
+                       (uint16_t*)dk, (uint16_t*)dv);
+    return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_bwd_bf16_d(const AttnArgs& a, const void* q, const void* k, const void* v,
                              const void* o, const void* dout, const float* lse, void* dq,
                              void* dk, void* dv, const BwdWorkspace& ws, hipStream_t stream, int parts) {
+    if ((parts & BWD_DQ) && (parts & BWD_DKDV) && class_bwd_fits<D>(a)) {
+        hipError_t e = hipSuccess;
+        if (parts & BWD_PRE)
+            e = launch_bwd_bf16_d<D>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, BWD_PRE);
+        if (e != hipSuccess) return e;
+        switch (a.n) {
+        case 32: return launch_class_bwd<D, 32>(a, q, k, v, dout, dq, dk, dv, ws, stream);
+        case 64: return launch_class_bwd<D, 64>(a, q, k, v, dout, dq, dk, dv, ws, stream);
+        case 96: return launch_class_bwd<D, 96>(a, q, k, v, dout, dq, dk, dv, ws, stream);
+        default:
+            if constexpr (D != 128) return launch_class_bwd<D, 128>(a, q, k, v, dout, dq, dk, dv, ws, stream);
+            return hipErrorInvalidValue;  // unreachable: class_bwd_fits keeps M <= 96 for D = 128
+        }
+    }
     switch (a.block) {
     case 16: return launch_bwd_bf16<D, 16>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
     case 32: return launch_bwd_bf16<D, 32>(a, q, k, v, o, dout, lse, dq, dk, dv, ws, stream, parts);
