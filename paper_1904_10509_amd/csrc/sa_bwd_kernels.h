@@ -150,14 +150,22 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     __shared__ int items;
     const int tid = threadIdx.x;
     if (g == 0 && tid < kQueues) queue[tid] = 0ull;
-    const int lower_cls = length_class(2);  // a half of non-summary keys meets at most a few blocks
+    // Columns no longer than an l-block (the local columns, and the halves of
+    // non-summary keys) share one class: inside a class items sit in about
+    // the order of their key blocks, so the local columns of one l-block stay
+    // adjacent, run at about the same time on neighbouring workgroups and
+    // share that l-block's Q / dO tiles in L2 (in length classes of their own,
+    // 1 .. l/B blocks long, they ran far apart and each re-read them).
+    const int short_len = a.l / a.block > 2 ? a.l / a.block : 2;
+    const int lower_cls = length_class(short_len);
+    auto cls_of = [&](int len) { return len <= short_len ? lower_cls : length_class(len); };
     const int32_t* cp = a.col_ptr + (int64_t)g * (a.nq + 1);
     int32_t* ord = order + (int64_t)g * 2 * a.nq;
     for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
     __syncthreads();
     for (int kb = tid; kb < a.nq; kb += blockDim.x) {
         const int split = split_column(a, g, kb);
-        if (split == 0 || pair_partner(a, kb) >= 0) atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1);
+        if (split == 0 || pair_partner(a, kb) >= 0) atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1);
         if (split) atomicAdd(&cls_pos[lower_cls], 1);
     }
     __syncthreads();
@@ -177,9 +185,9 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
         // class, the other half the short one
         const int sum_half = split == 1 ? 2 : 1, partner = split ? pair_partner(a, kb) : kb;
         if (split == 0)
-            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
+            ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
         else if (partner >= 0)
-            ord[atomicAdd(&cls_pos[length_class(cp[kb + 1] - cp[kb])], 1)] =
+            ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] =
                 item_code(kb, partner == kb ? sum_half : sum_half + 2);
         if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 3 - sum_half);
     }
