@@ -301,7 +301,8 @@ def decode_bench(args):
 
 
 def probe_lib():
-    """The measurement probe library (libsa_probe.so: the matrix-core peak and clock, the LDS read rate)."""
+    """The measurement probe library (libsa_probe.so: the matrix-core peak and clock, the LDS read rate, the
+    workgroup-to-XCD placement)."""
     import ctypes
     path = os.path.join(ROOT, "paper_1904_10509_amd", "libsa_probe.so")
     if not os.path.exists(path):
@@ -316,7 +317,27 @@ def probe_lib():
     L.sa_probe_lds_launch.restype = ctypes.c_int
     L.sa_probe_lds_launch.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p]
+    L.sa_probe_xcd_map_launch.restype = ctypes.c_int
+    L.sa_probe_xcd_map_launch.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     return L
+
+
+def xcd_map(torch, dev, grids=(768, 2048, 65536)):
+    """For grids of several sizes, how many workgroups L ran on XCD L mod 8
+    (the placement the kernels' work orders assume)."""
+    L = probe_lib()
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+    for g in grids:
+        xcd = torch.zeros(g, dtype=torch.int32, device=dev)
+        sink = torch.empty(g * 256, dtype=torch.float32, device=dev)
+        if L.sa_probe_xcd_map_launch(g, xcd.data_ptr(), sink.data_ptr(), stream.cuda_stream) != 0:
+            raise RuntimeError("probe launch failed")
+        torch.cuda.synchronize()
+        ids = xcd.cpu()
+        want = torch.arange(g, dtype=torch.int32) % 8
+        out[str(g)] = {"on_xcd_index_mod_8": int((ids == want).sum()), "workgroups": g}
+    return out
 
 
 def lds_read_rate(torch, dev, iters=4000, reps=5):
@@ -403,7 +424,7 @@ def main():
                          "long-sequence shapes")
     ap.add_argument("--mfma-peak", action="store_true",
                     help="instead of the metric's line, measure the achievable bf16 matrix-core rate and clock, "
-                         "and the LDS read rate per compute unit")
+                         "the LDS read rate per compute unit and the workgroup-to-XCD placement")
     args = ap.parse_args()
     if args.mfma_peak:
         import torch
@@ -411,7 +432,7 @@ def main():
         torch.cuda.set_device(dev)
         print(json.dumps({"metric": "achievable bf16 MFMA rate (v_mfma_f32_16x16x32_bf16)",
                           "peak_datasheet_tflops": PEAK_BF16_TFLOPS, **mfma_peak(torch, dev),
-                          "lds_read": lds_read_rate(torch, dev)}), flush=True)
+                          "lds_read": lds_read_rate(torch, dev), "xcd_map": xcd_map(torch, dev)}), flush=True)
         return
     if args.decode:
         decode_bench(args)
