@@ -118,8 +118,12 @@ SMALL_CASES = [
     # strided merged and A2 heads with l | n and n / l a multiple of 16 take
     # A2 by residue classes (the band over the layout, then dense causal
     # attention inside each class, merged in place): classes of 16, 32, 48,
-    # 96 and 256 positions (class blocks of 16, 32, 16, 32, 64), l / B of 1, 2,
-    # 4, A2 alone with l < B, d = 32 / 64 / 128, several (batch, head) pairs
+    # 64, 96, 128 and 256 positions (class blocks of 16, 32, 16, 32, 32, 32,
+    # 64), l / B of 1, 2, 4, A2 alone with l < B, d = 32 / 64 / 128, several
+    # (batch, head) pairs.  Classes of 32 to 128 positions (a multiple of 32)
+    # run their backward as one launch per class, except 128 positions at
+    # d = 128 (too large for LDS), which keeps the separate dQ and dK / dV
+    # launches; 16, 48 and 256 positions keep them too.
     (S, MG, 1024, 32, 64, 0, 64, torch.bfloat16, 2, 3),
     (S, MG, 2048, 64, 64, 0, 128, torch.bfloat16, 1, 2),
     (S, MG, 3072, 16, 32, 0, 32, torch.bfloat16, 1, 2),
@@ -128,6 +132,9 @@ SMALL_CASES = [
     (S, A2, 1536, 64, 32, 0, 64, torch.bfloat16, 2, 2),
     (S, A2, 2048, 32, 8, 0, 32, torch.bfloat16, 1, 2),
     (S, A2, 3072, 64, 32, 0, 128, torch.bfloat16, 1, 1),
+    (S, MG, 4096, 32, 32, 0, 64, torch.bfloat16, 1, 2),
+    (S, A2, 4096, 32, 32, 0, 128, torch.bfloat16, 1, 1),
+    (S, A2, 2048, 32, 32, 0, 32, torch.bfloat16, 2, 2),
     # few summary keys per row (c = 1, 2), A2 alone, many heads: the summary
     # columns sum hundreds of large weights, so the dV / dK products take P and
     # dS in two bf16 parts (shared window and a subblock per head; B = 64 with
