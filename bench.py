@@ -118,14 +118,24 @@ def measured_traffic(workload_name):
 
 def copy_calibration(torch, dev):
     """A copy-like elementwise kernel of known size (torch.neg: 256 MiB read,
-    256 MiB written), run when counters are collected so FETCH_SIZE /
-    WRITE_SIZE can be scaled to bytes."""
+    256 MiB written), and a 256 MiB read through direct-to-LDS loads
+    (dma_read_kernel), run when counters are collected so FETCH_SIZE /
+    WRITE_SIZE can be scaled to bytes for either kind of load."""
     src = torch.empty(128 << 20, dtype=torch.bfloat16, device=dev).fill_(1.0)
     dst = torch.empty_like(src)
     for _ in range(3):
         torch.neg(src, out=dst)
     torch.cuda.synchronize()
-    del src, dst
+    # the same 256 MiB read once more through direct-to-LDS loads (the kernels'
+    # tile staging): 1,024 workgroups x 4 waves x 64 KiB
+    L = probe_lib()
+    sink = torch.empty(1024 * 256, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(3):
+        if L.sa_probe_dma_read_launch(1024, 64, src.data_ptr(), sink.data_ptr(), stream.cuda_stream) != 0:
+            raise RuntimeError("probe launch failed")
+    torch.cuda.synchronize()
+    del src, dst, sink
 
 
 def cpu_baseline(workloads, inputs, budget_s=10.0):
@@ -317,6 +327,9 @@ def probe_lib():
     L.sa_probe_lds_launch.restype = ctypes.c_int
     L.sa_probe_lds_launch.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p]
+    L.sa_probe_dma_read_launch.restype = ctypes.c_int
+    L.sa_probe_dma_read_launch.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p]
     L.sa_probe_xcd_map_launch.restype = ctypes.c_int
     L.sa_probe_xcd_map_launch.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     return L

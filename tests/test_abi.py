@@ -308,15 +308,15 @@ def test_bwd_stage_validation(L):
 
 def test_probe_library_exports(L):
     """The measurement probes bench.py loads (matrix-core rate and clock, LDS
-    read rate, XCD placement) are exported and reject invalid launches before
-    touching a GPU."""
+    read rate, XCD placement, direct-to-LDS read calibration) are exported and
+    reject invalid launches before touching a GPU."""
     path = os.path.join(ROOT, "paper_1904_10509_amd", "libsa_probe.so")
     if not os.path.exists(path):
         from paper_1904_10509_amd import build
         build.build()
     P = ctypes.CDLL(path)
     for sym in ("sa_probe_mfma_flop", "sa_probe_mfma_launch", "sa_probe_lds_bytes", "sa_probe_lds_launch",
-                "sa_probe_xcd_map_launch"):
+                "sa_probe_xcd_map_launch", "sa_probe_dma_read_launch"):
         assert hasattr(P, sym), sym
     P.sa_probe_lds_bytes.restype = ctypes.c_double
     P.sa_probe_lds_bytes.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
@@ -330,3 +330,7 @@ def test_probe_library_exports(L):
     P.sa_probe_xcd_map_launch.restype = ctypes.c_int
     P.sa_probe_xcd_map_launch.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     assert P.sa_probe_xcd_map_launch(0, None, None, None) == -1
+    P.sa_probe_dma_read_launch.restype = ctypes.c_int
+    P.sa_probe_dma_read_launch.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p]
+    assert P.sa_probe_dma_read_launch(1, 0, None, None, None) == -1
