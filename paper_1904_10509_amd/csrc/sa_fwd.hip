@@ -291,8 +291,10 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                     }
 #pragma unroll
                     for (int hk = 0; hk < HK; ++hk) {
+                        // a chain of three-way maxima: two instructions per four scores
                         const f32x4 x = s[u][2 * kc + hk];
-                        mloc = fmaxf(mloc, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+                        mloc = fmaxf(fmaxf(mloc, x[0]), x[1]);
+                        mloc = fmaxf(fmaxf(mloc, x[2]), x[3]);
                     }
                 }
                 mloc = max_over_g(mloc);
