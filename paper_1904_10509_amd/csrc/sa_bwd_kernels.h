@@ -675,8 +675,10 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     TileReader<D> rd;
     rd.init(g, r);
     // Claims are made by thread 0, which walks the queues from its own XCD's
-    // on; a claim is (queue << 56 | index), kNoWork once all queues are dry.
+    // on; a claim is (queue << 56 | index), with bit kAscend set when the
+    // column is walked upwards (below), kNoWork once all queues are dry.
     constexpr unsigned long long kNoWork = ~0ull;
+    constexpr unsigned long long kAscend = 1ull << 55;
     int qx = 0, q_left = kQueues;
     uint64_t per_layout = 0;  // item slots taken per (batch, head): the largest item count of a layout
     if (tid == 0) {
@@ -712,6 +714,16 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     // The atomics of all workgroups on one counter are serialised
     // device-wide; with many short columns a claim waits longer than a column
     // takes, hence the fixed orders.  Every mode yields queue-encoded slots.
+    //   In the two serpentine orders the workgroups of a head start each
+    // round at about the same time, since their earlier columns' lengths
+    // sum to about the same.  Columns of even rounds are walked from their
+    // last query block down, of odd rounds from their first up: a column of
+    // length L started at time T then reads query block (last - L + 1) +
+    // (t - T), and T + L is about the same for every workgroup of the
+    // round, so they all read the same Q / dO tile at the same time and it
+    // is fetched into L2 once.  (Downwards in every round, the second
+    // round's walks start at staggered times from the same last block; the
+    // tiles between them outgrow an XCD's L2 and were fetched again by each.)
     uint64_t next_slot = blockIdx.x, sweep = 0;
     auto encode = [&](uint64_t rank, int bh) -> unsigned long long {
         const int x = bh % kQueues;
@@ -732,7 +744,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint64_t p = k * J + ((k & 1) ? J - 1 - j : j);
             const uint64_t i = p / per_layout;  // the i-th head of this XCD
             if (i >= (uint64_t)(bh_count / kQueues)) return kNoWork;
-            return encode(p - i * per_layout, x + kQueues * (int)i);
+            return encode(p - i * per_layout, x + kQueues * (int)i) | ((k & 1) ? kAscend : 0ull);
         }
         if (a.claim_mode == CLAIM_SERPENTINE) {
             const int bh = (int)(blockIdx.x % (uint64_t)bh_count);
@@ -740,7 +752,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint64_t J = (gridDim.x - bh + bh_count - 1) / bh_count;  // workgroups of this head
             const uint64_t k = sweep++;
             const uint64_t rank = k * J + ((k & 1) ? J - 1 - j : j);
-            return rank < per_layout ? encode(rank, bh) : kNoWork;
+            return rank < per_layout ? encode(rank, bh) | ((k & 1) ? kAscend : 0ull) : kNoWork;
         }
         while (q_left > 0) {
             const uint64_t t = atomicAdd(queue + qx, 1ull);
@@ -761,7 +773,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         unsigned long long next = 0ull;
         if (tid == 0) next = claim();  // claimed now, published after the column
         const int x = (int)(item >> 56);
-        const uint64_t t = item & ((1ull << 56) - 1);
+        const bool ascend = (item & kAscend) != 0ull;
+        const uint64_t t = item & (kAscend - 1);
         const int64_t nx = queue_heads(bh_count, x);
         // (the scalar unit holds every index of the column walk; the
         // readfirstlane calls only tell the compiler so)
@@ -844,12 +857,13 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         }
         // strided blocks away from the band are single diagonals (see the step)
         const bool diag_far = PAT == STRIDED && mp.part != PART_A1 && a.l % BLK == 0;
-        // The column is walked from its last query block down: the long
+        // The column is walked from its last query block down (or, in odd
+        // serpentine rounds, from its first up; see the claims): the long
         // columns of a head, started together, then visit the same query
         // blocks at about the same time and share those Q / dO tiles in L2.
         auto query_block = [&](int sidx) {
-            return a.walk == WALK_DENSE ? kb + len - 1 - sidx
-                                        : __builtin_amdgcn_readfirstlane(row_idx[e0 + len - 1 - sidx]);
+            const int e = ascend ? sidx : len - 1 - sidx;
+            return a.walk == WALK_DENSE ? kb + e : __builtin_amdgcn_readfirstlane(row_idx[e0 + e]);
         };
         auto load_block = [&](int qb, int stage) {
             const int64_t qbase = base + (int64_t)qb * BLK * a.ss;
