@@ -140,6 +140,28 @@ __device__ inline int pair_partner(const AttnArgs& a, int kb) {
     return kb + step < a.nq ? kb + step : kb;
 }
 
+// In the fixed pattern with B = 64 and l a multiple of 128, the short
+// columns of one l-block (whole blocks attended only inside it, and the
+// other-key halves of split blocks) form one item, kind kGroupKind, coded by
+// the l-block's first key block: one workgroup walks them one after the
+// other, so the l-block's Q / dO tiles are fetched once and then hit in L2
+// (as separate items they ran on different workgroups at different times
+// and were fetched again).  Returns the key blocks per l-block, or 0 where
+// columns are not grouped.
+constexpr int kGroupKind = 5;
+__device__ inline int group_blocks(const AttnArgs& a) {
+    return a.pattern == FIXED && a.block == 64 && a.l % 128 == 0 ? a.l / 64 : 0;
+}
+// The item kind key block kb takes inside its l-block's group (0: the whole
+// block, 1 / 2: its lower / upper 32 keys), or -1 when it has no short
+// column (its column is walked as an item of its own).  cp: layout g's
+// column pointers.
+__device__ inline int group_member(const AttnArgs& a, int g, int kb, const int32_t* cp) {
+    const int split = split_column(a, g, kb);
+    if (split) return split;  // the other half of a split block is short
+    return cp[kb + 1] - cp[kb] <= group_blocks(a) ? 0 : -1;
+}
+
 // Workgroup g < n_layouts of the pre kernel: layout g's items (2 nq slots)
 // ordered by length class, empty slots last (order inside a class is
 // arbitrary; it only affects scheduling), and its item count in items[g].
@@ -163,10 +185,29 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     int32_t* ord = order + (int64_t)g * 2 * a.nq;
     for (int i = tid; i < kLengthClasses; i += blockDim.x) cls_pos[i] = 0;
     __syncthreads();
+    const int G = group_blocks(a);
+    // a group's class follows the sum of its members' walks (a split block's
+    // short half walks at most the l-block's blocks)
+    auto group_len = [&](int kb0) {
+        int total = 0;
+        for (int kb = kb0; kb < kb0 + G && kb < a.nq; ++kb)
+            if (group_member(a, g, kb, cp) >= 0) total += min(cp[kb + 1] - cp[kb], G);
+        return total;
+    };
+    // (the counting pass takes the same decisions as the placing pass below)
     for (int kb = tid; kb < a.nq; kb += blockDim.x) {
-        const int split = split_column(a, g, kb);
-        if (split == 0 || pair_partner(a, kb) >= 0) atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1);
-        if (split) atomicAdd(&cls_pos[lower_cls], 1);
+        const int split = split_column(a, g, kb), partner = split ? pair_partner(a, kb) : kb;
+        const bool member = G && group_member(a, g, kb, cp) >= 0;
+        if (split == 0) {
+            if (!member) atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1);
+        } else if (partner >= 0) {
+            atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1);
+        }
+        if (!G && split) atomicAdd(&cls_pos[lower_cls], 1);
+        if (G && kb % G == 0) {
+            const int total = group_len(kb);
+            if (total > 0) atomicAdd(&cls_pos[cls_of(total)], 1);
+        }
     }
     __syncthreads();
     if (tid == 0) {
@@ -182,14 +223,20 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
     for (int kb = tid; kb < a.nq; kb += blockDim.x) {
         const int split = split_column(a, g, kb);
         // the summary half (alone or with its partner) takes the column's
-        // class, the other half the short one
+        // class, the other half the short one (or its l-block's group)
         const int sum_half = split == 1 ? 2 : 1, partner = split ? pair_partner(a, kb) : kb;
-        if (split == 0)
-            ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
-        else if (partner >= 0)
+        const bool member = G && group_member(a, g, kb, cp) >= 0;
+        if (split == 0) {
+            if (!member) ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
+        } else if (partner >= 0) {
             ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] =
                 item_code(kb, partner == kb ? sum_half : sum_half + 2);
-        if (split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 3 - sum_half);
+        }
+        if (!G && split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 3 - sum_half);
+        if (G && kb % G == 0) {
+            const int total = group_len(kb);
+            if (total > 0) ord[atomicAdd(&cls_pos[cls_of(total)], 1)] = item_code(kb, kGroupKind);
+        }
     }
     for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
     if (tid == 0) items_out[g] = items;
@@ -765,32 +812,53 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     if (tid == 0) sItem[0] = claim();
     __syncthreads();
     // Every wave leaves the loop at the same claim: the claim is shared
-    // through LDS and is kNoWork once every queue has run dry.
-    for (int it = 0;; ++it) {
-        const uint64_t item = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sItem[it & 1] >> 32)) << 32) |
-                              __builtin_amdgcn_readfirstlane((uint32_t)sItem[it & 1]);
-        if (item == kNoWork) break;
-        unsigned long long next = 0ull;
-        if (tid == 0) next = claim();  // claimed now, published after the column
-        const int x = (int)(item >> 56);
-        const bool ascend = (item & kAscend) != 0ull;
-        const uint64_t t = item & (kAscend - 1);
-        const int64_t nx = queue_heads(bh_count, x);
-        // (the scalar unit holds every index of the column walk; the
-        // readfirstlane calls only tell the compiler so)
-        const int rank = __builtin_amdgcn_readfirstlane((int)(t / (uint64_t)nx));  // position in the length order
-        const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
-        const int h = bh % a.heads, b = bh / a.heads;
-        const int lay = head_layout(a, h);
-        const int32_t code = a.walk != WALK_LAYOUT ? item_code(rank, 0)
-                                                   : __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
-        if (code < 0) {  // an empty slot (a layout with fewer items than another)
-            if (tid == 0) sItem[(it + 1) & 1] = next;
-            __syncthreads();
-            continue;
+    // through LDS and is kNoWork once every queue has run dry.  A group item
+    // takes one pass of the loop per key block of its l-block (grp_kb ..
+    // grp_end - 1 still to come, wave-uniform); the claim after it is made
+    // when the group starts and published after its last block.
+    int ci = 0, grp_kb = 0, grp_end = 0;
+    int h = 0, b = 0, lay = 0;
+    bool ascend = false;
+    unsigned long long next = 0ull;
+    for (;;) {
+        int kb = 0, kind = -1;
+        if (grp_kb < grp_end) {
+            kb = grp_kb++;
+            kind = __builtin_amdgcn_readfirstlane(group_member(a, lay, kb, col_ptr + (int64_t)lay * (a.nq + 1)));
+        } else {
+            const uint64_t item = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sItem[ci & 1] >> 32)) << 32) |
+                                  __builtin_amdgcn_readfirstlane((uint32_t)sItem[ci & 1]);
+            if (item == kNoWork) break;
+            if (tid == 0) next = claim();  // claimed now, published after the column (or group)
+            const int x = (int)(item >> 56);
+            ascend = (item & kAscend) != 0ull;
+            const uint64_t t = item & (kAscend - 1);
+            const int64_t nx = queue_heads(bh_count, x);
+            // (the scalar unit holds every index of the column walk; the
+            // readfirstlane calls only tell the compiler so)
+            const int rank = __builtin_amdgcn_readfirstlane((int)(t / (uint64_t)nx));  // position in the length order
+            const int bh = __builtin_amdgcn_readfirstlane(x + kQueues * (int)(t - (uint64_t)rank * nx));
+            h = bh % a.heads;
+            b = bh / a.heads;
+            lay = head_layout(a, h);
+            const int32_t code = a.walk != WALK_LAYOUT
+                                     ? item_code(rank, 0)
+                                     : __builtin_amdgcn_readfirstlane(order[(int64_t)lay * 2 * a.nq + rank]);
+            // code < 0: an empty slot (a layout with fewer items than another)
+            if (code >= 0) {
+                kb = code & ((1 << kItemShift) - 1);
+                kind = kHalves ? code >> kItemShift : 0;
+                if (kHalves && kind == kGroupKind) {
+                    grp_kb = kb + 1;
+                    grp_end = min(kb + group_blocks(a), a.nq);
+                    kind = __builtin_amdgcn_readfirstlane(
+                        group_member(a, lay, kb, col_ptr + (int64_t)lay * (a.nq + 1)));
+                }
+            }
         }
-        const int kb = code & ((1 << kItemShift) - 1);
-        const int kind = kHalves ? code >> kItemShift : 0;
+        // kind < 0: an empty slot, or a block of a group whose column is long
+        // (an item of its own)
+        if (kind >= 0) {
         // In a pair the first half of the waves takes the summary half of kb,
         // the second half that of kb + l / 64, each for all queries of a block;
         // a single half is shared by all waves: with four waves of 16 keys, two
@@ -1171,7 +1239,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 *dkp = pack_bf16x4_bits(xk);
             }
         }
-        if (tid == 0) sItem[(it + 1) & 1] = next;
+        }  // kind >= 0
+        if (grp_kb >= grp_end) {
+            if (tid == 0) sItem[(ci + 1) & 1] = next;
+            ++ci;
+        }
         // the ring is free again and the next claim is visible to every wave
         __syncthreads();
     }
