@@ -102,9 +102,11 @@ __device__ inline int64_t queue_heads(int64_t bh_count, int x) {
 }
 
 // Items of the dK / dV schedule: key block kb whole (kind 0), one 32-key
-// half of a 64-wide block (kind 1: keys 0..31, kind 2: keys 32..63), or a
+// half of a 64-wide block (kind 1: keys 0..31, kind 2: keys 32..63), a
 // pair of such halves (kind 3: keys 0..31, kind 4: keys 32..63, of kb and of
-// kb + l / 64); -1 is an empty slot.  kb < 2^27 (n < 2^31, B >= 16).
+// kb + l / 64), or the short columns of the l-block that starts at kb
+// (kind 5, kGroupKind below); -1 is an empty slot.  kb < 2^27 (n < 2^31,
+// B >= 16).
 constexpr int kItemShift = 28;
 __device__ inline int32_t item_code(int kb, int kind) { return kb | (kind << kItemShift); }
 
@@ -162,8 +164,9 @@ __device__ inline int group_member(const AttnArgs& a, int g, int kb, const int32
     return cp[kb + 1] - cp[kb] <= group_blocks(a) ? 0 : -1;
 }
 
-// Workgroup g < n_layouts of the pre kernel: layout g's items (2 nq slots)
-// ordered by length class, empty slots last (order inside a class is
+// Workgroup g < n_layouts of the row-statistics step (the pre kernel, or
+// the dQ kernel where it computes the statistics): layout g's items (2 nq
+// slots) ordered by length class, empty slots last (order inside a class is
 // arbitrary; it only affects scheduling), and its item count in items[g].
 // Workgroup 0 also empties the queues.
 __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* queue, int32_t* items_out,
@@ -672,7 +675,8 @@ struct DkvCfg {
     // keys per wave.  (32 keys per wave, two key groups sharing every Q / dO
     // operand read, needs about 290 registers: at one wave per SIMD it made the
     // fixed backward at n = 65,536 slower, 1.68 against 1.45 ms, and at two
-    // with spills 2.10 ms; the half and pair logic below handles both widths.)
+    // with spills 2.10 ms; at two with the step body free of spills, 2.80
+    // against 2.18 ms; the half and pair logic below handles both widths.)
     static constexpr int KW = 16;
     static constexpr int KBW = KW / 16;         // 16-key blocks per wave
     static constexpr int NW = BLK / KW;         // waves
