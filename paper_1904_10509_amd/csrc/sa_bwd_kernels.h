@@ -1145,12 +1145,13 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     }
                     // (SPLIT: every transposed operand is kept for the low parts,
                     // issued after every high part so that no product waits on the
-                    // one just issued; otherwise each is read just before its use)
-                    constexpr int kKeep = SPLIT ? C::DB : 1;
+                    // one just issued; otherwise each is read one d-block ahead of
+                    // its products, so that the products do not wait on the LDS: the
+                    // fixed backward at n = 65,536 took 4% less than with each read
+                    // just before its use)
+                    constexpr int kKeep = SPLIT ? C::DB : 2;
                     bf16x8 oT[kKeep], qT[kKeep];
-#pragma unroll
-                    for (int db = 0; db < C::DB; ++db) {
-                        const int x = SPLIT ? db : 0;
+                    auto read_tr = [&](int db, int x) {
                         if constexpr (BLK >= 32) {
                             oT[x] = rd.tr(tO, qc * 32, qc * 32 + 16, db);
                             qT[x] = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
@@ -1158,6 +1159,13 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                             oT[x] = rd.tr_half(tO, 0, db);
                             qT[x] = rd.tr_half(tQ, 0, db);
                         }
+                    };
+                    if constexpr (!SPLIT) read_tr(0, 0);
+#pragma unroll
+                    for (int db = 0; db < C::DB; ++db) {
+                        const int x = SPLIT ? db : (db & 1);
+                        if constexpr (SPLIT) read_tr(db, db);
+                        else if (db + 1 < C::DB) read_tr(db + 1, (db + 1) & 1);
 #pragma unroll
                         for (int kbw = 0; kbw < C::KBW; ++kbw) {
                             if (cls[kbw][qc] == CHUNK_NONE) continue;
@@ -1532,10 +1540,18 @@ bwd_class_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t
             }
         }
         const bf16x8 pb = pack_bf16x8(p[0], p[1]), sb = pack_bf16x8(ds[0], ds[1]);
+        // transposed operands one d-block ahead of their products
+        bf16x8 oT[2], qT[2];
+        oT[0] = rd.tr(sO, 32 * qc, 32 * qc + 16, 0);
+        qT[0] = rd.tr(sQ, 32 * qc, 32 * qc + 16, 0);
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) {
-            dvacc[db] = mfma_16x16x32(rd.tr(sO, 32 * qc, 32 * qc + 16, db), pb, dvacc[db]);
-            dkacc[db] = mfma_16x16x32(rd.tr(sQ, 32 * qc, 32 * qc + 16, db), sb, dkacc[db]);
+            if (db + 1 < C::DB) {
+                oT[(db + 1) & 1] = rd.tr(sO, 32 * qc, 32 * qc + 16, db + 1);
+                qT[(db + 1) & 1] = rd.tr(sQ, 32 * qc, 32 * qc + 16, db + 1);
+            }
+            dvacc[db] = mfma_16x16x32(oT[db & 1], pb, dvacc[db]);
+            dkacc[db] = mfma_16x16x32(qT[db & 1], sb, dkacc[db]);
         }
         // dS^T row j, queries 32 qc + 16 hq + 4 g .. +3
         *reinterpret_cast<uint2*>(&sST[j * C::MP + 32 * qc + 4 * g]) = pack_bf16x4_bits(ds[0]);
@@ -1572,9 +1588,13 @@ bwd_class_bf16_kernel(AttnArgs a, const uint16_t* __restrict__ q, const uint16_t
         const uint16_t* t = &sST[(32 * kc + 4 * g + r / 4) * C::MP + q0 + 4 * (r & 3)];
         const u32x2 lo = ld_tr16(t), hi = ld_tr16(t + 16 * C::MP);
         const bf16x8 dsb = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+        bf16x8 kT[2];  // one d-block ahead of its product
+        kT[0] = rd.tr(sK, 32 * kc, 32 * kc + 16, 0);
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
-            dqacc[db] = mfma_16x16x32(rd.tr(sK, 32 * kc, 32 * kc + 16, db), dsb, dqacc[db]);
+        for (int db = 0; db < C::DB; ++db) {
+            if (db + 1 < C::DB) kT[(db + 1) & 1] = rd.tr(sK, 32 * kc, 32 * kc + 16, db + 1);
+            dqacc[db] = mfma_16x16x32(kT[db & 1], dsb, dqacc[db]);
+        }
     }
     uint16_t* drow = dq + base + (int64_t)(q0 + r) * a.ss;
 #pragma unroll
