@@ -1108,6 +1108,28 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                             ds[kbw][hq] = dpacc;
                         }
                     }
+                    // (SPLIT: every transposed operand is kept for the low parts,
+                    // issued after every high part so that no product waits on the
+                    // one just issued; otherwise each is read one d-block ahead of
+                    // its products, in the fixed pattern the first before the
+                    // exponentials, so that the products do not wait on the LDS: the
+                    // fixed backward at n = 65,536 took 4% and then another 1.5% less
+                    // than with each read just before its use.  The strided kernels
+                    // read the first after the exponentials: earlier, its registers
+                    // made them spill.)
+                    constexpr int kKeep = SPLIT ? C::DB : 2;
+                    bf16x8 oT[kKeep], qT[kKeep];
+                    auto read_tr = [&](int db, int x) {
+                        if constexpr (BLK >= 32) {
+                            oT[x] = rd.tr(tO, qc * 32, qc * 32 + 16, db);
+                            qT[x] = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
+                        } else {
+                            oT[x] = rd.tr_half(tO, 0, db);
+                            qT[x] = rd.tr_half(tQ, 0, db);
+                        }
+                    };
+                    constexpr bool kEarly = !SPLIT && PAT == FIXED;
+                    if constexpr (kEarly) read_tr(0, 0);
                     bf16x8 pb[C::KBW], sb[C::KBW];
                     bf16x8 pbl[C::KBW], sbl[C::KBW];  // low parts (SPLIT)
 #pragma unroll
@@ -1143,24 +1165,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                         if (cls[kbw][qc] == CHUNK_ALL) chunk(std::false_type{});
                         else if (cls[kbw][qc] == CHUNK_PART) chunk(std::true_type{});
                     }
-                    // (SPLIT: every transposed operand is kept for the low parts,
-                    // issued after every high part so that no product waits on the
-                    // one just issued; otherwise each is read one d-block ahead of
-                    // its products, so that the products do not wait on the LDS: the
-                    // fixed backward at n = 65,536 took 4% less than with each read
-                    // just before its use)
-                    constexpr int kKeep = SPLIT ? C::DB : 2;
-                    bf16x8 oT[kKeep], qT[kKeep];
-                    auto read_tr = [&](int db, int x) {
-                        if constexpr (BLK >= 32) {
-                            oT[x] = rd.tr(tO, qc * 32, qc * 32 + 16, db);
-                            qT[x] = rd.tr(tQ, qc * 32, qc * 32 + 16, db);
-                        } else {
-                            oT[x] = rd.tr_half(tO, 0, db);
-                            qT[x] = rd.tr_half(tQ, 0, db);
-                        }
-                    };
-                    if constexpr (!SPLIT) read_tr(0, 0);
+                    if constexpr (!SPLIT && !kEarly) read_tr(0, 0);
 #pragma unroll
                     for (int db = 0; db < C::DB; ++db) {
                         const int x = SPLIT ? db : (db & 1);
