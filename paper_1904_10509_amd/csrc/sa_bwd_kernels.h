@@ -305,7 +305,8 @@ struct DqCfg {
     static constexpr int KC = (BLK + 31) / 32;
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // K / V ring stages
-    static constexpr int WAVES_PER_EU = RW == 16 ? 3 : 2;
+    // (d = 128 with 16-key blocks spilled 16 to 30 registers at three waves)
+    static constexpr int WAVES_PER_EU = RW == 16 && !(D == 128 && BLK == 16) ? 3 : 2;
 };
 
 // SPLIT (see split_products): the row is walked twice.  The first walk
@@ -686,7 +687,8 @@ struct DkvCfg {
     static constexpr int QC = (BLK + 31) / 32;  // 32-query chunks (contraction over queries)
     static constexpr int DB = D / 16;
     static constexpr int NS = 2;  // Q / dO (and row statistics) ring stages
-    static constexpr int WAVES_PER_EU = KW == 32 ? 2 : 3;
+    // (d = 128 with 16-query blocks spilled 51 to 90 registers at three waves)
+    static constexpr int WAVES_PER_EU = KW == 32 || (D == 128 && BLK == 16) ? 2 : 3;
 };
 
 // SPLIT: P and dS enter the dV and dK products as a high and a low bf16 part

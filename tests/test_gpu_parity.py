@@ -75,6 +75,9 @@ SMALL_CASES = [
     (F, A2, 256, 16, 64, 1, 32, torch.bfloat16, 1, 1),
     (F, MG, 256, 64, 64, 64, 64, torch.bfloat16, 1, 1),
     (F, IL, 512, 16, 48, 12, 64, torch.bfloat16, 1, 2),
+    # d = 128 with 16-wide blocks (two waves per SIMD in the backward)
+    (S, MG, 256, 16, 32, 0, 128, torch.bfloat16, 1, 2),
+    (F, IL, 256, 16, 64, 16, 128, torch.bfloat16, 1, 2),
     # fixed, B = 64, c = 32: rows whose far blocks pair up (even and odd counts)
     (F, A2, 1024, 64, 128, 32, 64, torch.bfloat16, 1, 2),
     (F, MG, 512, 64, 64, 32, 64, torch.bfloat16, 1, 1),
