@@ -84,6 +84,10 @@ SMALL_CASES = [
     (F, IL, 1024, 64, 128, 32, 128, torch.bfloat16, 2, 2),
     # an odd number of summary key blocks: one upper half left without a partner
     (F, MG, 768, 64, 256, 32, 64, torch.bfloat16, 1, 2),
+    # the short columns of an l-block walked as one dK / dV item: groups of 6
+    # and 8 key blocks (l = 384, 512), with and without summary pairs
+    (F, MG, 1536, 64, 384, 32, 64, torch.bfloat16, 1, 2),
+    (F, A2, 2048, 64, 512, 32, 64, torch.bfloat16, 1, 2),
     # d = 32 with pairs and half items; l = 96 (blocks straddle l-blocks): half
     # items without pairs
     (F, MG, 512, 64, 128, 32, 32, torch.bfloat16, 1, 2),
