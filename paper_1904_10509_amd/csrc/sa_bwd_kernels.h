@@ -166,9 +166,12 @@ __device__ inline int group_member(const AttnArgs& a, int g, int kb, const int32
 
 // Workgroup g < n_layouts of the row-statistics step (the pre kernel, or
 // the dQ kernel where it computes the statistics): layout g's items (2 nq
-// slots) ordered by length class, empty slots last (order inside a class is
-// arbitrary; it only affects scheduling), and its item count in items[g].
-// Workgroup 0 also empties the queues.
+// slots) ordered by length class, empty slots last, and its item count in
+// items[g].  Inside a class the items follow their key blocks (and a block's
+// items the order below), the same on every run: in the serpentine orders
+// an item's place decides which round walks its column and so the
+// direction, and with it the rounding of dK and dV.  Workgroup 0 also
+// empties the queues.
 __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* queue, int32_t* items_out,
                                int32_t* order) {
     __shared__ int cls_pos[kLengthClasses];
@@ -223,22 +226,69 @@ __device__ void build_schedule(const AttnArgs& a, int g, unsigned long long* que
         items = run;
     }
     __syncthreads();
-    for (int kb = tid; kb < a.nq; kb += blockDim.x) {
-        const int split = split_column(a, g, kb);
-        // the summary half (alone or with its partner) takes the column's
-        // class, the other half the short one (or its l-block's group)
-        const int sum_half = split == 1 ? 2 : 1, partner = split ? pair_partner(a, kb) : kb;
-        const bool member = G && group_member(a, g, kb, cp) >= 0;
-        if (split == 0) {
-            if (!member) ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] = item_code(kb, 0);
-        } else if (partner >= 0) {
-            ord[atomicAdd(&cls_pos[cls_of(cp[kb + 1] - cp[kb])], 1)] =
-                item_code(kb, partner == kb ? sum_half : sum_half + 2);
-        }
-        if (!G && split) ord[atomicAdd(&cls_pos[lower_cls], 1)] = item_code(kb, 3 - sum_half);
-        if (G && kb % G == 0) {
-            const int total = group_len(kb);
-            if (total > 0) ord[atomicAdd(&cls_pos[cls_of(total)], 1)] = item_code(kb, kGroupKind);
+    // Placing pass, by wave 0 alone: 64 key blocks at a time, in order, each
+    // lane holding block kb's up to three items (code, class; class -1: none).
+    // The items of one class in the chunk go to consecutive places ranked by
+    // (lane, item), a stable counting sort.
+    if (tid < 64) {
+        const int lane = tid;
+        const uint64_t below = lane == 0 ? 0ull : ~0ull >> (64 - lane);
+        for (int kb0 = 0; kb0 < a.nq; kb0 += 64) {
+            const int kb = kb0 + lane;
+            int32_t code[3] = {-1, -1, -1};
+            int cls[3] = {-1, -1, -1};
+            if (kb < a.nq) {
+                const int split = split_column(a, g, kb);
+                // the summary half (alone or with its partner) takes the
+                // column's class, the other half the short one (or its
+                // l-block's group)
+                const int sum_half = split == 1 ? 2 : 1, partner = split ? pair_partner(a, kb) : kb;
+                const bool member = G && group_member(a, g, kb, cp) >= 0;
+                if (split == 0) {
+                    if (!member) {
+                        code[0] = item_code(kb, 0);
+                        cls[0] = cls_of(cp[kb + 1] - cp[kb]);
+                    }
+                } else if (partner >= 0) {
+                    code[0] = item_code(kb, partner == kb ? sum_half : sum_half + 2);
+                    cls[0] = cls_of(cp[kb + 1] - cp[kb]);
+                }
+                if (!G && split) {
+                    code[1] = item_code(kb, 3 - sum_half);
+                    cls[1] = lower_cls;
+                }
+                if (G && kb % G == 0) {
+                    const int total = group_len(kb);
+                    if (total > 0) {
+                        code[2] = item_code(kb, kGroupKind);
+                        cls[2] = cls_of(total);
+                    }
+                }
+            }
+            uint64_t left[3];
+#pragma unroll
+            for (int i = 0; i < 3; ++i) left[i] = __ballot(cls[i] >= 0);
+            while (left[0] | left[1] | left[2]) {
+                // the next class: that of the first lane still holding an item
+                const int i0 = left[0] ? 0 : (left[1] ? 1 : 2);
+                const int c0 = i0 == 0 ? cls[0] : (i0 == 1 ? cls[1] : cls[2]);
+                const int c = __builtin_amdgcn_readlane(c0, __builtin_ctzll(left[i0]));
+                uint64_t m[3];
+                int before = 0, count = 0;
+#pragma unroll
+                for (int i = 0; i < 3; ++i) {
+                    m[i] = __ballot(cls[i] == c);
+                    before += __popcll(m[i] & below);
+                    count += __popcll(m[i]);
+                    left[i] &= ~m[i];
+                }
+                const int base = cls_pos[c];
+                int pos = base + before;
+#pragma unroll
+                for (int i = 0; i < 3; ++i)
+                    if (cls[i] == c) ord[pos++] = code[i];
+                if (lane == 0) cls_pos[c] = base + count;
+            }
         }
     }
     for (int i = items + tid; i < 2 * a.nq; i += blockDim.x) ord[i] = -1;
