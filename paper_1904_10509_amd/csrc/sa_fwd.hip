@@ -336,12 +336,13 @@ fwd_bf16_kernel(AttnArgs a, const int32_t* __restrict__ row_ptr, const int32_t* 
                 const float alpha = exp2_fast((m_run[u] - m_ref) * c2);
                 l_run[u] = fmaf(l_run[u], alpha, psum);
                 m_run[u] = m_new;
-                // O is rescaled only in the blocks where some row's maximum grew
-                // (a wave-uniform branch); everywhere else alpha is exactly 1.
-                if (__builtin_amdgcn_ballot_w64(grew) != 0ull) {
+                // O is rescaled on every step: where no row's maximum grew alpha
+                // is exactly 1 and O keeps its bits.  (Behind a branch on the
+                // growth the compiler kept O in other registers on the two sides
+                // and copied it back every step, which cost more than the
+                // multiplies: n = 1,048,576 forward 2.94 -> 2.90 ms.)
 #pragma unroll
-                    for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
-                }
+                for (int db = 0; db < C::DB; ++db) oacc[u][db] *= alpha;
             }
 
             // O^T += V^T P^T
