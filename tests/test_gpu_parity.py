@@ -136,6 +136,10 @@ SMALL_CASES = [
     (S, MG, 3072, 16, 32, 0, 32, torch.bfloat16, 1, 2),
     (S, MG, 4096, 16, 16, 0, 64, torch.bfloat16, 1, 2),
     (S, MG, 8192, 32, 128, 0, 64, torch.bfloat16, 1, 2),
+    # band columns of l / B + 1 = 9 blocks: the band's dK / dV takes one
+    # workgroup per column instead of the persistent grid
+    (S, MG, 8192, 64, 512, 0, 64, torch.bfloat16, 1, 2),
+    (S, MG, 4096, 16, 128, 0, 64, torch.bfloat16, 1, 2),
     (S, A2, 1536, 64, 32, 0, 64, torch.bfloat16, 2, 2),
     (S, A2, 2048, 32, 8, 0, 32, torch.bfloat16, 1, 2),
     (S, A2, 3072, 64, 32, 0, 128, torch.bfloat16, 1, 1),
