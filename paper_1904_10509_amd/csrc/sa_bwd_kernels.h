@@ -1409,12 +1409,16 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         const int64_t slots =
             split ? resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE, PAT == FIXED>>(DkvCfg<D, BLK, PAT>::NT)
                   : resident_workgroups<bwd_dkdv_bf16_kernel<D, BLK, PAT, MODE, false>>(DkvCfg<D, BLK, PAT>::NT);
-        // A band walk of long columns takes one workgroup per column instead
-        // of the persistent grid: the hardware then overlaps one column's
-        // register loads with the others' steps (l / B + 1 = 17 blocks at
-        // n = 1,048,576: backward 8.71 -> 8.53 ms; with 3 blocks, at
-        // n = 12,288, the persistent grid stays 2% faster).
-        const bool per_column = a.walk == WALK_BAND && a.l / BLK + 1 >= 8;
+        // A band walk of long columns, and a dense walk (the residue classes)
+        // of at least 8 blocks, take one workgroup per column instead of the
+        // persistent grid: the hardware then overlaps one column's register
+        // loads with the others' steps (n = 1,048,576: the band's 17-block
+        // columns, backward 8.71 -> 8.53 ms; the classes' 16 blocks, 8.39 ->
+        // 8.28 ms; with 3-block band columns, at n = 12,288, the persistent
+        // grid stays 2% faster).  Under CLAIM_XCD_SERPENTINE such a grid is
+        // the first round alone: the columns of a class unit take consecutive
+        // places on one XCD.
+        const bool per_column = (a.walk == WALK_BAND && a.l / BLK + 1 >= 8) || (a.walk == WALK_DENSE && a.nq >= 8);
         const unsigned qgrid = (unsigned)(slots > 0 && slots < items && !per_column
                                               ? slots
                                               : (items < (1ll << 31) ? items : (1ll << 31) - 1));

@@ -140,6 +140,10 @@ SMALL_CASES = [
     # workgroup per column instead of the persistent grid
     (S, MG, 8192, 64, 512, 0, 64, torch.bfloat16, 1, 2),
     (S, MG, 4096, 16, 128, 0, 64, torch.bfloat16, 1, 2),
+    # classes of 512 and 1,024 positions (8 and 16 class blocks of 64): their
+    # dK / dV take one workgroup per column too
+    (S, MG, 8192, 16, 16, 0, 64, torch.bfloat16, 1, 2),
+    (S, A2, 16384, 16, 16, 0, 32, torch.bfloat16, 1, 1),
     (S, A2, 1536, 64, 32, 0, 64, torch.bfloat16, 2, 2),
     (S, A2, 2048, 32, 8, 0, 32, torch.bfloat16, 1, 2),
     (S, A2, 3072, 64, 32, 0, 128, torch.bfloat16, 1, 1),
