@@ -26,19 +26,15 @@
 // device, the pre kernel sorts the key blocks of each layout by column length
 // (longest first, so the long columns of a head start together and walk the
 // same Q / dO tiles at about the same time), and each workgroup takes its
-// columns in one of the orders chosen per call (see the kernel's claims):
+// columns in one of three orders chosen per call:
 //   - serpentine per head (fixed pattern, a few workgroups per head): one
 //     head per workgroup, ranks j, 2J - 1 - j, 2J + j, ... over the head's J
-//     workgroups, which evens out the sums of the sorted lengths; with at
-//     most 8 heads only the first round so, the rest from one counter per
-//     head as workgroups come free;
+//     workgroups, which evens out the sums of the sorted lengths;
 //   - round-robin over the rank-major order (strided pattern, short columns);
-//   - head by head on each XCD (the residue classes' dense walks);
 //   - atomic counters, one queue per XCD holding the heads bh = x (mod 8),
 //     with stealing once a queue is dry (the remaining cases).
-// Claims on one counter are serialised across the device and, with short
-// columns, take longer than the columns, hence the fixed orders; the
-// per-head counters serve a few hundred claims over a long launch.
+// The first two use no atomics: claims on one counter are serialised across
+// the device and, with short columns, take longer than the columns.
 // The dq kernel repeats the S and dP products of the dkdv kernel; those two
 // extra products per block are the price of having no reduction across
 // workgroups.
@@ -786,7 +782,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     // column is walked upwards (below), kNoWork once all queues are dry.
     constexpr unsigned long long kNoWork = ~0ull;
     constexpr unsigned long long kAscend = 1ull << 55;
-    constexpr unsigned long long kDeferred = ~0ull - 1;
     int qx = 0, q_left = kQueues;
     uint64_t per_layout = 0;  // item slots taken per (batch, head): the largest item count of a layout
     if (tid == 0) {
@@ -811,15 +806,6 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     //     takes that head's ranks in serpentine order over the J workgroups of
     //     the head (j, 2J - 1 - j, 2J + j, ...), which evens out the sums of
     //     sorted column lengths, with no atomics;
-    //   CLAIM_SERPENTINE_TAIL: the first round as CLAIM_SERPENTINE (place j
-    //     of its head), every later slot from the head's counter (queue[bh],
-    //     at most kQueues heads), longest first, claimed only when the
-    //     workgroup is free: after a column, once it is walked (after a
-    //     group of short columns, at its start).  The workgroup with the
-    //     head's longest column then takes nothing after it, where the
-    //     serpentine rounds gave it three short-column items; the slots after
-    //     the first round are walked upwards whoever takes them, so the
-    //     results do not depend on which workgroup does;
     //   CLAIM_XCD_SERPENTINE: workgroup w (on XCD x = w mod 8, the j-th of
     //     its J there) serves the heads bh = x (mod 8), head by head with
     //     every column of a head, longest first, before the next: places
@@ -863,15 +849,11 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             if (i >= (uint64_t)(bh_count / kQueues)) return kNoWork;
             return encode(p - i * per_layout, x + kQueues * (int)i) | ((k & 1) ? kAscend : 0ull);
         }
-        if (a.claim_mode == CLAIM_SERPENTINE || a.claim_mode == CLAIM_SERPENTINE_TAIL) {
+        if (a.claim_mode == CLAIM_SERPENTINE) {
             const int bh = (int)(blockIdx.x % (uint64_t)bh_count);
             const uint64_t j = blockIdx.x / (uint64_t)bh_count;
             const uint64_t J = (gridDim.x - bh + bh_count - 1) / bh_count;  // workgroups of this head
             const uint64_t k = sweep++;
-            if (a.claim_mode == CLAIM_SERPENTINE_TAIL && k > 0) {
-                const uint64_t rank = J + atomicAdd(queue + bh, 1ull);
-                return rank < per_layout ? encode(rank, bh) | kAscend : kNoWork;
-            }
             const uint64_t rank = k * J + ((k & 1) ? J - 1 - j : j);
             return rank < per_layout ? encode(rank, bh) | ((k & 1) ? kAscend : 0ull) : kNoWork;
         }
@@ -903,7 +885,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint64_t item = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(sItem[ci & 1] >> 32)) << 32) |
                                   __builtin_amdgcn_readfirstlane((uint32_t)sItem[ci & 1]);
             if (item == kNoWork) break;
-            bool group_item = false;
+            if (tid == 0) next = claim();  // claimed now, published after the column (or group)
             const int x = (int)(item >> 56);
             ascend = (item & kAscend) != 0ull;
             const uint64_t t = item & (kAscend - 1);
@@ -923,18 +905,12 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                 kb = code & ((1 << kItemShift) - 1);
                 kind = kHalves ? code >> kItemShift : 0;
                 if (kHalves && kind == kGroupKind) {
-                    group_item = true;
                     grp_kb = kb + 1;
                     grp_end = min(kb + group_blocks(a), a.nq);
                     kind = __builtin_amdgcn_readfirstlane(
                         group_member(a, lay, kb, col_ptr + (int64_t)lay * (a.nq + 1)));
                 }
             }
-            // the next slot: claimed now and published after the column (or
-            // group); in CLAIM_SERPENTINE_TAIL after a column only once it is
-            // walked (kDeferred), so that the counters hand the remaining slots
-            // to the workgroups that are free
-            if (tid == 0) next = a.claim_mode == CLAIM_SERPENTINE_TAIL && !group_item ? kDeferred : claim();
         }
         // kind < 0: an empty slot, or a block of a group whose column is long
         // (an item of its own)
@@ -1334,10 +1310,7 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
         }
         }  // kind >= 0
         if (grp_kb >= grp_end) {
-            if (tid == 0) {
-                if (next == kDeferred) next = claim();
-                sItem[(ci + 1) & 1] = next;
-            }
+            if (tid == 0) sItem[(ci + 1) & 1] = next;
             ++ci;
         }
         // the ring is free again and the next claim is visible to every wave
@@ -1454,17 +1427,13 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, const void* q, const void* k, cons
         // column lengths change smoothly (strided: a band and a stride's worth
         // of rows per column) or columns are a few blocks long; serpentine per
         // head where long summary columns alternate with short ones (fixed) and
-        // each head has a few workgroups (its first round in place order and
-        // the rest from one counter per head where there are at most 8
-        // heads); the queues otherwise
+        // each head has a few workgroups; the queues otherwise
         const int64_t bh_count = (int64_t)a.batch * a.heads;
         ak.claim_mode = a.walk == WALK_DENSE && qgrid % kQueues == 0 && bh_count % kQueues == 0
                             ? CLAIM_XCD_SERPENTINE
                         : (PAT == STRIDED || a.nq <= 8)
                             ? CLAIM_ROUND_ROBIN
-                            : (bh_count * 4 <= (int64_t)qgrid
-                                   ? (bh_count <= kQueues ? CLAIM_SERPENTINE_TAIL : CLAIM_SERPENTINE)
-                                   : CLAIM_QUEUES);
+                            : (bh_count * 4 <= (int64_t)qgrid ? CLAIM_SERPENTINE : CLAIM_QUEUES);
         // Summary halves in pairs (fixed, B = 64, l a multiple of 64: n / l of
         // them per (batch, head)) only where each workgroup of a head gets at
         // least 2.5 of them on average: a pair's column takes one workgroup

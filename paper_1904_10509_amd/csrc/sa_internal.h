@@ -50,7 +50,7 @@ inline hipError_t with_pattern_mode(int pattern, int mode, F&& f) {
 }
 
 // Orders in which the dK / dV kernel takes its work.
-enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2, CLAIM_XCD_SERPENTINE = 3, CLAIM_SERPENTINE_TAIL = 4 };
+enum { CLAIM_QUEUES = 0, CLAIM_ROUND_ROBIN = 1, CLAIM_SERPENTINE = 2, CLAIM_XCD_SERPENTINE = 3 };
 
 // Which blocks a kernel walks:
 //   WALK_LAYOUT  the present blocks of the layout;
