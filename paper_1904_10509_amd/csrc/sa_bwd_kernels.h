@@ -805,7 +805,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
     //   CLAIM_SERPENTINE: workgroup w serves head w mod (batch heads) alone and
     //     takes that head's ranks in serpentine order over the J workgroups of
     //     the head (j, 2J - 1 - j, 2J + j, ...), which evens out the sums of
-    //     sorted column lengths, with no atomics;
+    //     sorted column lengths, with no atomics; after the first round the
+    //     first J / 16 places drop out of the serpentine (below);
     //   CLAIM_XCD_SERPENTINE: workgroup w (on XCD x = w mod 8, the j-th of
     //     its J there) serves the heads bh = x (mod 8), head by head with
     //     every column of a head, longest first, before the next: places
@@ -854,7 +855,19 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const uint64_t j = blockIdx.x / (uint64_t)bh_count;
             const uint64_t J = (gridDim.x - bh + bh_count - 1) / bh_count;  // workgroups of this head
             const uint64_t k = sweep++;
-            const uint64_t rank = k * J + ((k & 1) ? J - 1 - j : j);
+            // The first sixteenth of the places (the head's longest columns)
+            // take nothing after their first: with long summary columns the
+            // longest chain is the first place's column plus what follows it,
+            // and the later rounds serpentine over the other places.  (More
+            // places left out, an eighth or a quarter, crowded the short
+            // columns into fewer workgroups and fetched more.)
+            uint64_t rank = j;
+            if (k > 0) {
+                const uint64_t S = J / 16;
+                if (j < S) return kNoWork;
+                const uint64_t J2 = J - S, j2 = j - S, kk = k - 1;
+                rank = J + kk * J2 + ((kk & 1) ? j2 : J2 - 1 - j2);
+            }
             return rank < per_layout ? encode(rank, bh) | ((k & 1) ? kAscend : 0ull) : kNoWork;
         }
         while (q_left > 0) {
