@@ -960,8 +960,18 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
             const int j = key_of(kbw);
 #pragma unroll
             for (int ks = 0; ks < C::KS; ++ks) {
-                kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
-                vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                // In the fixed pattern these rows are read once, and kept out
+                // of L2 they leave it to the Q / dO tiles the walks share (510 ->
+                // 499 MiB fetched per launch at n = 65,536, the same time); the
+                // strided band reads them just after the dQ kernel did and
+                // takes them from the caches (non-temporal: 2-4% slower).
+                if constexpr (PAT == FIXED) {
+                    kf[kbw][ks] = ld_bf16x8_once(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                    vf[kbw][ks] = ld_bf16x8_once(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                } else {
+                    kf[kbw][ks] = ld_bf16x8(k + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                    vf[kbw][ks] = ld_bf16x8(v + base + (int64_t)j * a.ss + ks * 32 + 8 * g);
+                }
             }
             cl[kbw] = col_lane(j, a.dl, a.c, mp.w);
         }

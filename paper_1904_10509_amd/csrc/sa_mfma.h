@@ -38,6 +38,12 @@ __device__ inline bf16x8 ld_bf16x8(const uint16_t* p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
 }
 
+// The same from global memory with a non-temporal load, for data read once
+// that should not displace lines other workgroups still share.
+__device__ inline bf16x8 ld_bf16x8_once(const uint16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
+}
+
 // Round-to-nearest-even fp32 -> bf16 of two D results, as one operand.
 __device__ inline bf16x8 pack_bf16x8(f32x4 lo, f32x4 hi) {
     bf16x4 a = __builtin_convertvector(lo, bf16x4);
