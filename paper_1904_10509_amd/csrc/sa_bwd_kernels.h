@@ -1327,17 +1327,8 @@ bwd_dkdv_bf16_kernel(AttnArgs a, const int32_t* __restrict__ col_ptr, const int3
                     xv += bf16x4_to_f32x4(*dvp);
                     xk += bf16x4_to_f32x4(*dkp);
                 }
-                // fixed pattern: stored non-temporal, out of the way of the Q /
-                // dO tiles the walks share (498 -> 488 MiB fetched per launch
-                // at n = 65,536); the strided band's results are read back by
-                // the residue classes' kernel right after
-                if constexpr (PAT == FIXED) {
-                    store_once(dvp, pack_bf16x4_bits(xv));
-                    store_once(dkp, pack_bf16x4_bits(xk));
-                } else {
-                    *dvp = pack_bf16x4_bits(xv);
-                    *dkp = pack_bf16x4_bits(xk);
-                }
+                *dvp = pack_bf16x4_bits(xv);
+                *dkp = pack_bf16x4_bits(xk);
             }
         }
         }  // kind >= 0

@@ -70,12 +70,6 @@ __device__ inline uint2 pack_bf16x4_bits(f32x4 v) {
     return __builtin_bit_cast(uint2, a);
 }
 
-// An 8-byte store to global memory marked non-temporal: for results written
-// once and not read again by the kernels that follow.
-__device__ inline void store_once(uint2* p, uint2 v) {
-    __builtin_nontemporal_store(__builtin_bit_cast(u32x2, v), reinterpret_cast<u32x2*>(p));
-}
-
 // Four bf16 (8 bytes) to fp32, exactly.
 __device__ inline f32x4 bf16x4_to_f32x4(uint2 u) {
     return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
