@@ -187,6 +187,9 @@ int sparse_attn_bwd_workspace_size(int64_t n, int32_t block, int32_t stride_l,
  * sparse_attn_bwd_workspace_size bytes (SA_ERR_BUFFER_TOO_SMALL otherwise);
  * its contents on entry are ignored, and calls that share one workspace
  * must not overlap (it holds per-call row statistics and a work counter).
+ * Repeated calls with the same arguments on one device give the same bits;
+ * the order in which dK and dV sum their terms follows the device's number
+ * of compute units, so devices of another size can differ in the last bit.
  */
 int sparse_attn_bwd(int64_t n, int32_t block, int32_t stride_l, int32_t summary_c,
                     int32_t pattern, int32_t head_mode, const int32_t* row_ptr,
