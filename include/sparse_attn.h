@@ -61,7 +61,7 @@ extern "C" {
 typedef enum {
     SA_OK = 0,
     SA_ERR_INVALID = -1,          /* an argument is out of range or NULL */
-    SA_ERR_UNSUPPORTED = -2,      /* valid request this build does not implement */
+    SA_ERR_UNSUPPORTED = -2,      /* valid request the library does not implement */
     SA_ERR_BUFFER_TOO_SMALL = -3, /* a caller buffer is smaller than required */
     SA_ERR_HIP = -4               /* the HIP runtime reported an error */
 } sa_status;
